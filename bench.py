@@ -1,0 +1,210 @@
+"""Benchmark of the ARCHead packed LM-head forward on one MI355X.
+
+Workload (N=1): the Qwen3-8B-shaped packed head (V=151936, d=4096, INT4
+residual in groups of 128 with fp16 scales, core rank 64, correction rank 32,
+INT8 factors), synthetic seeded inputs.  A step is one forward of the whole
+hot path (stage-1 projections, head-streaming kernel with the fused rank-r
+expansion, logit store) for one decode token (M=1), with every input already
+resident in HBM.  The step rotates over three copies of the packed head
+(3 x 336 MB > the 256 MB Infinity Cache), so each step streams its head from
+HBM.  The headline value is decode GB/s over the packed bytes.  Secondary
+lines: decode M=4 and M=16, and the M=4096 prefill fused-CE pass (tok/s).
+
+Prints one JSON line (rank 0, N=1).  --gpus N > 1 is refused: this build
+runs on one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "ARCHead head fwd: decode HBM GB/s (% peak) + prefill tok/s, V=151936 d=4096"
+PEAK_HBM_GBS = 8000.0
+N_COPIES = 3
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def upload_copies(h, n):
+    import torch
+    from paper_2608_02703_amd import PackedHead
+    base = PackedHead.from_arrays(h)
+    heads = [base]
+    for _ in range(n - 1):
+        bufs = {k: (None if v is None else v.clone()) for k, v in base.buffers.items()}
+        heads.append(PackedHead(h.V, h.d, h.g, h.rc, h.rr, bufs, h.gV, h.gB))
+    torch.cuda.synchronize()
+    return heads
+
+
+def gemv_algorithmic_bytes(h, M):
+    """Bytes the head-streaming kernel must move once: residual codes and
+    scales, the vocabulary-side factors and their scales, x, t and the fp32
+    logits it writes."""
+    R = h.rc + h.rr
+    return (h.V * h.d // 2 + h.V * (h.d // h.g) * 2 + h.V * (h.rc + h.rr) +
+            (2 * h.V if h.rc else 0) + (2 * h.V if h.rr else 0) +
+            M * h.d * 2 + M * R * 4 + M * h.V * 4)
+
+
+def time_decode(heads, x, steps, warmup, ws=None):
+    """(ms per step, mean head-kernel ms) for `steps` logits calls."""
+    import torch
+    M = x.shape[0]
+    outs = [torch.empty((M, heads[0].V), device="cuda") for _ in heads]
+    wss = [hd.workspace(M, 0, x.device) for hd in heads]
+    for i in range(warmup):
+        k = i % len(heads)
+        heads[k].logits(x, out=outs[k], ws=wss[k])
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:        # create the underlying HIP events
+        a.record()
+        b.record()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t0.record()
+    for i in range(steps):
+        k = i % len(heads)
+        heads[k].set_timing_events(*ev[i])
+        heads[k].logits(x, out=outs[k], ws=wss[k])
+    t1.record()
+    torch.cuda.synchronize()
+    for hd in heads:
+        hd.set_timing_events(None, None)
+    total = t0.elapsed_time(t1)
+    kern = [a.elapsed_time(b) for a, b in ev]
+    return total / steps, float(np.mean(kern)), float(np.median(kern))
+
+
+def time_prefill(heads, x, y, steps, warmup):
+    import torch
+    M = x.shape[0]
+    ws = [hd.workspace(M, 1, x.device) for hd in heads]
+    for i in range(warmup):
+        heads[i % len(heads)].logits_ce(x, y, ws=ws[i % len(heads)])
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        ce, mean = heads[i % len(heads)].logits_ce(x, y, ws=ws[i % len(heads)])
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps, float(mean.cpu()[0])
+
+
+def cpu_baseline(h, xb, budget_s):
+    """The fp64 oracle on the host cores: full head, one token (M=1)."""
+    from oracle import head as ohead
+    from oracle.bytes import head_bytes
+    t = time.perf_counter()
+    ohead.logits(h, xb[:1])
+    sec = time.perf_counter() - t
+    cores = len(os.sched_getaffinity(0))
+    threads = int(os.environ.get("OMP_NUM_THREADS", cores))
+    return {"value": head_bytes(h) / sec / 1e9, "unit": "GB/s", "cores": min(cores, threads),
+            "kind": "oracle",
+            "sample": f"fp64 numpy oracle, full Qwen-shaped head, 1 token: {sec:.2f} s "
+                      f"({1 / sec:.3f} tok/s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--prefill-steps", type=int, default=3)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-prefill", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py: this build runs on one GPU only; multi-GPU (vocab-parallel) "
+              "runs are not part of it", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from oracle.bytes import head_bytes
+    from synth import CONFIGS, make_head, make_targets, make_x
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    cfg = "qwen_decode"
+    log("generating the packed head ...")
+    h = make_head(cfg)
+    pbytes = head_bytes(h)
+    heads = upload_copies(h, N_COPIES)
+    xb = make_x(cfg, 16)
+    x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+
+    res = {}
+    for M in (1, 4, 16):
+        x = x_all[:M]
+        ms, kern_ms, kern_med = time_decode(heads, x, args.steps if M == 1 else
+                                            max(20, args.steps // 4), args.warmup)
+        res[M] = (ms, kern_ms, kern_med)
+        log(f"decode M={M}: {ms * 1e3:.1f} us/step, head kernel {kern_ms * 1e3:.1f} us "
+            f"(median {kern_med * 1e3:.1f}), {pbytes / ms / 1e6:.0f} GB/s over packed bytes")
+
+    prefill = None
+    if not args.no_prefill:
+        pc = CONFIGS["qwen_prefill"]
+        Mp = pc["Ms"][0]
+        xp = torch.from_numpy(make_x("qwen_prefill", Mp).view(np.int16)).view(
+            torch.bfloat16).cuda()
+        yp = torch.from_numpy(make_targets("qwen_prefill", Mp)).cuda()
+        ms_p, mean_ce = time_prefill(heads, xp, yp, args.prefill_steps, 1)
+        prefill = {"M": Mp, "ms_per_step": ms_p, "tok_s": Mp / ms_p * 1e3,
+                   "mean_ce": mean_ce}
+        log(f"prefill CE M={Mp}: {ms_p:.2f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s")
+
+    ms1, kern1, _ = res[1]
+    value = pbytes / ms1 / 1e6          # GB/s
+    alg = gemv_algorithmic_bytes(h, 1)
+    achieved = alg / kern1 / 1e6
+    out = {
+        "metric": METRIC,
+        "value": round(value, 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms1, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "qwen3-8b-shaped packed head decode, M=1",
+                   "V": h.V, "d": h.d, "g": h.g, "r_c": h.rc, "r_r": h.rr,
+                   "packed_bytes": pbytes, "head_copies_rotated": N_COPIES,
+                   "parallelism": "none (1 GPU)"},
+        "pct_peak_hbm": round(100 * value / PEAK_HBM_GBS, 2),
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                     "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                     "traffic": None, "kernel": "k_gemv<1,64,false>",
+                     "kernel_us": round(kern1 * 1e3, 2), "algorithmic_bytes": alg},
+        "decode": {str(M): {"us_per_step": round(v[0] * 1e3, 2),
+                            "kernel_us": round(v[1] * 1e3, 2),
+                            "gbs_packed": round(pbytes / v[0] / 1e6, 1)}
+                   for M, v in res.items()},
+        "prefill": prefill,
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle (1 token, full head) ...")
+        out["cpu_baseline"] = cpu_baseline(h, xb, 30)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

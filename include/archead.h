@@ -1,0 +1,230 @@
+/*
+ * archead.h -- C ABI of the ARCHead packed LM-head forward for AMD Instinct
+ * MI355X (gfx950).
+ *
+ * The packed head (ARCHead, arXiv 2608.02703, Section 3.2 and the appendix
+ * table "Logical contents of the packed ARCHead state dictionary") holds
+ *
+ *   W_d   = Q5(A_c) Q8(B_c) + Q_SC4(W - A_c B_c)   quantized core
+ *   W_hat = W_d + A_w B_w                          core plus correction
+ *
+ * and the forward (Section 3.2, inference equation; appendix "Expanded
+ * Construction Procedure") is Y_hat = H W_d^T + (H B_w^T) A_w^T.  In the
+ * names of this library's buffers, for a token x (bf16 [d]) and vocabulary
+ * row v:
+ *
+ *   logit[v] = sum_j s_res[v,j] * sum_{i in group j} c[v,i] x[i]     residual
+ *            + s_U[v] * sum_k cU[v,k] * t_c[k]                       core
+ *            + s_A[v] * sum_k cA[v,k] * t_w[k]                       correction
+ *   t_c[k] = sum_i (s_V[k, i/g_v] cV[k,i]) x[i],
+ *   t_w[k] = sum_i (s_B[k, i/g_b] cB[k,i]) x[i]
+ *
+ * No dense head is ever formed: the residual is unpacked in registers and the
+ * two low-rank products are evaluated through t_c and t_w (the paper's
+ * bracketing H B_w^T first).  All arithmetic is fp32.
+ *
+ * Buffer layouts (all row-major, rows back to back, no padding):
+ *
+ *   res_codes     uint8   [V, d/2]     INT4 residual codes, ARCHEAD_INT4_V1
+ *   res_scales    fp16    [V, d/g]     residual group scales (groups of g
+ *                                      consecutive elements along d)
+ *   core_u        int8    [V, r_c]     core left codes (A_c side; any code
+ *                                      range that fits int8, e.g. 5-bit)
+ *   core_u_scale  fp16    [V]          per-row scales of core_u
+ *   core_v        int8    [r_c, d]     core right codes (B_c side)
+ *   core_v_scale  fp16    [r_c, d/g_v] group scales of core_v (g_v = d: one
+ *                                      scale per row)
+ *   corr_a        int8    [V, r_r]     correction left codes (A_w, row-wise)
+ *   corr_a_scale  fp16    [V]
+ *   corr_b        int8    [r_r, d]     correction right codes (B_w)
+ *   corr_b_scale  fp16    [r_r, d/g_b] group scales of corr_b
+ *
+ * ARCHEAD_INT4_V1: bytes 4w..4w+3 of a row, read as a little-endian 32-bit
+ * word q, hold elements 8w..8w+7 of that row.  Element 8w+2k (k = 0..3) is
+ * the nibble in bits [4k, 4k+4) of q, element 8w+2k+1 the nibble in bits
+ * [16+4k, 20+4k).  A nibble u stores the signed code c = u - 8 (c in
+ * [-8, 7]).  With this order, (q >> 4k) & 0x000F000F places elements
+ * (8w+2k, 8w+2k+1) in the two 16-bit halves of a register, ready to become
+ * a bf16 pair.
+ *
+ * Memory ownership: every device pointer is borrowed.  The caller allocates
+ * the head buffers, activations, outputs and the workspace, and keeps the
+ * head buffers alive and unchanged for the lifetime of the handle.  The
+ * library allocates no device memory.
+ *
+ * Errors: every call returns an archead_status; no C++ exception crosses the
+ * ABI.  Argument checks happen on the host before any launch.  A failed HIP
+ * launch returns ARCHEAD_E_HIP; archead_last_error() then gives a message
+ * (thread-local).  Kernel faults surface, as usual for HIP, at the caller's
+ * next synchronisation.  The compute calls are asynchronous on the given
+ * stream and never synchronise.
+ */
+#ifndef ARCHEAD_H_
+#define ARCHEAD_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ARCHEAD_ABI_VERSION 1u
+
+typedef enum archead_status {
+  ARCHEAD_OK = 0,
+  ARCHEAD_E_INVALID_ARG = 1, /* null pointer, bad shape, bad enum value     */
+  ARCHEAD_E_MISALIGNED = 2,  /* a pointer or stride breaks its alignment    */
+  ARCHEAD_E_UNSUPPORTED = 3, /* no gfx950 device, or a shape outside limits */
+  ARCHEAD_E_WORKSPACE = 4,   /* workspace smaller than archead_workspace_bytes */
+  ARCHEAD_E_HIP = 5          /* a HIP runtime call failed                   */
+} archead_status;
+
+typedef enum archead_dtype {
+  ARCHEAD_F32 = 0,
+  ARCHEAD_BF16 = 1,
+  ARCHEAD_F16 = 2,
+  ARCHEAD_I32 = 3,
+  ARCHEAD_I64 = 4,
+  ARCHEAD_I8 = 5
+} archead_dtype;
+
+typedef enum archead_int4_encoding { ARCHEAD_INT4_V1 = 1 } archead_int4_encoding;
+
+typedef enum archead_op {
+  ARCHEAD_OP_LOGITS = 0,    /* archead_logits    */
+  ARCHEAD_OP_LOGITS_CE = 1  /* archead_logits_ce */
+} archead_op;
+
+/* Shape and encoding of a packed head (the "integer shapes/groups" metadata
+ * of the paper's packed state dictionary).
+ *   0 < V < 2^31, 0 < d <= 16384, d % g == 0, g % 32 == 0;
+ *   r_c >= 0, r_r >= 0 (0 = component absent: r_c = r_r = 0 is plain group
+ *   INT4, r_r = 0 is the "core only" ablation);
+ *   g_v, g_b: group length along d of the core_v / corr_b scales, dividing d
+ *   and a multiple of 32 (d = one scale per row);
+ *   int4_encoding = ARCHEAD_INT4_V1, scale_dtype = ARCHEAD_F16,
+ *   factor_dtype = ARCHEAD_I8. */
+typedef struct archead_desc {
+  uint32_t abi_version; /* ARCHEAD_ABI_VERSION */
+  int64_t V, d, g;
+  int64_t r_c, r_r;
+  int64_t g_v, g_b;
+  int32_t int4_encoding;
+  int32_t scale_dtype;
+  int32_t factor_dtype;
+} archead_desc;
+
+/* Device pointers to the ten packed buffers (layouts above).  res_codes must
+ * be 16-byte aligned, fp16 buffers 2-byte aligned.  Pointers of an absent
+ * component (rank 0) may be NULL. */
+typedef struct archead_ptrs {
+  const void* res_codes;
+  const void* res_scales;
+  const void* core_u;
+  const void* core_u_scale;
+  const void* core_v;
+  const void* core_v_scale;
+  const void* corr_a;
+  const void* corr_a_scale;
+  const void* corr_b;
+  const void* corr_b_scale;
+} archead_ptrs;
+
+typedef struct archead_handle archead_handle;
+
+/* Check a descriptor on the host (no HIP call).  ARCHEAD_OK or
+ * ARCHEAD_E_INVALID_ARG / ARCHEAD_E_UNSUPPORTED with a message. */
+archead_status archead_validate_desc(const archead_desc* desc);
+
+/* Create a handle for the head described by desc whose buffers are at ptrs
+ * on the current HIP device.  The handle is host memory, immutable after
+ * creation apart from archead_set_gemv_max_m, and may be used from several
+ * threads and streams at once (each call with its own workspace).  Fails
+ * with ARCHEAD_E_UNSUPPORTED if the current device is not gfx950 or there is
+ * no device.  *out is set to NULL on failure. */
+archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs,
+                              archead_handle** out);
+
+/* Release a handle (NULL is a no-op).  Does not touch the borrowed buffers;
+ * the caller must make sure no call using the handle is still queued on a
+ * stream whose completion it has not awaited. */
+void archead_destroy(archead_handle* h);
+
+/* Bytes of workspace the call `op` needs for M tokens (0 for M == 0).  The
+ * workspace holds the low-rank projections t (fp32 [M, r_c + r_r]), the
+ * per-group sums of x and, for the CE call, the per-vocabulary-tile softmax
+ * partials.  Returns 0 for a NULL handle or M < 0. */
+size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op);
+
+/* logits[m, v] for m < M, v < V.
+ *   x        bf16 [M, ldx] device, 16-byte aligned, ldx >= d, ldx % 8 == 0
+ *   out      [M, ldo] device, out_dtype ARCHEAD_F32 (4-byte aligned) or
+ *            ARCHEAD_BF16 (2-byte aligned, fp32 result rounded to nearest
+ *            even), ldo >= V
+ *   ws       device workspace of ws_bytes >= archead_workspace_bytes(h, M,
+ *            ARCHEAD_OP_LOGITS), 256-byte aligned; its contents on entry do
+ *            not matter
+ *   stream   hipStream_t to launch on (NULL = the default stream)
+ * M == 0 returns ARCHEAD_OK without launching.  The kernels read the head
+ * once per call whatever M is (decode GEMV for small M, tiled bf16 MFMA for
+ * large M). */
+archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
+                              int64_t ldx, void* out, archead_dtype out_dtype,
+                              int64_t ldo, void* ws, size_t ws_bytes,
+                              void* stream);
+
+/* Fused log-softmax and cross-entropy: ce[m] = logsumexp_v(logit[m, :]) -
+ * logit[m, y_m] (natural log), and *mean_ce = (1/M) sum_m ce[m] when
+ * mean_ce is not NULL.  This is the paper's CE / perplexity evaluation
+ * (Section 4, "Data and metrics"; PPL = exp(mean CE)).  The [M, V] logits are
+ * never written to memory: each vocabulary tile leaves a (max, sum of exp)
+ * pair per token in the workspace and a merge kernel combines them in a fixed
+ * order, so results are bitwise reproducible.
+ *   targets  device int32 or int64 [M] (tgt_dtype ARCHEAD_I32 / ARCHEAD_I64)
+ *   ce       device fp32 [M];  mean_ce  device fp32 scalar or NULL
+ * A target outside [0, V) gives ce[m] = NaN (and a NaN mean); this is
+ * detected on the device, the host does not synchronise. */
+archead_status archead_logits_ce(const archead_handle* h, const void* x,
+                                 int64_t M, int64_t ldx, const void* targets,
+                                 archead_dtype tgt_dtype, float* ce,
+                                 float* mean_ce, void* ws, size_t ws_bytes,
+                                 void* stream);
+
+/* Largest M served by the decode GEMV kernel; larger M use the MFMA kernel.
+ * -1 restores the built-in threshold.  Not thread-safe with concurrent calls
+ * on the same handle (set it once, after create). */
+archead_status archead_set_gemv_max_m(archead_handle* h, int64_t m);
+int64_t archead_get_gemv_max_m(const archead_handle* h);
+
+/* Profiling hook: when start and stop are non-NULL hipEvent_t handles
+ * (created by the caller on the handle's device), every later compute call
+ * records `start` on its stream immediately before the launch of the kernel
+ * that streams the packed head and `stop` immediately after it (around all
+ * of its launches when M needs several), so the caller can time that kernel
+ * alone.  NULL, NULL turns it off.  Same threading rule as
+ * archead_set_gemv_max_m. */
+archead_status archead_set_timing_events(archead_handle* h, void* start, void* stop);
+
+/* Persistent bytes of the packed head: the sum over its buffers of element
+ * count times element size (the paper's bytes(ARCHead), Section 3.3).
+ * 0 for an invalid descriptor. */
+uint64_t archead_packed_bytes(const archead_desc* desc);
+
+/* Host-side INT4 packing to / from ARCHEAD_INT4_V1 (no HIP call).
+ * codes: int8 [rows, d] with values in [-8, 7]; packed: uint8 [rows, d/2];
+ * d % 8 == 0.  pack returns ARCHEAD_E_INVALID_ARG for a code out of range. */
+archead_status archead_pack_int4(const int8_t* codes, int64_t rows, int64_t d,
+                                 uint8_t* packed);
+archead_status archead_unpack_int4(const uint8_t* packed, int64_t rows, int64_t d,
+                                   int8_t* codes);
+
+const char* archead_status_str(archead_status s);
+/* Message of the last failing call on this thread ("" if none). */
+const char* archead_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ARCHEAD_H_ */

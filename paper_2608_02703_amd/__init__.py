@@ -1,0 +1,16 @@
+"""ARCHead packed LM-head forward for AMD Instinct MI355X (gfx950).
+
+The compute path is the C-ABI library libarchead.so (hand-written HIP
+kernels); ``archead`` is its thin ctypes binding, with PyTorch providing
+device memory and streams only.
+"""
+from .archead import (  # noqa: F401
+    ArcheadError,
+    Desc,
+    PackedHead,
+    lib,
+    pack_int4,
+    packed_bytes,
+    unpack_int4,
+    validate_desc,
+)

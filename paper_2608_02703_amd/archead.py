@@ -1,0 +1,269 @@
+"""ctypes binding of libarchead.so (argument marshalling only).
+
+Every step of the forward runs in the library's HIP kernels; this module only
+turns torch tensors into pointers, sizes and the caller's stream.  It fails
+loudly when the library has not been built: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libarchead.so")
+HOST_LIB_PATH = os.path.join(_PKG, "libarchead_host.so")
+
+ABI_VERSION = 1
+OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
+F32, BF16, F16, I32, I64, I8 = range(6)
+INT4_V1 = 1
+OP_LOGITS, OP_LOGITS_CE = 0, 1
+
+
+class ArcheadError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"archead status {status}: {msg}")
+        self.status = status
+
+
+class Desc(ctypes.Structure):
+    _fields_ = [("abi_version", ctypes.c_uint32), ("V", ctypes.c_int64),
+                ("d", ctypes.c_int64), ("g", ctypes.c_int64),
+                ("r_c", ctypes.c_int64), ("r_r", ctypes.c_int64),
+                ("g_v", ctypes.c_int64), ("g_b", ctypes.c_int64),
+                ("int4_encoding", ctypes.c_int32), ("scale_dtype", ctypes.c_int32),
+                ("factor_dtype", ctypes.c_int32)]
+
+    @classmethod
+    def make(cls, V, d, g, rc, rr, gV=None, gB=None, abi=ABI_VERSION,
+             enc=INT4_V1, scale_dtype=F16, factor_dtype=I8):
+        return cls(abi, V, d, g, rc, rr, d if gV is None else gV,
+                   d if gB is None else gB, enc, scale_dtype, factor_dtype)
+
+
+class Ptrs(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
+        "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale")]
+
+
+_SIGS = {
+    "archead_validate_desc": (ctypes.c_int, [ctypes.POINTER(Desc)]),
+    "archead_create": (ctypes.c_int, [ctypes.POINTER(Desc), ctypes.POINTER(Ptrs),
+                                      ctypes.POINTER(ctypes.c_void_p)]),
+    "archead_destroy": (None, [ctypes.c_void_p]),
+    "archead_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p, ctypes.c_int64,
+                                                  ctypes.c_int]),
+    "archead_logits": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                      ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
+                                      ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t,
+                                      ctypes.c_void_p]),
+    "archead_logits_ce": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                         ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
+                                         ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_set_gemv_max_m": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64]),
+    "archead_get_gemv_max_m": (ctypes.c_int64, [ctypes.c_void_p]),
+    "archead_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p,
+                                                 ctypes.c_void_p]),
+    "archead_packed_bytes": (ctypes.c_uint64, [ctypes.POINTER(Desc)]),
+    "archead_pack_int4": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                         ctypes.c_void_p]),
+    "archead_unpack_int4": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                           ctypes.c_void_p]),
+    "archead_status_str": (ctypes.c_char_p, [ctypes.c_int]),
+    "archead_last_error": (ctypes.c_char_p, []),
+}
+
+HOST_SYMBOLS = ("archead_validate_desc", "archead_set_gemv_max_m", "archead_set_timing_events",
+                "archead_get_gemv_max_m", "archead_packed_bytes", "archead_pack_int4",
+                "archead_unpack_int4", "archead_status_str", "archead_last_error")
+
+_libs = {}
+
+
+def _load(path: str, names) -> ctypes.CDLL:
+    if path in _libs:
+        return _libs[path]
+    if not os.path.exists(path):
+        raise RuntimeError(
+            f"{os.path.basename(path)} is not built; run "
+            "`python -m paper_2608_02703_amd.build` (or __graft_entry__.build())")
+    h = ctypes.CDLL(path)
+    for n in names:
+        res, args = _SIGS[n]
+        f = getattr(h, n)
+        f.restype = res
+        f.argtypes = args
+    _libs[path] = h
+    return h
+
+
+def lib() -> ctypes.CDLL:
+    """The HIP library (all entry points)."""
+    return _load(LIB_PATH, list(_SIGS))
+
+
+def host_lib(path: Optional[str] = None) -> ctypes.CDLL:
+    """A host-only build of the argument checks and packers (g++)."""
+    return _load(path or HOST_LIB_PATH, HOST_SYMBOLS)
+
+
+def _check(st: int, L=None):
+    if st != OK:
+        L = L or lib()
+        raise ArcheadError(st, L.archead_last_error().decode())
+
+
+def validate_desc(desc: Desc, L=None) -> int:
+    L = L or lib()
+    return L.archead_validate_desc(ctypes.byref(desc))
+
+
+def packed_bytes(desc: Desc, L=None) -> int:
+    L = L or lib()
+    return int(L.archead_packed_bytes(ctypes.byref(desc)))
+
+
+def pack_int4(codes: np.ndarray, L=None) -> np.ndarray:
+    L = L or lib()
+    c = np.ascontiguousarray(codes, dtype=np.int8)
+    rows, d = c.shape
+    out = np.empty((rows, d // 2), dtype=np.uint8)
+    _check(L.archead_pack_int4(c.ctypes.data, rows, d, out.ctypes.data), L)
+    return out
+
+
+def unpack_int4(packed: np.ndarray, d: int, L=None) -> np.ndarray:
+    L = L or lib()
+    p = np.ascontiguousarray(packed, dtype=np.uint8)
+    rows = p.shape[0]
+    if p.shape[1] * 2 != d:
+        raise ValueError("packed row length must be d/2")
+    out = np.empty((rows, d), dtype=np.int8)
+    _check(L.archead_unpack_int4(p.ctypes.data, rows, d, out.ctypes.data), L)
+    return out
+
+
+def _ptr(t) -> int:
+    return 0 if t is None else int(t.data_ptr())
+
+
+class PackedHead:
+    """A packed head resident on the current GPU plus its library handle.
+
+    ``buffers`` maps the ten buffer names to torch tensors on the device (the
+    caller keeps ownership; the handle only borrows them)."""
+
+    BUFFERS = ("res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
+               "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale")
+
+    def __init__(self, V, d, g, rc, rr, buffers: dict, gV=None, gB=None):
+        import torch  # noqa: F401  (device memory only)
+        self.V, self.d, self.g, self.rc, self.rr = V, d, g, rc, rr
+        self.gV = d if gV is None else gV
+        self.gB = d if gB is None else gB
+        self.buffers = buffers
+        self.desc = Desc.make(V, d, g, rc, rr, self.gV, self.gB)
+        self.ptrs = Ptrs(*[_ptr(buffers.get(n)) for n in self.BUFFERS])
+        self._lib = lib()
+        h = ctypes.c_void_p()
+        _check(self._lib.archead_create(ctypes.byref(self.desc), ctypes.byref(self.ptrs),
+                                        ctypes.byref(h)), self._lib)
+        self.handle = h
+        self._ws = {}
+
+    @classmethod
+    def from_arrays(cls, h, device="cuda"):
+        """Upload a head given as numpy arrays (the attributes of
+        synth.HeadArrays) to ``device``."""
+        import torch
+        bufs = {}
+        for n in cls.BUFFERS:
+            a = np.ascontiguousarray(getattr(h, n))
+            if a.size == 0:
+                bufs[n] = None
+                continue
+            if a.dtype == np.float16:
+                t = torch.from_numpy(a.view(np.int16)).view(torch.float16)
+            elif a.dtype == np.uint8:
+                t = torch.from_numpy(a)
+            else:
+                t = torch.from_numpy(a.astype(np.int8, copy=False))
+            bufs[n] = t.to(device)
+        return cls(h.V, h.d, h.g, h.rc, h.rr, bufs, getattr(h, "gV", None),
+                   getattr(h, "gB", None))
+
+    def close(self):
+        if getattr(self, "handle", None):
+            self._lib.archead_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    # ------------------------------------------------------------------
+    def set_gemv_max_m(self, m: int):
+        _check(self._lib.archead_set_gemv_max_m(self.handle, m), self._lib)
+
+    def set_timing_events(self, start, stop):
+        """start / stop: torch.cuda.Event objects already recorded once (so
+        their HIP events exist), or None to switch timing off."""
+        p0 = ctypes.c_void_p(start.cuda_event) if start is not None else None
+        p1 = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
+        _check(self._lib.archead_set_timing_events(self.handle, p0, p1), self._lib)
+
+    def workspace_bytes(self, M: int, op: int = OP_LOGITS) -> int:
+        return int(self._lib.archead_workspace_bytes(self.handle, M, op))
+
+    def workspace(self, M: int, op: int, device):
+        import torch
+        n = self.workspace_bytes(M, op)
+        key = (str(device), n)
+        ws = self._ws.get(key)
+        if ws is None:
+            ws = torch.empty(max(n, 256), dtype=torch.uint8, device=device)
+            self._ws = {key: ws}
+        return ws
+
+    @staticmethod
+    def _stream(device):
+        import torch
+        return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+    def logits(self, x, out=None, out_dtype=None, ws=None):
+        """x: torch.bfloat16 [M, d] (row stride may exceed d) on the GPU."""
+        import torch
+        if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+            raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+        M = x.shape[0]
+        if out is None:
+            out = torch.empty((M, self.V), dtype=out_dtype or torch.float32,
+                              device=x.device)
+        code = {torch.float32: F32, torch.bfloat16: BF16}[out.dtype]
+        ws = self.workspace(M, OP_LOGITS, x.device) if ws is None else ws
+        _check(self._lib.archead_logits(
+            self.handle, _ptr(x), M, x.stride(0), _ptr(out), code, out.stride(0),
+            _ptr(ws), ws.numel(), self._stream(x.device)), self._lib)
+        return out
+
+    def logits_ce(self, x, targets, ce=None, mean=None, ws=None):
+        """Fused log-softmax + cross-entropy; returns (ce [M], mean [1])."""
+        import torch
+        if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+            raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+        M = x.shape[0]
+        code = {torch.int32: I32, torch.int64: I64}[targets.dtype]
+        ce = torch.empty(M, dtype=torch.float32, device=x.device) if ce is None else ce
+        mean = torch.empty(1, dtype=torch.float32, device=x.device) if mean is None else mean
+        ws = self.workspace(M, OP_LOGITS_CE, x.device) if ws is None else ws
+        _check(self._lib.archead_logits_ce(
+            self.handle, _ptr(x), M, x.stride(0), _ptr(targets), code, _ptr(ce),
+            _ptr(mean), _ptr(ws), ws.numel(), self._stream(x.device)), self._lib)
+        return ce, mean

@@ -1,0 +1,162 @@
+// Host-only part of the ARCHead C ABI: descriptor checks, byte accounting,
+// INT4 packing and error reporting.  No HIP calls, so it also builds with a
+// plain C++ compiler for the CPU tests.
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include "internal.h"
+
+namespace archead {
+
+static thread_local char g_err[512];
+
+archead_status fail(archead_status s, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
+  va_end(ap);
+  return s;
+}
+
+void clear_error() { g_err[0] = 0; }
+
+int lanes_per_row(int64_t d) {
+  int64_t chunks = d / 32;
+  int lpr = 64;
+  while (lpr > 1 && chunks % lpr) lpr >>= 1;
+  return lpr;
+}
+
+bool use_gemv(const archead_handle* h, int64_t M) {
+  return M <= h->gemv_max_m.load(std::memory_order_relaxed);
+}
+
+}  // namespace archead
+
+using namespace archead;
+
+extern "C" {
+
+const char* archead_status_str(archead_status s) {
+  switch (s) {
+    case ARCHEAD_OK: return "ok";
+    case ARCHEAD_E_INVALID_ARG: return "invalid argument";
+    case ARCHEAD_E_MISALIGNED: return "misaligned pointer or stride";
+    case ARCHEAD_E_UNSUPPORTED: return "unsupported device or shape";
+    case ARCHEAD_E_WORKSPACE: return "workspace too small";
+    case ARCHEAD_E_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+const char* archead_last_error(void) { return archead::g_err; }
+
+archead_status archead_validate_desc(const archead_desc* p) {
+  if (!p) return fail(ARCHEAD_E_INVALID_ARG, "desc is NULL");
+  const archead_desc& d = *p;
+  if (d.abi_version != ARCHEAD_ABI_VERSION)
+    return fail(ARCHEAD_E_INVALID_ARG, "abi_version %u, library is %u",
+                d.abi_version, ARCHEAD_ABI_VERSION);
+  if (d.V <= 0 || d.d <= 0 || d.g <= 0)
+    return fail(ARCHEAD_E_INVALID_ARG, "V, d and g must be positive");
+  if (d.V > (int64_t(1) << 31) - 1 || d.d > 16384)
+    return fail(ARCHEAD_E_UNSUPPORTED, "V must be < 2^31 and d <= 16384");
+  if (d.g % 32) return fail(ARCHEAD_E_INVALID_ARG, "g = %lld is not a multiple of 32", (long long)d.g);
+  if (d.d % d.g) return fail(ARCHEAD_E_INVALID_ARG, "g = %lld does not divide d = %lld", (long long)d.g, (long long)d.d);
+  if (d.r_c < 0 || d.r_r < 0) return fail(ARCHEAD_E_INVALID_ARG, "ranks must be >= 0");
+  if (d.r_c + d.r_r > 1024) return fail(ARCHEAD_E_UNSUPPORTED, "r_c + r_r must be <= 1024");
+  const int64_t gs[2] = {d.g_v, d.g_b};
+  const int64_t rk[2] = {d.r_c, d.r_r};
+  for (int i = 0; i < 2; ++i) {
+    if (rk[i] == 0) continue;
+    if (gs[i] <= 0 || gs[i] % 32 || d.d % gs[i])
+      return fail(ARCHEAD_E_INVALID_ARG, "%s = %lld must divide d and be a multiple of 32",
+                  i ? "g_b" : "g_v", (long long)gs[i]);
+  }
+  if (d.int4_encoding != ARCHEAD_INT4_V1)
+    return fail(ARCHEAD_E_INVALID_ARG, "unknown int4_encoding %d", d.int4_encoding);
+  if (d.scale_dtype != ARCHEAD_F16)
+    return fail(ARCHEAD_E_UNSUPPORTED, "scale_dtype must be ARCHEAD_F16");
+  if (d.factor_dtype != ARCHEAD_I8)
+    return fail(ARCHEAD_E_UNSUPPORTED, "factor_dtype must be ARCHEAD_I8");
+  return ARCHEAD_OK;
+}
+
+uint64_t archead_packed_bytes(const archead_desc* p) {
+  if (archead_validate_desc(p) != ARCHEAD_OK) return 0;
+  const archead_desc& d = *p;
+  const uint64_t V = d.V, D = d.d;
+  uint64_t b = V * D / 2 + V * (D / d.g) * 2;                 // residual codes + scales
+  if (d.r_c) b += V * d.r_c + V * 2 + d.r_c * D + d.r_c * (D / d.g_v) * 2;
+  if (d.r_r) b += V * d.r_r + V * 2 + d.r_r * D + d.r_r * (D / d.g_b) * 2;
+  return b;
+}
+
+archead_status archead_pack_int4(const int8_t* codes, int64_t rows, int64_t d,
+                                 uint8_t* packed) {
+  if (!codes || !packed || rows < 0 || d <= 0 || d % 8)
+    return fail(ARCHEAD_E_INVALID_ARG, "pack_int4: bad pointers or shape (d %% 8 == 0)");
+  for (int64_t r = 0; r < rows; ++r) {
+    const int8_t* c = codes + r * d;
+    uint8_t* o = packed + r * (d / 2);
+    for (int64_t w = 0; w < d / 8; ++w) {
+      uint32_t q = 0;
+      for (int k = 0; k < 8; ++k) {
+        int v = c[8 * w + k];
+        if (v < -8 || v > 7)
+          return fail(ARCHEAD_E_INVALID_ARG, "pack_int4: code %d out of [-8, 7] at (%lld, %lld)",
+                      v, (long long)r, (long long)(8 * w + k));
+        // element 2j -> bits [4j, 4j+4), element 2j+1 -> bits [16+4j, 20+4j)
+        int shift = 4 * (k >> 1) + ((k & 1) ? 16 : 0);
+        q |= uint32_t(v + 8) << shift;
+      }
+      o[4 * w + 0] = uint8_t(q);
+      o[4 * w + 1] = uint8_t(q >> 8);
+      o[4 * w + 2] = uint8_t(q >> 16);
+      o[4 * w + 3] = uint8_t(q >> 24);
+    }
+  }
+  return ARCHEAD_OK;
+}
+
+archead_status archead_unpack_int4(const uint8_t* packed, int64_t rows, int64_t d,
+                                   int8_t* codes) {
+  if (!codes || !packed || rows < 0 || d <= 0 || d % 8)
+    return fail(ARCHEAD_E_INVALID_ARG, "unpack_int4: bad pointers or shape (d %% 8 == 0)");
+  for (int64_t r = 0; r < rows; ++r) {
+    const uint8_t* p = packed + r * (d / 2);
+    int8_t* c = codes + r * d;
+    for (int64_t w = 0; w < d / 8; ++w) {
+      uint32_t q = uint32_t(p[4 * w]) | uint32_t(p[4 * w + 1]) << 8 |
+                   uint32_t(p[4 * w + 2]) << 16 | uint32_t(p[4 * w + 3]) << 24;
+      for (int k = 0; k < 8; ++k) {
+        int shift = 4 * (k >> 1) + ((k & 1) ? 16 : 0);
+        c[8 * w + k] = int8_t(int((q >> shift) & 0xF) - 8);
+      }
+    }
+  }
+  return ARCHEAD_OK;
+}
+
+archead_status archead_set_gemv_max_m(archead_handle* h, int64_t m) {
+  if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
+  if (m < -1) return fail(ARCHEAD_E_INVALID_ARG, "gemv_max_m must be >= -1");
+  h->gemv_max_m.store(m == -1 ? kDefaultGemvMaxM : m);
+  return ARCHEAD_OK;
+}
+
+archead_status archead_set_timing_events(archead_handle* h, void* start, void* stop) {
+  if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
+  if ((start == nullptr) != (stop == nullptr))
+    return fail(ARCHEAD_E_INVALID_ARG, "start and stop must both be set or both be NULL");
+  h->ev_start.store(start);
+  h->ev_stop.store(stop);
+  return ARCHEAD_OK;
+}
+
+int64_t archead_get_gemv_max_m(const archead_handle* h) {
+  return h ? h->gemv_max_m.load() : -1;
+}
+
+}  // extern "C"

@@ -1,0 +1,54 @@
+// Host-side internals shared by the host translation unit and the HIP one.
+#pragma once
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <atomic>
+
+#include "archead.h"
+
+struct archead_handle {
+  archead_desc desc;
+  archead_ptrs ptrs;
+  int device;             // HIP device the buffers live on
+  int n_cu;               // compute units of that device
+  std::atomic<int64_t> gemv_max_m;
+  // persistent-grid sizes found with the occupancy API, keyed by kernel
+  // variant; 0 = not computed yet
+  std::atomic<int> grid_cache[64];
+  // caller-owned hipEvent_t pair recorded around the head-streaming kernel
+  std::atomic<void*> ev_start;
+  std::atomic<void*> ev_stop;
+};
+
+namespace archead {
+
+constexpr int64_t kDefaultGemvMaxM = 4;   // tokens per GEMV pass
+constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
+
+archead_status fail(archead_status s, const char* fmt, ...);
+void clear_error();
+
+// chunk = 32 consecutive INT4 codes = 16 bytes; lanes per row of the GEMV
+int lanes_per_row(int64_t d);
+
+// Workspace carve-up (byte offsets, each 256-aligned).
+struct WsLayout {
+  size_t t_off = 0;      // fp32 [M, r_c + r_r]
+  size_t xs_off = 0;     // fp32 [M, d/g] (MFMA path)
+  size_t part_off = 0;   // float2 [M, n_part] (CE)
+  size_t tgt_off = 0;    // fp32 [M] (CE)
+  size_t total = 0;
+  int64_t n_part = 0;
+};
+WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op);
+bool use_gemv(const archead_handle* h, int64_t M);
+
+// grid of the GEMV kernel: persistent workgroups, at most one per 8 rows
+int64_t gemv_grid(const archead_handle* h, int tok, bool ce);
+// rows handled by one MFMA workgroup tile
+constexpr int64_t kMfmaTileV = 128;
+constexpr int64_t kMfmaTileM = 128;
+
+}  // namespace archead

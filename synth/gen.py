@@ -33,7 +33,8 @@ CONFIGS = {
                  alpha=1.5, outliers=0, targets="uniform"),
     "qwen_decode": dict(cfg_id=2, V=151936, d=4096, g=128, rc=64, rr=32,
                         Ms=(1, 4, 16), alpha=1.5, outliers=0, targets="uniform"),
-    "qwen_prefill": dict(cfg_id=3, V=151936, d=4096, g=128, rc=64, rr=32,
+    # the prefill workload evaluates the same packed head as the decode one
+    "qwen_prefill": dict(cfg_id=3, head_cfg_id=2, V=151936, d=4096, g=128, rc=64, rr=32,
                          Ms=(4096,), alpha=1.5, outliers=0, targets="zipf",
                          zipf_s=1.1),
     "gemma": dict(cfg_id=4, V=262144, d=2560, g=128, rc=64, rr=32,
@@ -123,12 +124,16 @@ def make_head(cfg="tiny", draw: int = 0, **over) -> HeadArrays:
     """Draw a packed head.  ``over`` may replace V, d, g, rc, rr, gV, gB (for
     ragged and degenerate shapes); gV/gB default to d (one scale per row)."""
     c = _cfg(cfg)
-    c.update({k: v for k, v in over.items() if k in ("V", "d", "g", "rc", "rr",
-                                                        "gV", "gB", "cfg_id")})
+    unknown = set(over) - {"V", "d", "g", "rc", "rr", "gV", "gB", "cfg_id"}
+    if unknown:
+        raise TypeError(f"unknown head overrides {sorted(unknown)}")
+    c.update(over)
+    if "cfg_id" in over:
+        c.pop("head_cfg_id", None)
     V, d, g, rc, rr = c["V"], c["d"], c["g"], c["rc"], c["rr"]
     gV = c.get("gV", d)
     gB = c.get("gB", d)
-    cid = c["cfg_id"]
+    cid = c.get("head_cfg_id", c["cfg_id"])
     assert d % 2 == 0 and d % g == 0 and d % gV == 0 and d % gB == 0
     r = functools.partial(_rng, cid, draw=draw)
     res_codes = r("res_codes").integers(0, 256, size=(V, d // 2), dtype=np.uint8)

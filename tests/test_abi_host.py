@@ -1,0 +1,183 @@
+"""CPU tests of the C-ABI library: exports, argument checks, byte accounting
+and the host INT4 packer (checked against the oracle's own unpacker).  No
+compute call is made, so no GPU is needed."""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+from hypothesis import given, settings, strategies as st
+
+import oracle.bytes as obytes
+from oracle import layout
+from paper_2608_02703_amd import archead as ab
+from synth import CONFIGS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "archead.h")
+
+
+def _declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(archead_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def L():
+    return ab.lib()
+
+
+def test_library_exports_every_declared_symbol(L):
+    names = _declared_functions()
+    assert len(names) >= 12
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(ab._SIGS), "binding and header disagree"
+
+
+def test_status_strings(L):
+    for s in range(6):
+        assert L.archead_status_str(s)
+    assert L.archead_status_str(99) == b"unknown status"
+
+
+def _desc(**kw):
+    base = dict(V=1000, d=256, g=64, rc=8, rr=4)
+    base.update(kw)
+    extra = {k: base.pop(k) for k in ("gV", "gB", "abi", "enc", "scale_dtype",
+                                       "factor_dtype") if k in base}
+    return ab.Desc.make(base["V"], base["d"], base["g"], base["rc"], base["rr"],
+                        **extra)
+
+
+@pytest.mark.parametrize("kw,status", [
+    ({}, ab.OK),
+    (dict(abi=2), ab.E_INVALID_ARG),
+    (dict(V=0), ab.E_INVALID_ARG),
+    (dict(d=0), ab.E_INVALID_ARG),
+    (dict(g=48), ab.E_INVALID_ARG),            # not a multiple of 32
+    (dict(d=320, g=64, gV=64, gB=64), ab.OK),
+    (dict(d=288, g=64), ab.E_INVALID_ARG),     # g does not divide d
+    (dict(rc=-1), ab.E_INVALID_ARG),
+    (dict(gV=96), ab.E_INVALID_ARG),           # does not divide d
+    (dict(gB=16), ab.E_INVALID_ARG),           # not a multiple of 32
+    (dict(rc=0, gV=0), ab.OK),                 # absent component: group ignored
+    (dict(enc=2), ab.E_INVALID_ARG),
+    (dict(scale_dtype=ab.BF16), ab.E_UNSUPPORTED),
+    (dict(factor_dtype=ab.I32), ab.E_UNSUPPORTED),
+    (dict(rc=1000, rr=100), ab.E_UNSUPPORTED),
+    (dict(V=2 ** 31), ab.E_UNSUPPORTED),
+    (dict(d=32768, g=64), ab.E_UNSUPPORTED),
+])
+def test_validate_desc(L, kw, status):
+    st_ = ab.validate_desc(_desc(**kw), L)
+    assert st_ == status, L.archead_last_error()
+    if status != ab.OK:
+        assert L.archead_last_error()
+        assert ab.packed_bytes(_desc(**kw), L) == 0
+
+
+@pytest.mark.parametrize("name", sorted(CONFIGS))
+def test_packed_bytes_matches_oracle_on_configs(L, name):
+    c = CONFIGS[name]
+    d = ab.Desc.make(c["V"], c["d"], c["g"], c["rc"], c["rr"])
+    assert ab.packed_bytes(d, L) == obytes.packed_bytes(c["V"], c["d"], c["g"],
+                                                        c["rc"], c["rr"])
+
+
+@settings(max_examples=80, deadline=None)
+@given(st.integers(1, 300000), st.integers(1, 64), st.sampled_from([32, 64, 128]),
+       st.integers(0, 200), st.integers(0, 200), st.integers(1, 4), st.integers(1, 4))
+def test_packed_bytes_matches_oracle(V, dmul, g, rc, rr, fv, fb):
+    L = ab.lib()
+    d = g * dmul
+    gV = d // fv if (d // fv) % 32 == 0 and d % fv == 0 else d
+    gB = d // fb if (d // fb) % 32 == 0 and d % fb == 0 else d
+    desc = ab.Desc.make(V, d, g, rc, rr, gV, gB)
+    assert ab.packed_bytes(desc, L) == obytes.packed_bytes(V, d, g, rc, rr, gV, gB)
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.integers(1, 9), st.integers(1, 40), st.integers(0, 2 ** 32 - 1))
+def test_cpp_pack_matches_oracle_unpack(rows, words, seed):
+    L = ab.lib()
+    rng = np.random.default_rng(seed)
+    codes = rng.integers(-8, 8, size=(rows, 8 * words)).astype(np.int8)
+    packed = ab.pack_int4(codes, L)
+    assert np.array_equal(layout.unpack_int4(packed, 8 * words), codes)
+    raw = rng.integers(0, 256, size=(rows, 4 * words), dtype=np.uint8)
+    assert np.array_equal(ab.unpack_int4(raw, 8 * words, L),
+                          layout.unpack_int4(raw, 8 * words))
+
+
+def test_cpp_pack_golden_words(L):
+    from tests import fixtures
+    for b, c in fixtures.layout_cases():
+        assert ab.pack_int4(c.reshape(1, 8), L).tolist() == [b.tolist()]
+        assert ab.unpack_int4(b.reshape(1, 4), 8, L).tolist() == [c.tolist()]
+
+
+def test_cpp_pack_rejects_bad_input(L):
+    with pytest.raises(ab.ArcheadError) as e:
+        ab.pack_int4(np.full((2, 8), 8, dtype=np.int8), L)
+    assert e.value.status == ab.E_INVALID_ARG
+    assert b"out of [-8, 7]" in L.archead_last_error()
+    with pytest.raises(ab.ArcheadError):
+        ab.pack_int4(np.zeros((1, 12), dtype=np.int8), L)   # d % 8 != 0
+    assert L.archead_pack_int4(None, 1, 8, None) == ab.E_INVALID_ARG
+
+
+def test_create_checks_arguments_before_touching_the_device(L):
+    desc = _desc()
+    h = ctypes.c_void_p(123)
+    # missing residual pointers
+    ptrs = ab.Ptrs()
+    assert L.archead_create(ctypes.byref(desc), ctypes.byref(ptrs),
+                            ctypes.byref(h)) == ab.E_INVALID_ARG
+    assert h.value is None
+    # r_c > 0 without core pointers
+    ptrs = ab.Ptrs(res_codes=4096, res_scales=4096)
+    assert L.archead_create(ctypes.byref(desc), ctypes.byref(ptrs),
+                            ctypes.byref(h)) == ab.E_INVALID_ARG
+    # misaligned codes
+    full = ab.Ptrs(*([4096] * 10))
+    full.res_codes = 4100
+    assert L.archead_create(ctypes.byref(desc), ctypes.byref(full),
+                            ctypes.byref(h)) == ab.E_MISALIGNED
+    full = ab.Ptrs(*([4096] * 10))
+    full.core_u_scale = 4097
+    assert L.archead_create(ctypes.byref(desc), ctypes.byref(full),
+                            ctypes.byref(h)) == ab.E_MISALIGNED
+    bad = _desc(abi=7)
+    assert L.archead_create(ctypes.byref(bad), ctypes.byref(full),
+                            ctypes.byref(h)) == ab.E_INVALID_ARG
+    assert L.archead_create(ctypes.byref(desc), ctypes.byref(full), None) == \
+        ab.E_INVALID_ARG
+
+
+def test_null_handle_calls(L):
+    assert L.archead_workspace_bytes(None, 4, ab.OP_LOGITS) == 0
+    assert L.archead_logits(None, None, 1, 8, None, ab.F32, 8, None, 0, None) == \
+        ab.E_INVALID_ARG
+    assert L.archead_logits_ce(None, None, 1, 8, None, ab.I32, None, None, None, 0,
+                               None) == ab.E_INVALID_ARG
+    assert L.archead_set_gemv_max_m(None, 3) == ab.E_INVALID_ARG
+    assert L.archead_get_gemv_max_m(None) == -1
+    L.archead_destroy(None)
+
+
+def test_host_only_build_agrees(tmp_path):
+    """The same host translation unit built with g++ (no HIP) gives the same
+    answers (it is what the sanitizer build runs)."""
+    from paper_2608_02703_amd import build
+    path = build.build_host()
+    H = ab.host_lib(path)
+    desc = _desc()
+    assert ab.validate_desc(desc, H) == ab.OK
+    assert ab.packed_bytes(desc, H) == ab.packed_bytes(desc, ab.lib())
+    codes = np.random.default_rng(0).integers(-8, 8, size=(3, 64)).astype(np.int8)
+    assert np.array_equal(ab.pack_int4(codes, H), ab.pack_int4(codes, ab.lib()))

@@ -1,0 +1,291 @@
+"""GPU parity of the HIP path against the fp64 CPU oracle (through the C ABI).
+
+Tolerances: fp32 logits max |d| <= 2e-3 (1 + |logit|); CE max |d| <= 1e-4
+nats per token; bf16 logits within one bf16 step of RNE(oracle); integer
+probes and the hand-derived worked example bit-exact; argmax equal on every
+token whose oracle top-2 gap exceeds twice the logit tolerance.
+"""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import head as ohead
+from synth import CONFIGS, make_head, make_targets, make_x
+from tests import fixtures
+from tests.gpu_util import (argmax_agreement, assert_bf16_output, assert_ce_close,
+                            assert_logits_close, cached_head, cached_oracle_logits, say,
+                            torch_x)
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    yield
+    torch.cuda.synchronize()
+
+
+_heads = {}
+
+
+def packed(cfg, **over):
+    from paper_2608_02703_amd import PackedHead
+    key = (cfg, tuple(sorted(over.items())))
+    if key not in _heads:
+        if len(_heads) > 2:
+            for k in list(_heads)[:-1]:
+                _heads.pop(k).close()
+        h = cached_head(cfg, **over) if over else cached_head(cfg)
+        _heads[key] = PackedHead.from_arrays(h)
+    return _heads[key]
+
+
+def gpu_logits(ph, x_bits, out_dtype=None, **kw):
+    lg = ph.logits(torch_x(x_bits, **kw), out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    if lg.dtype == torch.bfloat16:
+        return lg.view(torch.int16).cpu().numpy().view(np.uint16)
+    return lg.cpu().numpy()
+
+
+def gpu_ce(ph, x_bits, y, dtype=None):
+    t = torch.from_numpy(np.asarray(y)).to("cuda")
+    if dtype is not None:
+        t = t.to(dtype)
+    ce, mean = ph.logits_ce(torch_x(x_bits), t)
+    torch.cuda.synchronize()
+    return ce.cpu().numpy(), float(mean.cpu().numpy()[0])
+
+
+# ------------------------------------------------------------- exact probes
+
+def test_worked_example_exact():
+    from paper_2608_02703_amd import PackedHead
+    h, x, expect, y = fixtures.worked_head()
+    say("worked example V=2 d=64 g=32 rc=1 rr=1 M=3")
+    ph = PackedHead.from_arrays(h)
+    lg = gpu_logits(ph, x)
+    assert np.array_equal(lg.astype(np.float64), expect), lg
+    ce, mean = gpu_ce(ph, x, y)
+    ref = ohead.cross_entropy(expect, y)
+    assert_ce_close(ce, ref, 1e-6, "worked example CE")
+    assert abs(mean - ref.mean()) < 1e-6
+    ph.close()
+
+
+def test_identity_probe_tiny_bit_exact():
+    h = make_head("tiny", rc=0, rr=0)
+    from paper_2608_02703_amd import PackedHead
+    ph = PackedHead.from_arrays(h)
+    eye = np.zeros((h.d, h.d), dtype=np.uint16)
+    eye[np.arange(h.d), np.arange(h.d)] = 0x3F80
+    say("identity probe tiny: M=512 V=8192")
+    lg = gpu_logits(ph, eye)
+    ref = ohead.logits(h, eye)
+    bad = np.argwhere(lg.astype(np.float64) != ref)
+    assert bad.size == 0, f"{len(bad)} mismatches, first {bad[:5].tolist()}"
+    ph.close()
+
+
+def test_identity_probe_qwen_sampled_bit_exact():
+    h = make_head("qwen_decode", rc=0, rr=0)
+    from paper_2608_02703_amd import PackedHead
+    ph = PackedHead.from_arrays(h)
+    rng = np.random.default_rng(5)
+    cols = np.unique(np.concatenate([[0, 1, 7, 8, 31, 32, 127, 128, 2047, 4095],
+                                     rng.integers(0, h.d, 54)]))
+    x = np.zeros((cols.size, h.d), dtype=np.uint16)
+    x[np.arange(cols.size), cols] = 0x3F80
+    say(f"identity probe qwen: M={cols.size} V={h.V}")
+    lg = gpu_logits(ph, x)
+    ref = ohead.logits(h, x)
+    bad = np.argwhere(lg.astype(np.float64) != ref)
+    assert bad.size == 0, f"{len(bad)} mismatches, first {bad[:5].tolist()}"
+    ph.close()
+
+
+# ------------------------------------------------------------- random x
+
+LOGIT_CASES = [("tiny", 1), ("tiny", 8), ("qwen_decode", 1), ("qwen_decode", 4),
+               ("qwen_decode", 16), ("gemma", 1), ("gemma", 8), ("gemma", 64)]
+
+
+@pytest.mark.parametrize("cfg,M", LOGIT_CASES)
+def test_logits_parity(cfg, M):
+    Mmax = max(CONFIGS[cfg]["Ms"])
+    say(f"logits parity {cfg} M={M}")
+    ref = cached_oracle_logits(cfg, Mmax)[:M]
+    ph = packed(cfg)
+    x = make_x(cfg, Mmax)[:M]
+    lg = gpu_logits(ph, x)
+    err = assert_logits_close(lg, ref, what=f"{cfg} M={M}")
+    say(f"  max rel err {err:.2e}")
+    if cfg == "gemma":
+        n, excl = argmax_agreement(lg, ref)
+        say(f"  argmax equal on {n} tokens ({excl} near-ties excluded)")
+
+
+@pytest.mark.timeout(600)
+def test_logits_parity_sweep128k_sampled():
+    cfg = "sweep128k"
+    h = cached_head(cfg)
+    ph = packed(cfg)
+    x_all = make_x(cfg, 512)
+    rng = np.random.default_rng(9)
+    vocab = np.unique(np.concatenate([[0, 1, h.V - 1], rng.integers(0, h.V, 3000)]))
+    ref_all = ohead.logits(h, x_all, vocab=vocab)
+    for M in CONFIGS[cfg]["Ms"]:
+        say(f"sweep128k M={M}")
+        lg = gpu_logits(ph, x_all[:M])
+        assert_logits_close(lg[:, vocab], ref_all[:M], what=f"sweep128k M={M}")
+
+
+@pytest.mark.parametrize("cfg,M", [("tiny", 8), ("qwen_decode", 4)])
+def test_bf16_logits(cfg, M):
+    Mmax = max(CONFIGS[cfg]["Ms"])
+    ref = cached_oracle_logits(cfg, Mmax)[:M]
+    x = make_x(cfg, Mmax)[:M]
+    bits = gpu_logits(packed(cfg), x, out_dtype=torch.bfloat16)
+    f32 = gpu_logits(packed(cfg), x)
+    assert_logits_close(f32, ref, what=f"{cfg} M={M} fp32")
+    assert_bf16_output(bits, f32, ref, f"{cfg} M={M} bf16")
+
+
+# ------------------------------------------------------------- CE
+
+def test_ce_parity_tiny():
+    cfg = "tiny"
+    ref_lg = cached_oracle_logits(cfg, 8)
+    y = make_targets(cfg, 8)
+    ce, mean = gpu_ce(packed(cfg), make_x(cfg, 8), y)
+    ref = ohead.cross_entropy(ref_lg, y)
+    err = assert_ce_close(ce, ref, what="tiny CE")
+    assert abs(mean - ref.mean()) <= 1e-4
+    say(f"tiny CE max err {err:.2e}")
+
+
+def test_ce_parity_gemma_m64_int64_targets():
+    cfg = "gemma"
+    ref_lg = cached_oracle_logits(cfg, 64)
+    y = make_targets(cfg, 64)
+    ce, mean = gpu_ce(packed(cfg), make_x(cfg, 64), y, dtype=torch.int64)
+    assert_ce_close(ce, ohead.cross_entropy(ref_lg, y), what="gemma CE")
+
+
+@pytest.mark.timeout(600)
+def test_ce_parity_qwen_prefill_sampled():
+    cfg = "qwen_prefill"
+    M = CONFIGS[cfg]["Ms"][0]
+    x = make_x(cfg, M)
+    y = make_targets(cfg, M)
+    say(f"prefill CE M={M}")
+    ce, mean = gpu_ce(packed("qwen_decode"), x, y)
+    assert np.isfinite(ce).all()
+    rng = np.random.default_rng(4)
+    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, 30)]))
+    h = cached_head("qwen_decode")
+    ref = ohead.cross_entropy(ohead.logits(h, x[rows]), y[rows])
+    err = assert_ce_close(ce[rows], ref, what="prefill CE sampled")
+    say(f"prefill CE sampled max err {err:.2e}, mean CE {mean:.4f}")
+    assert abs(mean - float(np.mean(ce.astype(np.float64)))) <= 1e-5
+
+
+def test_ce_target_out_of_range_is_nan():
+    cfg = "tiny"
+    V = CONFIGS[cfg]["V"]
+    x = make_x(cfg, 8)[:4]
+    ce, mean = gpu_ce(packed(cfg), x, np.array([0, -1, V, 5], dtype=np.int32))
+    assert np.isnan(ce[1]) and np.isnan(ce[2])
+    assert np.isfinite(ce[0]) and np.isfinite(ce[3]) and np.isnan(mean)
+
+
+# ------------------------------------------------------------- special cases
+
+@pytest.mark.parametrize("rc,rr", [(0, 0), (64, 0), (0, 32)])
+def test_ablations(rc, rr):
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", rc=rc, rr=rr)
+    x = make_x("tiny", 5)
+    ph = PackedHead.from_arrays(h)
+    assert_logits_close(gpu_logits(ph, x), ohead.logits(h, x), what=f"rc={rc} rr={rr}")
+    ph.close()
+
+
+def test_groupwise_factor_scales():
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", gV=128, gB=64)
+    x = make_x("tiny", 3)
+    ph = PackedHead.from_arrays(h)
+    assert_logits_close(gpu_logits(ph, x), ohead.logits(h, x), what="gV=128 gB=64")
+    ph.close()
+
+
+@pytest.mark.parametrize("V,d,g,M", [(1000, 512, 64, 3), (8191, 512, 64, 7),
+                                     (777, 96, 32, 5), (1500, 1024, 256, 2),
+                                     (999, 3072, 128, 6), (33, 160, 32, 1)])
+def test_ragged_shapes(V, d, g, M):
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", V=V, d=d, g=g, rc=16, rr=8)
+    x = make_x("tiny", M, d=d, basis="identity")
+    say(f"ragged V={V} d={d} g={g} M={M}")
+    ph = PackedHead.from_arrays(h)
+    ref = ohead.logits(h, x)
+    assert_logits_close(gpu_logits(ph, x, ld=d + 8), ref, what=f"ragged {V}x{d}")
+    out = torch.full((M, V + 3), 7.0, device="cuda")
+    ph.logits(torch_x(x), out=out[:, :V])
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert (o[:, V:] == 7.0).all(), "wrote past the row"
+    assert_logits_close(o[:, :V], ref, what="ldo > V")
+    y = np.arange(M, dtype=np.int32) * 7 % V
+    ce, _ = gpu_ce(ph, x, y)
+    assert_ce_close(ce, ohead.cross_entropy(ref, y), what="ragged CE")
+    ph.close()
+
+
+def test_determinism_bitwise():
+    cfg = "qwen_decode"
+    ph = packed(cfg)
+    x = make_x(cfg, 16)[:4]
+    a = gpu_logits(ph, x)
+    b = gpu_logits(ph, x)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+    y = make_targets(cfg, 4)
+    c1, m1 = gpu_ce(ph, x, y)
+    c2, m2 = gpu_ce(ph, x, y)
+    assert np.array_equal(c1.view(np.uint32), c2.view(np.uint32)) and m1 == m2
+
+
+# ------------------------------------------------------------- errors
+
+def test_error_paths_on_device():
+    from paper_2608_02703_amd import archead as ab
+    ph = packed("tiny")
+    L = ab.lib()
+    x = torch_x(make_x("tiny", 8))
+    out = torch.empty((8, ph.V), device="cuda")
+    ws = ph.workspace(8, ab.OP_LOGITS, x.device)
+    s = ph._stream(x.device)
+
+    def call(xp, M, ldx, outp, dt, ldo, wsp, wsn):
+        return L.archead_logits(ph.handle, xp, M, ldx, outp, dt, ldo, wsp, wsn, s)
+    assert call(x.data_ptr(), 0, ph.d, 0, ab.F32, ph.V, 0, 0) == ab.OK        # M = 0
+    assert call(x.data_ptr() + 2, 8, ph.d, out.data_ptr(), ab.F32, ph.V,
+                ws.data_ptr(), ws.numel()) == ab.E_MISALIGNED
+    assert call(x.data_ptr(), 8, ph.d - 8, out.data_ptr(), ab.F32, ph.V,
+                ws.data_ptr(), ws.numel()) == ab.E_INVALID_ARG
+    assert call(x.data_ptr(), 8, ph.d, out.data_ptr(), ab.F32, ph.V,
+                ws.data_ptr(), 16) == ab.E_WORKSPACE
+    assert call(x.data_ptr(), 8, ph.d, out.data_ptr(), ab.I32, ph.V,
+                ws.data_ptr(), ws.numel()) == ab.E_INVALID_ARG
+    assert call(x.data_ptr(), 8, ph.d, out.data_ptr(), ab.F32, ph.V - 1,
+                ws.data_ptr(), ws.numel()) == ab.E_INVALID_ARG
+    assert call(x.data_ptr(), -1, ph.d, out.data_ptr(), ab.F32, ph.V,
+                ws.data_ptr(), ws.numel()) == ab.E_INVALID_ARG
+    assert L.archead_last_error()
+    torch.cuda.synchronize()
