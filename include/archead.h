@@ -199,10 +199,9 @@ int64_t archead_get_gemv_max_m(const archead_handle* h);
 
 /* Profiling hook: when start and stop are non-NULL hipEvent_t handles
  * (created by the caller on the handle's device), every later compute call
- * records `start` on its stream immediately before the launch of the kernel
- * that streams the packed head and `stop` immediately after it (around all
- * of its launches when M needs several), so the caller can time that kernel
- * alone.  NULL, NULL turns it off.  Same threading rule as
+ * attaches `start` to the dispatch of the kernel that streams the packed head
+ * and `stop` to its completion (the first and last dispatch when M needs
+ * several), so hipEventElapsedTime gives that kernel's execution time alone.  NULL, NULL turns it off.  Same threading rule as
  * archead_set_gemv_max_m. */
 archead_status archead_set_timing_events(archead_handle* h, void* start, void* stop);
 

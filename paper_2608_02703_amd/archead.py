@@ -103,8 +103,9 @@ def _load(path: str, names) -> ctypes.CDLL:
 
 
 def lib() -> ctypes.CDLL:
-    """The HIP library (all entry points)."""
-    return _load(LIB_PATH, list(_SIGS))
+    """The HIP library (all entry points).  ARCHEAD_LIB may name another
+    build of it (tuning experiments)."""
+    return _load(os.environ.get("ARCHEAD_LIB", LIB_PATH), list(_SIGS))
 
 
 def host_lib(path: Optional[str] = None) -> ctypes.CDLL:

@@ -42,13 +42,13 @@ def _run(cmd, verbose):
                            f"{r.stdout}\n{r.stderr}")
 
 
-def build_hip(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [_hipcc(), *HIP_FLAGS, f"-I{INCLUDE}", os.path.join(CSRC, "host.cpp"),
-           os.path.join(CSRC, "archead.hip"), "-o", tmp]
+def build_hip(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    tmp = out + ".tmp"
+    cmd = [_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], f"-I{INCLUDE}",
+           os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "archead.hip"), "-o", tmp]
     _run(cmd, verbose)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 def build_host(verbose: bool = False, sanitize: bool = False) -> str:

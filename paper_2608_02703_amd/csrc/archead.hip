@@ -15,8 +15,12 @@
 // sum (c + 136) x; the accumulator starts at -136 * sum x over the chunk, so
 // the group partial is sum c x.  The group scale multiplies that fp32 partial
 // (it is never folded into a bf16 weight).
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <math.h>
+#include <stdlib.h>
+
+#include <type_traits>
 #include <stdint.h>
 #include <string.h>
 
@@ -26,11 +30,37 @@
 namespace {
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+
+// 16-byte streaming load (read once: non-temporal hint).
+__device__ __forceinline__ uint4 load_stream16(const uint8_t* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ uint4 load_stream16(const __attribute__((address_space(1))) uint8_t* p) {
+  const u32x4_t v = __builtin_nontemporal_load(
+      reinterpret_cast<const __attribute__((address_space(1))) u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 
 constexpr int kBlock = 256;          // 4 waves of 64
 constexpr int kWaves = kBlock / 64;
-constexpr int kRowsPerStep = 8;      // rows (per lane segment) of one GEMV step
+#ifndef ARCHEAD_ROWS_PER_STEP
+#define ARCHEAD_ROWS_PER_STEP 8
+#endif
+#ifndef ARCHEAD_GEMV_BLOCKS_PER_CU
+#define ARCHEAD_GEMV_BLOCKS_PER_CU 3
+#endif
+#ifndef ARCHEAD_GEMV_PREFETCH
+#define ARCHEAD_GEMV_PREFETCH 1   // GEMV iterations of loads in flight ahead of compute
+#endif
+constexpr int kRowsPerStep = ARCHEAD_ROWS_PER_STEP;  // rows per lane segment of a GEMV step
+constexpr int kGemvBlocksPerCu = ARCHEAD_GEMV_BLOCKS_PER_CU;  // resident GEMV workgroups per CU
 constexpr float kLog2e = 1.4426950408889634f;
+// Fourth word of a gfx9 buffer resource for raw (untyped) 32-bit accesses.
+constexpr int kBufferWord3 = 0x00020000;
+// Cache-policy operand of a buffer load: non-temporal (read-once data).
+constexpr int kLoadStream = 2;
 
 __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2_t, a),
@@ -41,6 +71,21 @@ __device__ __forceinline__ float f16_to_f32(uint16_t h) {
 }
 __device__ __forceinline__ float bf16_lo(uint32_t p) { return __uint_as_float(p << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
+
+// (x & m) | o in one VALU op.  The compiler splits it into v_and + v_or when
+// both constants are literals (gfx9 VOP3 has no literal operand), so the
+// constants are kept in registers and the fused instruction is named here.
+__device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t o) {
+  uint32_t r;
+  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(m), "v"(o));
+  return r;
+}
+
+// Bf16 pair (136 + c) of INT4_V1 elements (8w + 2k, 8w + 2k + 1) of word q.
+template <int K>
+__device__ __forceinline__ uint32_t int4_pair(uint32_t q, uint32_t mask, uint32_t magic) {
+  return and_or(K ? (q >> (4 * K)) : q, mask, magic);
+}
 
 // fp32 -> bf16, round to nearest even; NaN stays NaN.
 __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
@@ -71,8 +116,10 @@ __device__ __forceinline__ float seg_sum(float v) {
 
 // ------------------------------------------------------------------ stage 1
 // t[m, k] = sum_i (s[k, i/grp] c[k, i]) x[m, i] for the rows k of V_c (k <
-// r_c) then of B_w.  One wave per (k, block of 8 tokens); each lane covers
-// 8 consecutive elements per step.  s * c is exact in fp32 (11 x 8 bits).
+// r_c) then of B_w.  One workgroup per (k, block of 8 tokens): the 256
+// threads split d in 8-element pieces, every load of the row is issued before
+// the arithmetic, and the block sums the 256 partials.  s * c is exact in fp32
+// (11 x 8 significant bits).
 struct Stage1Args {
   const uint16_t* x;
   int64_t ldx, M, d;
@@ -83,17 +130,17 @@ struct Stage1Args {
   const uint16_t* sb;
   int64_t gb, rr;
   float* t;  // [M, rc + rr]
+  int64_t mbase;  // first token of this launch
 };
 
 constexpr int kS1Tok = 8;
+constexpr int64_t kMaxGridY = 65535;
 
 __global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
-  const int lane = threadIdx.x & 63;
-  const int64_t wave = int64_t(blockIdx.x) * kWaves + (threadIdx.x >> 6);
+  __shared__ float red[kWaves][kS1Tok];
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int64_t R = a.rc + a.rr;
-  const int64_t mblocks = (a.M + kS1Tok - 1) / kS1Tok;
-  if (wave >= R * mblocks) return;  // uniform per wave
-  const int64_t k = wave % R, m0 = (wave / R) * kS1Tok;
+  const int64_t k = blockIdx.x, m0 = a.mbase + int64_t(blockIdx.y) * kS1Tok;
   const bool core = k < a.rc;
   const int8_t* crow = core ? a.cv + k * a.d : a.cb + (k - a.rc) * a.d;
   const int64_t grp = core ? a.gv : a.gb;
@@ -102,7 +149,8 @@ __global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
   float acc[kS1Tok];
 #pragma unroll
   for (int j = 0; j < kS1Tok; ++j) acc[j] = 0.f;
-  for (int64_t i = int64_t(lane) * 8; i < a.d; i += 512) {
+#pragma unroll 4
+  for (int64_t i = int64_t(threadIdx.x) * 8; i < a.d; i += kBlock * 8) {
     const uint2 cw = *reinterpret_cast<const uint2*>(crow + i);
     const float s = f16_to_f32(srow[i / grp]);
     float w[8];
@@ -126,8 +174,15 @@ __global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
   }
 #pragma unroll
   for (int tt = 0; tt < kS1Tok; ++tt) {
-    const float s = seg_sum<64>(acc[tt]);
-    if (lane == 0 && tt < ntok) a.t[(m0 + tt) * R + k] = s;
+    const float v = seg_sum<64>(acc[tt]);
+    if (lane == 0) red[wid][tt] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x < ntok) {
+    const int tt = threadIdx.x;
+    float v = red[0][tt];
+    for (int w = 1; w < kWaves; ++w) v += red[w][tt];
+    a.t[(m0 + tt) * R + k] = v;
   }
 }
 
@@ -135,8 +190,11 @@ __global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
 // Lanes are split into segments of LPR lanes; a segment owns one vocabulary
 // row at a time and walks along d in 16-byte chunks (32 codes), LPR chunks
 // per iteration, so each segment load is LPR * 16 contiguous bytes.  A wave
-// step covers kRowsPerStep rows per segment.  Waves get contiguous, balanced
-// ranges of steps (persistent grid).  x, the chunk biases and t sit in LDS.
+// step covers kRowsPerStep rows per segment (WR rows in all).  Waves get
+// contiguous, balanced ranges of steps (persistent grid).  x, the chunk
+// biases and t sit in LDS.  Step bases are wave-uniform (scalar registers);
+// per-lane offsets are 32-bit and computed once per step.  Rows past V (the
+// last step only) are clamped to row V-1 for loading and never stored.
 struct GemvArgs {
   const uint8_t* codes;
   const uint16_t* rs;
@@ -148,9 +206,13 @@ struct GemvArgs {
   int64_t ldx;
   const float* t;  // [M, rc + rr]
   int64_t tok0;    // first token of this pass
-  int64_t V, d, g, rc, rr;
-  int64_t nsteps;  // ceil(V / rows per wave step)
+  int64_t V;
+  int d, g, rc, rr;
+  int gshift;      // log2(g / 32) when g is a power of two, else -1
+  int vec_exp;     // expansion codes loaded as one dword per lane (see ExpOps)
+  int64_t cu_stride, ca_stride, su_stride, sa_stride;  // 0 for an absent factor
   int nit;         // iterations along d: (d / 32) / LPR
+  int64_t nsteps;  // ceil(V / rows per wave step)
   void* out;
   int64_t ldo;
   int out_bf16;
@@ -162,171 +224,452 @@ struct GemvArgs {
   float* tgt_logit;  // [M]
 };
 
+// Sum RB per-lane values over the LPR lanes of each segment.  The first
+// log2(RB) butterfly stages halve the number of values per lane (a lane keeps
+// one half, its partner the other), so 8 rows cost 7 exchanges + 3 instead of
+// 8 * log2(LPR).  Afterwards every lane holds the total of the row given by
+// row_of_lane.  Written with compile-time indices throughout so the values
+// stay in registers (a runtime index would turn the selects into an indexed
+// array access).
+__device__ __forceinline__ void xchg_add(float& lo, float hi_v, bool hi, int off) {
+  const float send = hi ? lo : hi_v;
+  const float keep = hi ? hi_v : lo;
+  lo = keep + __shfl_xor(send, off, 64);
+}
+
+template <int J, int H, int RB>
+__device__ __forceinline__ void xchg_range(float (&v)[RB], bool hi, int off) {
+  if constexpr (J < H) {
+    xchg_add(v[J], v[J + H], hi, off);
+    xchg_range<J + 1, H, RB>(v, hi, off);
+  }
+}
+
+template <int OFF, int N, int RB>
+__device__ __forceinline__ void reduce_stage(float (&v)[RB], int lane) {
+  if constexpr (OFF >= 1) {
+    if constexpr (N > 1) {
+      xchg_range<0, N / 2, RB>(v, (lane & OFF) != 0, OFF);
+      reduce_stage<OFF / 2, N / 2, RB>(v, lane);
+    } else {
+      v[0] += __shfl_xor(v[0], OFF, 64);
+      reduce_stage<OFF / 2, 1, RB>(v, lane);
+    }
+  }
+}
+
+template <int LPR, int RB>
+__device__ __forceinline__ float seg_reduce_rows(float (&v)[RB], int lane) {
+  static_assert(LPR >= RB, "needs at least one lane per row");
+  reduce_stage<LPR / 2, RB, RB>(v, lane);
+  return v[0];
+}
+
+// A pointer every lane of the wave holds, moved to scalar registers so
+// loads can use the scalar-base + 32-bit-offset addressing form.
+#define ARCHEAD_GLOBAL __attribute__((address_space(1)))
+template <typename T>
+__device__ __forceinline__ const ARCHEAD_GLOBAL T* wave_uniform(const T* p) {
+  const uint64_t u = reinterpret_cast<uint64_t>(p);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane(uint32_t(u));
+  const uint32_t hi = __builtin_amdgcn_readfirstlane(uint32_t(u >> 32));
+  return reinterpret_cast<const ARCHEAD_GLOBAL T*>((uint64_t(hi) << 32) | lo);
+}
+
+// Row (0..RB-1) whose total seg_reduce_rows leaves in this lane.
+template <int LPR, int RB>
+__device__ __forceinline__ int row_of_lane(int lane) {
+  int r = 0, n = RB;
+#pragma unroll
+  for (int off = LPR / 2; off > 0 && n > 1; off >>= 1) {
+    n /= 2;
+    if (lane & off) r += n;
+  }
+  return r;
+}
+
+// Rank-r expansion operands of a step's rows, loaded with the step's first
+// chunk of codes.  The (r_c + r_r) / 4 dwords of a row -- U_c codes first,
+// then A_w codes -- are dealt to the lanes of its segment, KD per lane: lane
+// sl holds dwords q = sl + kd * LPR (4 codes each) and the matching row
+// scale (s_U for a U_c dword, s_A for an A_w dword).  Since t is laid out as
+// [t_c | t_w], dword q pairs with t[4q .. 4q + 3] in both cases.  Used when
+// r_c and r_r are multiples of 4 and (r_c + r_r) / 4 <= KD * LPR.
+template <int RB, int KD>
+struct ExpOps {
+  uint32_t c[RB][KD];   // four int8 codes
+  uint32_t s[RB][KD];   // fp16 bit pattern of the row scale
+};
+
+template <int LPR>
+struct ExpLanes {
+  static constexpr int KD = LPR >= 64 ? 1 : 2;
+};
+
+// acc += scale * (codes . t) over the lane's dwords of each row.
+template <int TOK, int RB, int KD, int LPR>
+__device__ __forceinline__ void apply_expansion(float (&acc)[RB][TOK], const ExpOps<RB, KD>& e,
+                                                const float* st, int R, int sl) {
+  const int R4 = R / 4;
+#pragma unroll
+  for (int kd = 0; kd < KD; ++kd) {
+    const int q = sl + kd * LPR;
+    const bool valid = q < R4;
+    const int qq = valid ? q : 0;
+#pragma unroll
+    for (int tt = 0; tt < TOK; ++tt) {
+      const float4 t4 = *reinterpret_cast<const float4*>(st + tt * R + 4 * qq);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const uint32_t u = e.c[rb][kd];
+        float du = float(int8_t(u)) * t4.x;
+        du = fmaf(float(int8_t(u >> 8)), t4.y, du);
+        du = fmaf(float(int8_t(u >> 16)), t4.z, du);
+        du = fmaf(float(int8_t(u >> 24)), t4.w, du);
+        const float sc = valid ? f16_to_f32(uint16_t(e.s[rb][kd])) : 0.f;
+        acc[rb][tt] = fmaf(sc, du, acc[rb][tt]);
+      }
+    }
+  }
+}
+
+// One d-iteration of a step: RB rows x one 16-byte chunk per lane.
+template <int TOK, int RB>
+__device__ __forceinline__ void gemv_chunk(float (&acc)[RB][TOK], const uint4 (&q)[RB],
+                                           const uint32_t (&sc)[RB], const uint16_t* sx,
+                                           const float* sxb, int d, int C, int c,
+                                           uint32_t kMask, uint32_t kMagic) {
+  uint32_t xw[TOK][16];
+  float xb[TOK];
+#pragma unroll
+  for (int tt = 0; tt < TOK; ++tt) {
+    // x is held in LDS as [token][part j][chunk c] of 16-byte units, so the
+    // lanes of a wave (consecutive chunks) read consecutive 16-byte units
+    const uint4* px = reinterpret_cast<const uint4*>(sx) + tt * 4 * C + c;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint4 u = px[j * C];
+      xw[tt][4 * j] = u.x; xw[tt][4 * j + 1] = u.y;
+      xw[tt][4 * j + 2] = u.z; xw[tt][4 * j + 3] = u.w;
+    }
+    xb[tt] = sxb[tt * C + c];
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const float s = f16_to_f32(uint16_t(sc[rb]));
+    const uint32_t w4[4] = {q[rb].x, q[rb].y, q[rb].z, q[rb].w};
+    uint32_t pr[16];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      pr[4 * w + 0] = int4_pair<0>(w4[w], kMask, kMagic);
+      pr[4 * w + 1] = int4_pair<1>(w4[w], kMask, kMagic);
+      pr[4 * w + 2] = int4_pair<2>(w4[w], kMask, kMagic);
+      pr[4 * w + 3] = int4_pair<3>(w4[w], kMask, kMagic);
+    }
+#pragma unroll
+    for (int tt = 0; tt < TOK; ++tt) {
+      float dsum = xb[tt];
+#pragma unroll
+      for (int j = 0; j < 16; ++j) dsum = dot2_bf16(pr[j], xw[tt][j], dsum);
+      acc[rb][tt] = fmaf(s, dsum, acc[rb][tt]);
+    }
+  }
+}
+
+// Per-lane softmax state of the fused CE epilogue.
+template <int TOK>
+struct CeState {
+  float mx[TOK], se[TOK];
+  int64_t y[TOK];
+};
+
+// End of a step: add the rank-r expansions of the lane's rows, reduce over
+// the segment and store the logits (or fold them into the softmax state).
+// Row rb of the lane is row0 + min(seg + rb * SEG, lim).
+template <int TOK, int LPR, int RB, bool CE, bool EXPAND>
+__device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvArgs& a,
+                                              int64_t row0, uint32_t lim, int seg, int sl,
+                                              int lane, int my_row, bool writer,
+                                              const float* st, CeState<TOK>& ce) {
+  constexpr int SEG = 64 / LPR;
+  const int R = a.rc + a.rr;
+#pragma unroll
+  for (int rb = 0; rb < RB && EXPAND; ++rb) {
+    uint32_t r = uint32_t(seg + rb * SEG);
+    r = r < lim ? r : lim;
+    const int64_t v = row0 + r;
+    if (a.rc) {
+      const float su = f16_to_f32(a.su[v]);
+      for (int k = sl; k < a.rc; k += LPR) {
+        const float u = su * float(a.cu[v * a.rc + k]);
+#pragma unroll
+        for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = fmaf(u, st[tt * R + k], acc[rb][tt]);
+      }
+    }
+    if (a.rr) {
+      const float sa = f16_to_f32(a.sa[v]);
+      for (int k = sl; k < a.rr; k += LPR) {
+        const float u = sa * float(a.ca[v * a.rr + k]);
+#pragma unroll
+        for (int tt = 0; tt < TOK; ++tt)
+          acc[rb][tt] = fmaf(u, st[tt * R + a.rc + k], acc[rb][tt]);
+      }
+    }
+  }
+  const int64_t v = row0 + seg + int64_t(my_row) * SEG;   // row this lane reports
+  const bool store = writer && v < a.V;
+#pragma unroll
+  for (int tt = 0; tt < TOK; ++tt) {
+    float col[RB];
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) col[rb] = acc[rb][tt];
+    const float l = seg_reduce_rows<LPR, RB>(col, lane);
+    if (store) {
+      if constexpr (!CE) {
+        const int64_t o = (a.tok0 + tt) * a.ldo + v;
+        if (a.out_bf16)
+          reinterpret_cast<uint16_t*>(a.out)[o] = f32_to_bf16_rne(l);
+        else
+          reinterpret_cast<float*>(a.out)[o] = l;
+      } else {
+        if (l > ce.mx[tt]) {
+          ce.se[tt] = ce.se[tt] * fast_exp(ce.mx[tt] - l) + 1.f;
+          ce.mx[tt] = l;
+        } else {
+          ce.se[tt] += fast_exp(l - ce.mx[tt]);
+        }
+        if (v == ce.y[tt]) a.tgt_logit[a.tok0 + tt] = l;
+      }
+    }
+  }
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = 0.f;
+}
+
+// Waves per SIMD the single-token GEMV is compiled for (register budget
+// 512 / waves per lane).
+#ifndef ARCHEAD_GEMV_WAVES
+#define ARCHEAD_GEMV_WAVES 3
+#endif
 template <int TOK, int LPR, bool CE>
-__global__ __launch_bounds__(kBlock) void k_gemv(GemvArgs a) {
+__global__ __launch_bounds__(kBlock)
+__attribute__((amdgpu_waves_per_eu(TOK == 1 ? (LPR >= 64 ? ARCHEAD_GEMV_WAVES : 2) : 1)))
+void k_gemv(GemvArgs a) {
   constexpr int SEG = 64 / LPR;              // rows in flight per wave
-  constexpr int RB = kRowsPerStep;
+  constexpr int RB = LPR < kRowsPerStep ? LPR : kRowsPerStep;
   constexpr int WR = RB * SEG;               // rows per wave step
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float2 red[kWaves][TOK];
 
-  const int64_t C = a.d / 32;                // 16-byte chunks per row
-  const int64_t R = a.rc + a.rr;
+  const int d = a.d;
+  const int C = d / 32;                      // 16-byte chunks per row
+  const int R = a.rc + a.rr;
   uint16_t* sx = reinterpret_cast<uint16_t*>(smem);          // [TOK][d]
-  float* sxb = reinterpret_cast<float*>(sx + TOK * a.d);      // [TOK][C]
+  float* sxb = reinterpret_cast<float*>(sx + TOK * d);        // [TOK][C]
   float* st = sxb + TOK * C;                                  // [TOK][R]
 
-  const int64_t x8 = a.d / 8;
-  for (int64_t i = threadIdx.x; i < TOK * x8; i += kBlock) {
-    const int64_t tt = i / x8, j = i - tt * x8;
-    reinterpret_cast<uint4*>(sx)[i] =
-        *reinterpret_cast<const uint4*>(a.x + (a.tok0 + tt) * a.ldx + j * 8);
+  {
+    const int x8 = d / 8;   // 16-byte units per token: unit u = chunk u/4, part u%4
+    for (int i = threadIdx.x; i < TOK * x8; i += kBlock) {
+      const int tt = i / x8, u = i - tt * x8;
+      reinterpret_cast<uint4*>(sx)[(tt * 4 + (u & 3)) * C + (u >> 2)] =
+          *reinterpret_cast<const uint4*>(a.x + (a.tok0 + tt) * a.ldx + u * 8);
+    }
+    for (int i = threadIdx.x; i < TOK * R; i += kBlock) {
+      const int tt = i / R;
+      st[i] = a.t[(a.tok0 + tt) * R + (i - tt * R)];
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < TOK * C; i += kBlock) {
+      const int tt = i / C, c = i - tt * C;
+      float s = 0.f;
+      for (int j = 0; j < 4; ++j) {
+        const uint4 u = reinterpret_cast<const uint4*>(sx)[(tt * 4 + j) * C + c];
+        s += bf16_lo(u.x) + bf16_hi(u.x) + bf16_lo(u.y) + bf16_hi(u.y) +
+             bf16_lo(u.z) + bf16_hi(u.z) + bf16_lo(u.w) + bf16_hi(u.w);
+      }
+      sxb[i] = -float(archead::kInt4Bias) * s;
+    }
+    __syncthreads();
   }
-  for (int64_t i = threadIdx.x; i < TOK * R; i += kBlock) {
-    const int64_t tt = i / R;
-    st[i] = a.t[(a.tok0 + tt) * R + (i - tt * R)];
-  }
-  __syncthreads();
-  for (int64_t i = threadIdx.x; i < TOK * C; i += kBlock) {
-    const int64_t tt = i / C, c = i - tt * C;
-    const uint32_t* p = reinterpret_cast<const uint32_t*>(sx + tt * a.d + c * 32);
-    float s = 0.f;
-    for (int j = 0; j < 16; ++j) s += bf16_lo(p[j]) + bf16_hi(p[j]);
-    sxb[i] = -float(archead::kInt4Bias) * s;
-  }
-  __syncthreads();
 
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
   const int seg = lane / LPR, sl = lane % LPR;
+  // Steps are dealt out grid-stride (wave gw takes steps gw, gw + W, ...), so
+  // at any moment the whole grid streams one compact window of the head.
   const int64_t W = int64_t(gridDim.x) * kWaves;
+  const int wid = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int64_t gw = int64_t(blockIdx.x) * kWaves + wid;
-  const int64_t s_begin = a.nsteps * gw / W, s_end = a.nsteps * (gw + 1) / W;
-  const int64_t rowbytes = a.d / 2, ngrp = a.d / a.g;
+  const uint32_t rowbytes = uint32_t(d) / 2;
+  const uint32_t ngrp = uint32_t(d / a.g);
+  const int my_row = row_of_lane<LPR, RB>(lane);   // row this lane ends up with
+  const bool writer = (sl & (LPR / RB - 1)) == 0;
+  // nibble-pair mask and bf16 128.0 bit pattern, held in registers
+  const uint32_t kMask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+  const uint32_t kMagic = __builtin_amdgcn_readfirstlane(0x43004300u);
 
-  float mx[TOK], se[TOK];
+  CeState<TOK> ce;
 #pragma unroll
-  for (int tt = 0; tt < TOK; ++tt) { mx[tt] = -INFINITY; se[tt] = 0.f; }
-  int64_t y[TOK];
-  if constexpr (CE) {
+  for (int tt = 0; tt < TOK; ++tt) {
+    ce.mx[tt] = -INFINITY;
+    ce.se[tt] = 0.f;
+    if constexpr (CE)
+      ce.y[tt] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + tt]
+                         : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + tt]);
+  }
+  float acc[RB][TOK];
 #pragma unroll
-    for (int tt = 0; tt < TOK; ++tt)
-      y[tt] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + tt]
-                      : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + tt]);
+  for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+    for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = 0.f;
+
+  // ---- full steps (every row < V): software-pipelined.  Loads run kPD
+  // iterations ahead of the arithmetic in a ring of kPD + 1 register
+  // buffers, so a wave keeps about kPD iterations of codes in flight while it
+  // computes; codes and scales are read through buffer resources whose base
+  // and per-row offsets live in scalar registers.
+  const int64_t full_steps = a.vec_exp ? a.V / WR : 0;
+  if (gw < full_steps) {
+    constexpr int kPD = ARCHEAD_GEMV_PREFETCH;
+    constexpr int NB = kPD + 1;
+    const uint32_t voff = uint32_t(seg) * rowbytes + uint32_t(sl) * 16u;
+    const uint32_t svoff = uint32_t(seg) * ngrp;
+    // every load below is unconditional: absent factors point at a valid
+    // buffer with row stride 0 (see gemv_args), lanes without a dword
+    // re-read dword 0, and loads past the wave's last iteration re-read that
+    // iteration; all of it is masked or unused, so no branch separates a
+    // load from its use (a branch would make the wait-count pass drain the
+    // loads in flight)
+    constexpr int KD = ExpLanes<LPR>::KD;
+    const int rc4 = a.rc / 4, R4 = R / 4;
+    auto load = [&](int64_t stp, int itx, uint4 (&q)[RB], uint32_t (&sc)[RB]) {
+      const uint64_t cbytes = uint64_t(a.V - stp * WR) * rowbytes;
+      const uint64_t sbytes = uint64_t(a.V - stp * WR) * ngrp * 2u;
+      const __amdgpu_buffer_rsrc_t rc_ = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint8_t*>(a.codes + uint64_t(stp) * WR * rowbytes), 0,
+          int(cbytes < 0xffffffffull ? cbytes : 0xffffffffull), kBufferWord3);
+      const __amdgpu_buffer_rsrc_t rs_ = __builtin_amdgcn_make_buffer_rsrc(
+          const_cast<uint16_t*>(a.rs + uint64_t(stp) * WR * ngrp), 0,
+          int(sbytes < 0xffffffffull ? sbytes : 0xffffffffull), kBufferWord3);
+      const uint32_t c = uint32_t(itx * LPR + sl);
+      const uint32_t grp = a.gshift >= 0 ? (c >> a.gshift) : (c * 32u) / uint32_t(a.g);
+      const int itoff = itx * LPR * 16;
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(
+            rc_, int(voff), int(uint32_t(rb * SEG) * rowbytes) + itoff, kLoadStream);
+        q[rb] = make_uint4(v.x, v.y, v.z, v.w);
+      }
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        sc[rb] = __builtin_amdgcn_raw_buffer_load_b16(
+            rs_, int((svoff + grp) * 2u), int(uint32_t(rb * SEG) * ngrp * 2u), 0);
+    };
+    // expansion operands of step stp (one buffer: the next step's operands
+    // are requested right after the current step's have been applied)
+    auto load_exp = [&](int64_t stp, ExpOps<RB, KD>& e) {
+      const int64_t v0 = stp * WR + seg;
+#pragma unroll
+      for (int kd = 0; kd < KD; ++kd) {
+        int q = sl + kd * LPR;
+        q = q < R4 ? q : 0;
+        const bool isu = q < rc4;
+        const int8_t* cb = isu ? a.cu + 4 * q : a.ca + 4 * (q - rc4);
+        const int64_t cs = isu ? a.cu_stride : a.ca_stride;
+        const uint16_t* sp = isu ? a.su : a.sa;
+        const int64_t ss = isu ? a.su_stride : a.sa_stride;
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) {
+          const int64_t v = v0 + rb * SEG;
+          e.c[rb][kd] = *reinterpret_cast<const uint32_t*>(cb + v * cs);
+          e.s[rb][kd] = sp[v * ss];
+        }
+      }
+    };
+    uint4 q[NB][RB];
+    uint32_t sc[NB][RB];
+    ExpOps<RB, KD> e;
+    const int64_t last_step = gw + ((full_steps - 1 - gw) / W) * W;
+    auto advance = [&](int64_t& st, int& itv) {
+      if (++itv == a.nit) { itv = 0; st += W; }
+    };
+    int64_t cstep = gw, lstep = gw;   // compute and load cursors
+    int cit = 0, lit = 0;
+#pragma unroll
+    for (int j = 0; j < kPD; ++j) {
+      const bool ok = lstep < full_steps;
+      load(ok ? lstep : last_step, ok ? lit : a.nit - 1, q[j], sc[j]);
+      advance(lstep, lit);
+    }
+    load_exp(cstep, e);
+    bool done = false;
+    auto body = [&](auto J) {
+      constexpr int j = decltype(J)::value;
+      constexpr int jl = (j + kPD) % NB;
+      {
+        const bool ok = lstep < full_steps;
+        load(ok ? lstep : last_step, ok ? lit : a.nit - 1, q[jl], sc[jl]);
+        advance(lstep, lit);
+      }
+      asm volatile("" ::: "memory");  // keep the loads ahead of the work below
+      if (cit == 0) apply_expansion<TOK, RB, KD, LPR>(acc, e, st, R, sl);
+      int64_t nstep = cstep;
+      int nit = cit;
+      advance(nstep, nit);
+      const bool more = nstep < full_steps;
+      if (nit == 0) load_exp(more ? nstep : cstep, e);
+      gemv_chunk<TOK, RB>(acc, q[j], sc[j], sx, sxb, d, C, cit * LPR + sl, kMask, kMagic);
+      if (cit == a.nit - 1)
+        gemv_epilogue<TOK, LPR, RB, CE, false>(acc, a, cstep * WR, uint32_t(WR - 1), seg, sl,
+                                               lane, my_row, writer, st, ce);
+      cstep = nstep;
+      cit = nit;
+      done = !more;
+    };
+    while (true) {
+      body(std::integral_constant<int, 0>{});
+      if (done) break;
+      body(std::integral_constant<int, 1>{});
+      if (done) break;
+      if constexpr (NB > 2) {
+        body(std::integral_constant<int, 2 % NB>{});
+        if (done) break;
+      }
+      if constexpr (NB > 3) {
+        body(std::integral_constant<int, 3 % NB>{});
+        if (done) break;
+      }
+    }
   }
 
-  for (int64_t step = s_begin; step < s_end; ++step) {
-    float acc[RB][TOK];
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb)
-#pragma unroll
-      for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = 0.f;
-    const int64_t vbase = step * WR + seg;
-
+  // ---- steps not taken above: the partial last step (rows past V clamped
+  // to V-1, never stored), or every step when the expansion codes cannot be
+  // read as dwords; grid-stride like the fast path
+  int64_t first = full_steps + ((gw - full_steps % W) % W + W) % W;
+  for (int64_t step = first; step < a.nsteps; step += W) {
+    const int64_t row0 = step * WR;
+    const uint8_t* cbase = a.codes + row0 * rowbytes;
+    const uint16_t* sbase = a.rs + row0 * ngrp;
+    const int64_t left = a.V - 1 - row0;
+    const uint32_t lim = uint32_t(left < WR - 1 ? left : WR - 1);
     for (int it = 0; it < a.nit; ++it) {
-      const int64_t c = int64_t(it) * LPR + sl;
+      const uint32_t c = uint32_t(it * LPR + sl);
+      const uint32_t grp = a.gshift >= 0 ? (c >> a.gshift) : (c * 32u) / uint32_t(a.g);
       uint4 q[RB];
-      uint16_t sc[RB];
+      uint32_t sc[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const int64_t v = vbase + rb * SEG;
-        if (v < a.V) {
-          q[rb] = *reinterpret_cast<const uint4*>(a.codes + v * rowbytes + c * 16);
-          sc[rb] = a.rs[v * ngrp + (c * 32) / a.g];
-        } else {
-          q[rb] = make_uint4(0x88888888u, 0x88888888u, 0x88888888u, 0x88888888u);
-          sc[rb] = 0;
-        }
+        uint32_t r = uint32_t(seg + rb * SEG);
+        r = r < lim ? r : lim;
+        q[rb] = load_stream16(cbase + uint64_t(r) * rowbytes + c * 16u);
+        sc[rb] = sbase[uint64_t(r) * ngrp + grp];
       }
-      uint32_t xw[TOK][16];
-      float xb[TOK];
-#pragma unroll
-      for (int tt = 0; tt < TOK; ++tt) {
-        const uint4* px = reinterpret_cast<const uint4*>(sx + tt * a.d + c * 32);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const uint4 u = px[j];
-          xw[tt][4 * j] = u.x; xw[tt][4 * j + 1] = u.y;
-          xw[tt][4 * j + 2] = u.z; xw[tt][4 * j + 3] = u.w;
-        }
-        xb[tt] = sxb[tt * C + c];
-      }
-#pragma unroll
-      for (int rb = 0; rb < RB; ++rb) {
-        const float s = f16_to_f32(sc[rb]);
-        const uint32_t w4[4] = {q[rb].x, q[rb].y, q[rb].z, q[rb].w};
-        uint32_t pr[16];
-#pragma unroll
-        for (int w = 0; w < 4; ++w)
-#pragma unroll
-          for (int k = 0; k < 4; ++k)
-            pr[4 * w + k] = ((w4[w] >> (4 * k)) & 0x000F000Fu) | 0x43004300u;
-#pragma unroll
-        for (int tt = 0; tt < TOK; ++tt) {
-          float dsum = xb[tt];
-#pragma unroll
-          for (int j = 0; j < 16; ++j) dsum = dot2_bf16(pr[j], xw[tt][j], dsum);
-          acc[rb][tt] = fmaf(s, dsum, acc[rb][tt]);
-        }
-      }
+      gemv_chunk<TOK, RB>(acc, q, sc, sx, sxb, d, C, int(c), kMask, kMagic);
     }
-
-    // epilogue: rank-r expansions, segment reduction, store or softmax partials
-#pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const int64_t v = vbase + rb * SEG;
-      const bool ok = v < a.V;
-      if (ok) {
-        if (a.rc) {
-          float ec[TOK];
-#pragma unroll
-          for (int tt = 0; tt < TOK; ++tt) ec[tt] = 0.f;
-          for (int64_t k = sl; k < a.rc; k += LPR) {
-            const float u = float(a.cu[v * a.rc + k]);
-#pragma unroll
-            for (int tt = 0; tt < TOK; ++tt) ec[tt] = fmaf(u, st[tt * R + k], ec[tt]);
-          }
-          const float su = f16_to_f32(a.su[v]);
-#pragma unroll
-          for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = fmaf(su, ec[tt], acc[rb][tt]);
-        }
-        if (a.rr) {
-          float ew[TOK];
-#pragma unroll
-          for (int tt = 0; tt < TOK; ++tt) ew[tt] = 0.f;
-          for (int64_t k = sl; k < a.rr; k += LPR) {
-            const float u = float(a.ca[v * a.rr + k]);
-#pragma unroll
-            for (int tt = 0; tt < TOK; ++tt) ew[tt] = fmaf(u, st[tt * R + a.rc + k], ew[tt]);
-          }
-          const float sa = f16_to_f32(a.sa[v]);
-#pragma unroll
-          for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = fmaf(sa, ew[tt], acc[rb][tt]);
-        }
-      }
-#pragma unroll
-      for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] = seg_sum<LPR>(acc[rb][tt]);
-      if (ok && sl == 0) {
-#pragma unroll
-        for (int tt = 0; tt < TOK; ++tt) {
-          const float l = acc[rb][tt];
-          if constexpr (!CE) {
-            const int64_t o = (a.tok0 + tt) * a.ldo + v;
-            if (a.out_bf16)
-              reinterpret_cast<uint16_t*>(a.out)[o] = f32_to_bf16_rne(l);
-            else
-              reinterpret_cast<float*>(a.out)[o] = l;
-          } else {
-            if (l > mx[tt]) {
-              se[tt] = se[tt] * fast_exp(mx[tt] - l) + 1.f;
-              mx[tt] = l;
-            } else {
-              se[tt] += fast_exp(l - mx[tt]);
-            }
-            if (v == y[tt]) a.tgt_logit[a.tok0 + tt] = l;
-          }
-        }
-      }
-    }
+    gemv_epilogue<TOK, LPR, RB, CE, true>(acc, a, row0, lim, seg, sl, lane, my_row, writer, st,
+                                          ce);
   }
 
   if constexpr (CE) {
@@ -334,11 +677,11 @@ __global__ __launch_bounds__(kBlock) void k_gemv(GemvArgs a) {
     for (int tt = 0; tt < TOK; ++tt) {
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
-        const float om = __shfl_xor(mx[tt], off, 64);
-        const float os = __shfl_xor(se[tt], off, 64);
-        lse_merge(mx[tt], se[tt], om, os);
+        const float om = __shfl_xor(ce.mx[tt], off, 64);
+        const float os = __shfl_xor(ce.se[tt], off, 64);
+        lse_merge(ce.mx[tt], ce.se[tt], om, os);
       }
-      if (lane == 0) red[wid][tt] = make_float2(mx[tt], se[tt]);
+      if (lane == 0) red[wid][tt] = make_float2(ce.mx[tt], ce.se[tt]);
     }
     __syncthreads();
     if (threadIdx.x < TOK) {
@@ -428,7 +771,8 @@ size_t gemv_lds_bytes(const archead_desc& d, int tok) {
 }
 
 int64_t gemv_rows_per_step(const archead_desc& d) {
-  return int64_t(kRowsPerStep) * (64 / archead::lanes_per_row(d.d));
+  const int lpr = archead::lanes_per_row(d.d);
+  return int64_t(lpr < kRowsPerStep ? lpr : kRowsPerStep) * (64 / lpr);
 }
 
 archead_status hip_fail(hipError_t e, const char* what) {
@@ -456,6 +800,11 @@ int64_t gemv_grid(const archead_handle* h, int tok, bool ce) {
                                                      kBlock, lds) != hipSuccess ||
         nb <= 0)
       nb = 1;
+    // a few resident workgroups per CU stream best; ARCHEAD_GEMV_BLOCKS_PER_CU
+    // overrides the built-in choice (tuning only)
+    int want = kGemvBlocksPerCu;
+    if (const char* e = getenv("ARCHEAD_GEMV_BLOCKS_PER_CU")) want = atoi(e) > 0 ? atoi(e) : want;
+    if (nb > want) nb = want;
     cached = nb * h->n_cu;
     mh->grid_cache[slot].store(cached, std::memory_order_relaxed);
   }
@@ -526,11 +875,15 @@ archead_status launch_stage1(const archead_handle* h, const void* x, int64_t M, 
   a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
   a.gb = d.r_r ? d.g_b : d.d; a.rr = d.r_r;
   a.t = t;
-  const int64_t waves = R * ((M + kS1Tok - 1) / kS1Tok);
-  const int64_t blocks = (waves + kWaves - 1) / kWaves;
-  hipLaunchKernelGGL(k_stage1, dim3(unsigned(blocks)), dim3(kBlock), 0, s, a);
-  hipError_t e = hipGetLastError();
-  return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "stage-1 launch");
+  for (int64_t m0 = 0; m0 < M; m0 += kMaxGridY * kS1Tok) {
+    const int64_t rest = M - m0;
+    const int64_t mblocks = (rest < kMaxGridY * kS1Tok ? rest + kS1Tok - 1 : kMaxGridY * kS1Tok) / kS1Tok;
+    a.mbase = m0;
+    hipLaunchKernelGGL(k_stage1, dim3(unsigned(R), unsigned(mblocks)), dim3(kBlock), 0, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_fail(e, "stage-1 launch");
+  }
+  return ARCHEAD_OK;
 }
 
 GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const float* t) {
@@ -546,7 +899,20 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const fl
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx;
   a.t = t;
-  a.V = d.V; a.d = d.d; a.g = d.g; a.rc = d.r_c; a.rr = d.r_r;
+  a.V = d.V; a.d = int(d.d); a.g = int(d.g); a.rc = int(d.r_c); a.rr = int(d.r_r);
+  const int64_t cpg = d.g / 32;
+  a.gshift = (cpg & (cpg - 1)) == 0 ? __builtin_ctzll(uint64_t(cpg)) : -1;
+  const int lpr = lanes_per_row(d.d);
+  const int kd = lpr >= 64 ? 1 : 2;   // ExpLanes<LPR>::KD
+  a.vec_exp = d.r_c % 4 == 0 && d.r_r % 4 == 0 && (d.r_c + d.r_r) / 4 <= int64_t(kd) * lpr &&
+              (d.r_c == 0 || aligned(h->ptrs.core_u, 4)) &&
+              (d.r_r == 0 || aligned(h->ptrs.corr_a, 4));
+  // an absent factor reads the (valid, 16-byte aligned) residual buffers with
+  // stride 0 instead; its contribution is masked to zero in the kernel
+  a.cu_stride = d.r_c; a.su_stride = d.r_c ? 1 : 0;
+  a.ca_stride = d.r_r; a.sa_stride = d.r_r ? 1 : 0;
+  if (!d.r_c) { a.cu = reinterpret_cast<const int8_t*>(a.codes); a.su = a.rs; }
+  if (!d.r_r) { a.ca = reinterpret_cast<const int8_t*>(a.codes); a.sa = a.rs; }
   const int64_t wr = gemv_rows_per_step(d);
   a.nsteps = (d.V + wr - 1) / wr;
   a.nit = int((d.d / 32) / lanes_per_row(d.d));
@@ -558,12 +924,10 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const fl
 archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M, bool ce,
                                   int64_t forced_grid, hipStream_t s) {
   const int lpr = lanes_per_row(h->desc.d);
-  void* ev0 = h->ev_start.load(std::memory_order_relaxed);
-  void* ev1 = h->ev_stop.load(std::memory_order_relaxed);
-  if (ev0) {
-    hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev0), s);
-    if (e != hipSuccess) return hip_fail(e, "timing event record");
-  }
+  // timing events (if set) are attached to the first and last dispatch
+  // packets themselves, so they bracket exactly the kernel execution
+  hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
+  hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
   for (int64_t m0 = 0; m0 < M; m0 += 4) {
     const int tok = int(M - m0 < 4 ? M - m0 : 4);
     GemvFn fn = ce ? gemv_fn<true>(tok, lpr) : gemv_fn<false>(tok, lpr);
@@ -575,13 +939,12 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
                                          hipFuncAttributeMaxDynamicSharedMemorySize, int(lds));
       if (e != hipSuccess) return hip_fail(e, "LDS size attribute");
     }
-    fn<<<dim3(unsigned(grid)), dim3(kBlock), lds, s>>>(a);
-    hipError_t e = hipGetLastError();
+    void* args[] = {&a};
+    const bool first = m0 == 0, last = m0 + 4 >= M;
+    hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(grid)),
+                                      dim3(kBlock), args, lds, s, first ? ev0 : nullptr,
+                                      last ? ev1 : nullptr, 0);
     if (e != hipSuccess) return hip_fail(e, "GEMV launch");
-  }
-  if (ev1) {
-    hipError_t e = hipEventRecord(static_cast<hipEvent_t>(ev1), s);
-    if (e != hipSuccess) return hip_fail(e, "timing event record");
   }
   return ARCHEAD_OK;
 }
