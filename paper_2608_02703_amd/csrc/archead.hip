@@ -131,6 +131,8 @@ struct Stage1Args {
   int64_t gb, rr;
   float* t;  // [M, rc + rr]
   int64_t mbase;  // first token of this launch
+  float* xs;      // [M, d/g] per-group sums of x (MFMA path), or null
+  int64_t g;
 };
 
 constexpr int kS1Tok = 8;
@@ -141,6 +143,38 @@ __global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int64_t R = a.rc + a.rr;
   const int64_t k = blockIdx.x, m0 = a.mbase + int64_t(blockIdx.y) * kS1Tok;
+  if (k >= R) {
+    // per-group sums xs[m, j] = sum over group j of x[m, i] (bias of the MFMA
+    // kernel's offset-binary unpack); one workgroup per (group, token block)
+    const int64_t j = k - R, ngrp = a.d / a.g;
+    const int ntok = int(a.M - m0 < kS1Tok ? a.M - m0 : kS1Tok);
+    float acc[kS1Tok];
+#pragma unroll
+    for (int tt = 0; tt < kS1Tok; ++tt) acc[tt] = 0.f;
+    for (int64_t i = j * a.g + int64_t(threadIdx.x) * 8; i < (j + 1) * a.g; i += kBlock * 8) {
+#pragma unroll
+      for (int tt = 0; tt < kS1Tok; ++tt) {
+        if (tt < ntok) {
+          const uint4 xv = *reinterpret_cast<const uint4*>(a.x + (m0 + tt) * a.ldx + i);
+          acc[tt] += (bf16_lo(xv.x) + bf16_hi(xv.x)) + (bf16_lo(xv.y) + bf16_hi(xv.y)) +
+                     (bf16_lo(xv.z) + bf16_hi(xv.z)) + (bf16_lo(xv.w) + bf16_hi(xv.w));
+        }
+      }
+    }
+#pragma unroll
+    for (int tt = 0; tt < kS1Tok; ++tt) {
+      const float v = seg_sum<64>(acc[tt]);
+      if (lane == 0) red[wid][tt] = v;
+    }
+    __syncthreads();
+    if (threadIdx.x < ntok) {
+      const int tt = threadIdx.x;
+      float v = red[0][tt];
+      for (int w = 1; w < kWaves; ++w) v += red[w][tt];
+      a.xs[(m0 + tt) * ngrp + j] = v;
+    }
+    return;
+  }
   const bool core = k < a.rc;
   const int8_t* crow = core ? a.cv + k * a.d : a.cb + (k - a.rc) * a.d;
   const int64_t grp = core ? a.gv : a.gb;
@@ -693,6 +727,330 @@ void k_gemv(GemvArgs a) {
   }
 }
 
+// ------------------------------------------------------------ prefill MFMA
+// Tiled bf16 MFMA kernel for many tokens.  A workgroup owns a kTM x kTN tile
+// (tokens x vocabulary rows); its four waves own 64 x 64 quarters, each a
+// 4 x 4 grid of 16x16 MFMA tiles (v_mfma_f32_16x16x32_bf16: A lane l holds
+// row l%16, k = 8 (l/16) .. +7; B likewise by column; D lane l holds rows
+// 4 (l/16) .. +3 of column l%16).  The K loop runs over d in stages of KS
+// elements staged in double-buffered LDS (rows padded so fragment reads are
+// bank-conflict free).  Codes are unpacked to bf16 (136 + c) per wave; the
+// MFMA of the first chunk of every scale group starts from -136 * (sum of x
+// over the group), so the group partial is sum c x; the fp32 group scale then
+// multiplies it into the accumulator.  The rank-r expansion runs as extra
+// K-chunks with t split into three bf16 parts (hi + mid + lo = t to fp32
+// precision) against the int8 codes (exact in bf16), scaled by s_U / s_A.
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+constexpr int kTM = 128, kTN = 128;
+
+struct MfmaArgs {
+  const uint8_t* codes;
+  const uint16_t* rs;
+  const int8_t* cu;
+  const uint16_t* su;
+  const int8_t* ca;
+  const uint16_t* sa;
+  const uint16_t* x;
+  int64_t ldx;
+  const float* t;    // [M, rc + rr]
+  const float* xs;   // [M, d/g]
+  int64_t M, V;
+  int d, g, rc, rr;
+  int64_t n_vt, n_tiles, tiles_per_xcd;
+  void* out;
+  int64_t ldo;
+  int out_bf16;
+  const void* tgt;
+  int tgt64;
+  float2* part;      // [M, n_vt]
+  float* tgt_logit;  // [M]
+};
+
+__device__ __forceinline__ bf16x8_t unpack8(uint32_t q, uint32_t kMask, uint32_t kMagic) {
+  uint32_t p[4];
+  p[0] = int4_pair<0>(q, kMask, kMagic);
+  p[1] = int4_pair<1>(q, kMask, kMagic);
+  p[2] = int4_pair<2>(q, kMask, kMagic);
+  p[3] = int4_pair<3>(q, kMask, kMagic);
+  return __builtin_bit_cast(bf16x8_t, p);
+}
+
+template <int KS, bool CE>
+__global__ __launch_bounds__(kBlock) void k_mfma(MfmaArgs a) {
+  constexpr int KC = KS / 32;            // MFMA K-chunks per stage
+  constexpr int XROW = KS + 8;           // bf16 per LDS x row (16 bytes of padding)
+  constexpr int CROW = KS / 2 + 16;      // bytes per LDS code row (16 bytes of padding)
+  constexpr int XBUF = kTM * XROW * 2;   // bytes of one x buffer
+  constexpr int CBUF = kTN * CROW;       // bytes of one code buffer
+  constexpr int TROW = 32 + 4;           // floats per LDS t row (expansion)
+  constexpr int EROW = 32 + 8;           // bf16 per LDS expansion-code row
+  constexpr int TBYTES = kTM * TROW * 4, EBYTES = kTN * EROW * 2;   // expansion staging
+  constexpr int POOL = 2 * XBUF + 2 * CBUF > TBYTES + EBYTES ? 2 * XBUF + 2 * CBUF
+                                                              : TBYTES + EBYTES;
+  __shared__ __align__(16) unsigned char lds[POOL];
+  __shared__ float sscale[2][kTN];
+  __shared__ float sbias[2][kTM];
+  __shared__ int64_t sy[kTM];
+  __shared__ float2 sred[2][kTM];
+
+  // tile: workgroups are dealt to the 8 XCDs round-robin; give each XCD a
+  // contiguous run of tiles (vocabulary tiles fastest) so concurrent tiles on
+  // one XCD share the same token rows in its L2
+  const int64_t b = blockIdx.x;
+  const int64_t lin = (b % 8) * a.tiles_per_xcd + b / 8;
+  if (lin >= a.n_tiles) return;
+  const int64_t mt = lin / a.n_vt, vt = lin - mt * a.n_vt;
+  const int64_t m0 = mt * kTM, v0 = vt * kTN;
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wid >> 1, wn = wid & 1;
+  const int lr = lane & 15, lq = lane >> 4;
+  const uint32_t kMask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
+  const uint32_t kMagic = __builtin_amdgcn_readfirstlane(0x43004300u);
+  const int ngrp = a.d / a.g;
+  const int64_t rowbytes = a.d / 2;
+  const int R = a.rc + a.rr;
+
+  f32x4_t acc[4][4], D[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  // ---- staging of one K stage: x [kTM x KS] bf16 and codes [kTN x KS/2]
+  constexpr int XU = kTM * KS / 8 / kBlock;   // 16-byte x units per thread
+  constexpr int CU = kTN * KS / 2 / 16;       // 16-byte code units in all
+  uint4 rx[XU], rcd;
+  auto gload = [&](int stage) {
+    const int64_t k0 = int64_t(stage) * KS;
+#pragma unroll
+    for (int j = 0; j < XU; ++j) {
+      const int u = tid + j * kBlock, r = u / (KS / 8), c8 = u % (KS / 8);
+      const int64_t m = m0 + r < a.M ? m0 + r : a.M - 1;
+      rx[j] = *reinterpret_cast<const uint4*>(a.x + m * a.ldx + k0 + 8 * c8);
+    }
+    if (tid < CU) {
+      const int r = tid / (KS / 32), c16 = tid % (KS / 32);
+      const int64_t v = v0 + r < a.V ? v0 + r : a.V - 1;
+      rcd = *reinterpret_cast<const uint4*>(a.codes + v * rowbytes + k0 / 2 + 16 * c16);
+    }
+  };
+  auto lstore = [&](int buf) {
+    uint16_t* sx = reinterpret_cast<uint16_t*>(lds + buf * XBUF);
+#pragma unroll
+    for (int j = 0; j < XU; ++j) {
+      const int u = tid + j * kBlock, r = u / (KS / 8), c8 = u % (KS / 8);
+      *reinterpret_cast<uint4*>(sx + r * XROW + 8 * c8) = rx[j];
+    }
+    if (tid < CU) {
+      const int r = tid / (KS / 32), c16 = tid % (KS / 32);
+      *reinterpret_cast<uint4*>(lds + 2 * XBUF + buf * CBUF + r * CROW + 16 * c16) = rcd;
+    }
+  };
+  // scale group j: scales of the tile's columns and -136 * xs of its rows
+  float gsc = 0.f, gbi = 0.f;
+  auto gload_group = [&](int j) {
+    if (tid < kTN) {
+      const int64_t v = v0 + tid < a.V ? v0 + tid : a.V - 1;
+      gsc = f16_to_f32(a.rs[v * ngrp + j]);
+    } else {
+      const int r = tid - kTN;
+      const int64_t m = m0 + r < a.M ? m0 + r : a.M - 1;
+      gbi = -float(archead::kInt4Bias) * a.xs[m * ngrp + j];
+    }
+  };
+  auto lstore_group = [&](int j) {
+    if (tid < kTN) sscale[j & 1][tid] = gsc;
+    else sbias[j & 1][tid - kTN] = gbi;
+  };
+  if (CE && tid < kTM) {
+    const int64_t m = m0 + tid < a.M ? m0 + tid : a.M - 1;
+    sy[tid] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m]
+                      : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m]);
+  }
+
+  const int nstage = a.d / KS;
+  const int spg = a.g / KS;   // stages per scale group
+  gload(0);
+  gload_group(0);
+  lstore(0);
+  lstore_group(0);
+  __syncthreads();
+
+  for (int s = 0; s < nstage; ++s) {
+    const int buf = s & 1, grp = s / spg;
+    const bool gstart = s % spg == 0, gend = (s + 1) % spg == 0;
+    if (s + 1 < nstage) {
+      gload(s + 1);
+      if ((s + 1) % spg == 0) gload_group((s + 1) / spg);
+    }
+    const uint16_t* sx = reinterpret_cast<const uint16_t*>(lds + buf * XBUF);
+    const unsigned char* scd = lds + 2 * XBUF + buf * CBUF;
+#pragma unroll
+    for (int kc = 0; kc < KC; ++kc) {
+      bf16x8_t A[4], B[4];
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi)
+        A[mi] = *reinterpret_cast<const bf16x8_t*>(sx + (64 * wm + 16 * mi + lr) * XROW +
+                                                   kc * 32 + 8 * lq);
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni)
+        B[ni] = unpack8(*reinterpret_cast<const uint32_t*>(
+                            scd + (64 * wn + 16 * ni + lr) * CROW + kc * 16 + 4 * lq),
+                        kMask, kMagic);
+      if (gstart && kc == 0) {
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi) {
+          const float* sb = sbias[grp & 1] + 64 * wm + 16 * mi + 4 * lq;
+          const f32x4_t bias = {sb[0], sb[1], sb[2], sb[3]};
+#pragma unroll
+          for (int ni = 0; ni < 4; ++ni)
+            D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mi], B[ni], bias, 0, 0, 0);
+        }
+      } else {
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+          for (int ni = 0; ni < 4; ++ni)
+            D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mi], B[ni], D[mi][ni], 0, 0, 0);
+      }
+    }
+    if (gend) {
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni) {
+        const float sc = sscale[grp & 1][64 * wn + 16 * ni + lr];
+#pragma unroll
+        for (int mi = 0; mi < 4; ++mi) acc[mi][ni] += sc * D[mi][ni];
+      }
+    }
+    if (s + 1 < nstage) {
+      lstore(buf ^ 1);
+      if ((s + 1) % spg == 0) lstore_group((s + 1) / spg);
+    }
+    __syncthreads();
+  }
+
+  // ---- rank-r expansion: two more "groups" (core U_c, correction A_w)
+#pragma unroll 1
+  for (int part = 0; part < 2; ++part) {
+    const int r = part ? a.rr : a.rc;
+    if (r == 0) continue;
+    const int8_t* codes8 = part ? a.ca : a.cu;
+    const uint16_t* rscale = part ? a.sa : a.su;
+    const int toff = part ? a.rc : 0;
+    const int nchunk = (r + 31) / 32;
+#pragma unroll 1
+    for (int c = 0; c < nchunk; ++c) {
+      float* st = reinterpret_cast<float*>(lds);                       // [kTM][TROW]
+      __bf16* se = reinterpret_cast<__bf16*>(lds + TBYTES);            // [kTN][EROW]
+      for (int e = tid; e < kTM * 32; e += kBlock) {
+        const int row = e >> 5, k = e & 31, kk = c * 32 + k;
+        const int64_t m = m0 + row < a.M ? m0 + row : a.M - 1;
+        st[row * TROW + k] = kk < r ? a.t[m * R + toff + kk] : 0.f;
+      }
+      for (int e = tid; e < kTN * 32; e += kBlock) {
+        const int col = e >> 5, k = e & 31, kk = c * 32 + k;
+        const int64_t v = v0 + col < a.V ? v0 + col : a.V - 1;
+        se[col * EROW + k] = kk < r ? (__bf16)float(codes8[v * r + kk]) : (__bf16)0.f;
+      }
+      __syncthreads();
+      bf16x8_t B[4];
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni)
+        B[ni] = *reinterpret_cast<const bf16x8_t*>(se + (64 * wn + 16 * ni + lr) * EROW + 8 * lq);
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) {
+        const float* tp = st + (64 * wm + 16 * mi + lr) * TROW + 8 * lq;
+        bf16x8_t hi, mid, lo;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float v = tp[j];
+          const __bf16 h = (__bf16)v;
+          const float r1 = v - float(h);
+          const __bf16 m_ = (__bf16)r1;
+          hi[j] = h;
+          mid[j] = m_;
+          lo[j] = (__bf16)(r1 - float(m_));
+        }
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          f32x4_t dd = c == 0 ? f32x4_t{0.f, 0.f, 0.f, 0.f} : D[mi][ni];
+          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, B[ni], dd, 0, 0, 0);
+          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, B[ni], dd, 0, 0, 0);
+          D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, B[ni], dd, 0, 0, 0);
+        }
+      }
+      __syncthreads();
+    }
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) {
+      const int64_t v = v0 + 64 * wn + 16 * ni + lr;
+      const float sc = f16_to_f32(rscale[v < a.V ? v : a.V - 1]);
+#pragma unroll
+      for (int mi = 0; mi < 4; ++mi) acc[mi][ni] += sc * D[mi][ni];
+    }
+  }
+
+  // ---- epilogue
+  if constexpr (!CE) {
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int64_t m = m0 + 64 * wm + 16 * mi + 4 * lq + i;
+        if (m >= a.M) continue;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int64_t v = v0 + 64 * wn + 16 * ni + lr;
+          if (v >= a.V) continue;
+          const float l = acc[mi][ni][i];
+          if (a.out_bf16)
+            reinterpret_cast<uint16_t*>(a.out)[m * a.ldo + v] = f32_to_bf16_rne(l);
+          else
+            reinterpret_cast<float*>(a.out)[m * a.ldo + v] = l;
+        }
+      }
+  } else {
+    // per-row (max, sum exp) over this tile's valid columns; the 16 lanes of a
+    // quarter-wave share rows, the two waves of a row half are merged in LDS
+#pragma unroll
+    for (int mi = 0; mi < 4; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int rloc = 64 * wm + 16 * mi + 4 * lq + i;
+        float mx = -INFINITY;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int64_t v = v0 + 64 * wn + 16 * ni + lr;
+          if (v < a.V) mx = fmaxf(mx, acc[mi][ni][i]);
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        float se = 0.f;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int64_t v = v0 + 64 * wn + 16 * ni + lr;
+          if (v < a.V) {
+            se += fast_exp(acc[mi][ni][i] - mx);
+            if (v == sy[rloc] && m0 + rloc < a.M) a.tgt_logit[m0 + rloc] = acc[mi][ni][i];
+          }
+        }
+#pragma unroll
+        for (int off = 1; off < 16; off <<= 1) se += __shfl_xor(se, off, 64);
+        if (lr == 0) sred[wn][rloc] = make_float2(mx, se);
+      }
+    __syncthreads();
+    if (tid < kTM && m0 + tid < a.M) {
+      float m_ = sred[0][tid].x, s_ = sred[0][tid].y;
+      lse_merge(m_, s_, sred[1][tid].x, sred[1][tid].y);
+      a.part[(m0 + tid) * a.n_vt + vt] = make_float2(m_, s_);
+    }
+  }
+}
+
 // ---------------------------------------------------------------- CE merge
 // ce[m] = MX + ln S - l[m, y_m], combining the per-tile (max, sum exp) pairs
 // in a fixed order (strided per thread, then a fixed tree) so the result is
@@ -818,16 +1176,23 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
   if (!h || M <= 0) return w;
   const archead_desc& d = h->desc;
   size_t off = 0;
+  const bool gemv = use_gemv(h, M);
   w.t_off = off;
   off = align256(off + sizeof(float) * size_t(M) * size_t(d.r_c + d.r_r));
   w.xs_off = off;
+  if (!gemv) off = align256(off + sizeof(float) * size_t(M) * size_t(d.d / d.g));
   if (op == ARCHEAD_OP_LOGITS_CE) {
-    // all CE passes share one grid (the smallest of the variants used) so
-    // every token row of the partials has the same number of slots
+    // GEMV: all CE passes share one grid (the smallest of the variants
+    // used) so every token row of the partials has the same number of
+    // slots.  MFMA: one slot per vocabulary tile.
     int64_t np = 0;
-    const int64_t full = M / 4, rem = M % 4;
-    if (full) np = gemv_grid(h, 4, true);
-    if (rem) { const int64_t g = gemv_grid(h, int(rem), true); np = (np == 0 || g < np) ? g : np; }
+    if (gemv) {
+      const int64_t full = M / 4, rem = M % 4;
+      if (full) np = gemv_grid(h, 4, true);
+      if (rem) { const int64_t g = gemv_grid(h, int(rem), true); np = (np == 0 || g < np) ? g : np; }
+    } else {
+      np = (d.V + kTN - 1) / kTN;
+    }
     w.n_part = np;
     w.part_off = off;
     off = align256(off + 2 * sizeof(float) * size_t(M) * size_t(np));
@@ -861,10 +1226,11 @@ archead_status check_call(const archead_handle* h, const void* x, int64_t M, int
 }
 
 archead_status launch_stage1(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
-                             float* t, hipStream_t s) {
+                             float* t, float* xs, hipStream_t s) {
   const archead_desc& d = h->desc;
   const int64_t R = d.r_c + d.r_r;
-  if (R == 0) return ARCHEAD_OK;
+  const int64_t nx = xs ? d.d / d.g : 0;   // extra workgroups for the group sums
+  if (R + nx == 0) return ARCHEAD_OK;
   Stage1Args a;
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx; a.M = M; a.d = d.d;
@@ -875,11 +1241,13 @@ archead_status launch_stage1(const archead_handle* h, const void* x, int64_t M, 
   a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
   a.gb = d.r_r ? d.g_b : d.d; a.rr = d.r_r;
   a.t = t;
+  a.xs = xs;
+  a.g = d.g;
   for (int64_t m0 = 0; m0 < M; m0 += kMaxGridY * kS1Tok) {
     const int64_t rest = M - m0;
     const int64_t mblocks = (rest < kMaxGridY * kS1Tok ? rest + kS1Tok - 1 : kMaxGridY * kS1Tok) / kS1Tok;
     a.mbase = m0;
-    hipLaunchKernelGGL(k_stage1, dim3(unsigned(R), unsigned(mblocks)), dim3(kBlock), 0, s, a);
+    hipLaunchKernelGGL(k_stage1, dim3(unsigned(R + nx), unsigned(mblocks)), dim3(kBlock), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "stage-1 launch");
   }
@@ -947,6 +1315,43 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
     if (e != hipSuccess) return hip_fail(e, "GEMV launch");
   }
   return ARCHEAD_OK;
+}
+
+MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
+                   const float* t, const float* xs) {
+  const archead_desc& d = h->desc;
+  MfmaArgs a;
+  memset(&a, 0, sizeof a);
+  a.codes = static_cast<const uint8_t*>(h->ptrs.res_codes);
+  a.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
+  a.cu = static_cast<const int8_t*>(h->ptrs.core_u);
+  a.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
+  a.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
+  a.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
+  a.x = static_cast<const uint16_t*>(x);
+  a.ldx = ldx;
+  a.t = t;
+  a.xs = xs;
+  a.M = M; a.V = d.V;
+  a.d = int(d.d); a.g = int(d.g); a.rc = int(d.r_c); a.rr = int(d.r_r);
+  a.n_vt = (d.V + kTN - 1) / kTN;
+  a.n_tiles = a.n_vt * ((M + kTM - 1) / kTM);
+  a.tiles_per_xcd = (a.n_tiles + 7) / 8;
+  return a;
+}
+
+archead_status launch_mfma(const archead_handle* h, MfmaArgs a, bool ce, hipStream_t s) {
+  using Fn = void (*)(MfmaArgs);
+  const bool k64 = a.g % 64 == 0;
+  Fn fn = ce ? (k64 ? k_mfma<64, true> : k_mfma<32, true>)
+             : (k64 ? k_mfma<64, false> : k_mfma<32, false>);
+  hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
+  hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
+  void* args[] = {&a};
+  hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void*>(fn),
+                                    dim3(unsigned(8 * a.tiles_per_xcd)), dim3(kBlock), args, 0,
+                                    s, ev0, ev1, 0);
+  return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "MFMA launch");
 }
 
 }  // namespace
@@ -1022,7 +1427,17 @@ archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
   hipStream_t s = static_cast<hipStream_t>(stream);
   const WsLayout w = ws_layout(h, M, ARCHEAD_OP_LOGITS);
   float* t = reinterpret_cast<float*>(static_cast<char*>(ws) + w.t_off);
-  st = launch_stage1(h, x, M, ldx, t, s);
+  if (!use_gemv(h, M)) {
+    float* xs = reinterpret_cast<float*>(static_cast<char*>(ws) + w.xs_off);
+    st = launch_stage1(h, x, M, ldx, t, xs, s);
+    if (st != ARCHEAD_OK) return st;
+    MfmaArgs a = mfma_args(h, x, M, ldx, t, xs);
+    a.out = out;
+    a.ldo = ldo;
+    a.out_bf16 = out_dtype == ARCHEAD_BF16;
+    return launch_mfma(h, a, false, s);
+  }
+  st = launch_stage1(h, x, M, ldx, t, nullptr, s);
   if (st != ARCHEAD_OK) return st;
   GemvArgs a = gemv_args(h, x, ldx, t);
   a.out = out;
@@ -1049,19 +1464,31 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t
   float* t = reinterpret_cast<float*>(base + w.t_off);
   float2* part = reinterpret_cast<float2*>(base + w.part_off);
   float* tl = reinterpret_cast<float*>(base + w.tgt_off);
-  st = launch_stage1(h, x, M, ldx, t, s);
-  if (st != ARCHEAD_OK) return st;
-  GemvArgs a = gemv_args(h, x, ldx, t);
-  a.tgt = targets;
-  a.tgt64 = tgt_dtype == ARCHEAD_I64;
-  a.part = part;
-  a.n_part = w.n_part;
-  a.tgt_logit = tl;
   const int64_t n_part = w.n_part;
-  st = launch_gemv_passes(h, a, M, true, n_part, s);
+  if (!use_gemv(h, M)) {
+    float* xs = reinterpret_cast<float*>(base + w.xs_off);
+    st = launch_stage1(h, x, M, ldx, t, xs, s);
+    if (st != ARCHEAD_OK) return st;
+    MfmaArgs a = mfma_args(h, x, M, ldx, t, xs);
+    a.tgt = targets;
+    a.tgt64 = tgt_dtype == ARCHEAD_I64;
+    a.part = part;
+    a.tgt_logit = tl;
+    st = launch_mfma(h, a, true, s);
+  } else {
+    st = launch_stage1(h, x, M, ldx, t, nullptr, s);
+    if (st != ARCHEAD_OK) return st;
+    GemvArgs a = gemv_args(h, x, ldx, t);
+    a.tgt = targets;
+    a.tgt64 = tgt_dtype == ARCHEAD_I64;
+    a.part = part;
+    a.n_part = n_part;
+    a.tgt_logit = tl;
+    st = launch_gemv_passes(h, a, M, true, n_part, s);
+  }
   if (st != ARCHEAD_OK) return st;
   hipLaunchKernelGGL(k_ce_merge, dim3(unsigned(M)), dim3(kBlock), 0, s, part, n_part, targets,
-                     int(a.tgt64), tl, h->desc.V, ce);
+                     int(tgt_dtype == ARCHEAD_I64), tl, h->desc.V, ce);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "CE merge launch");
   if (mean_ce) {

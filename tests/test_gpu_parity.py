@@ -289,3 +289,65 @@ def test_error_paths_on_device():
                 ws.data_ptr(), ws.numel()) == ab.E_INVALID_ARG
     assert L.archead_last_error()
     torch.cuda.synchronize()
+
+
+# ------------------------------------------------------------- forced paths
+
+@pytest.mark.parametrize("cfg,M", [("tiny", 8), ("qwen_decode", 16), ("gemma", 8)])
+def test_gemv_and_mfma_paths_both_match_oracle(cfg, M):
+    """The same tokens through the decode GEMV (forced for any M) and the
+    MFMA kernel (forced for any M): both within tolerance of the oracle."""
+    Mmax = max(CONFIGS[cfg]["Ms"])
+    ref = cached_oracle_logits(cfg, Mmax)[:M]
+    ph = packed(cfg)
+    x = make_x(cfg, Mmax)[:M]
+    y = make_targets(cfg, M)
+    ref_ce = ohead.cross_entropy(ref, y)
+    try:
+        for name, thr in (("gemv", 10 ** 9), ("mfma", 0)):
+            ph.set_gemv_max_m(thr)
+            say(f"{cfg} M={M} forced {name}")
+            assert_logits_close(gpu_logits(ph, x), ref, what=f"{cfg} M={M} {name}")
+            ce, mean = gpu_ce(ph, x, y)
+            assert_ce_close(ce, ref_ce, what=f"{cfg} M={M} {name} CE")
+    finally:
+        ph.set_gemv_max_m(-1)
+
+
+def test_identity_probe_gemv_forced_bit_exact():
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", rc=0, rr=0)
+    ph = PackedHead.from_arrays(h)
+    ph.set_gemv_max_m(10 ** 9)
+    eye = np.zeros((h.d, h.d), dtype=np.uint16)
+    eye[np.arange(h.d), np.arange(h.d)] = 0x3F80
+    lg = gpu_logits(ph, eye[:96])
+    ref = ohead.logits(h, eye[:96])
+    assert np.array_equal(lg.astype(np.float64), ref)
+    ph.close()
+
+
+@pytest.mark.parametrize("V,d,g,M", [(1000, 512, 64, 130), (777, 256, 32, 33),
+                                     (300, 1024, 256, 5)])
+def test_mfma_ragged_tiles(V, d, g, M):
+    """Token and vocabulary counts that leave partial MFMA tiles; ranks that
+    are not multiples of 32; row strides wider than the rows."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", V=V, d=d, g=g, rc=40, rr=12)
+    x = make_x("tiny", M, d=d, basis="identity")
+    ph = PackedHead.from_arrays(h)
+    ph.set_gemv_max_m(0)
+    ref = ohead.logits(h, x)
+    say(f"mfma ragged V={V} d={d} g={g} M={M}")
+    assert_logits_close(gpu_logits(ph, x, ld=d + 16), ref, what="mfma ragged")
+    out = torch.full((M, V + 5), 3.0, device="cuda")
+    ph.logits(torch_x(x), out=out[:, :V])
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert (o[:, V:] == 3.0).all(), "wrote past the row"
+    y = (np.arange(M) * 13 % V).astype(np.int64)
+    ce, mean = gpu_ce(ph, x, y, dtype=torch.int64)
+    assert_ce_close(ce, ohead.cross_entropy(ref, y), what="mfma ragged CE")
+    bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
+    assert_bf16_output(bits, o[:, :V], ref, "mfma ragged bf16")
+    ph.close()
