@@ -20,6 +20,7 @@
 #include <math.h>
 #include <stdlib.h>
 
+#include <algorithm>
 #include <type_traits>
 #include <stdint.h>
 #include <string.h>
@@ -31,6 +32,7 @@ namespace {
 
 typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // 16-byte streaming load (read once: non-temporal hint).
 __device__ __forceinline__ uint4 load_stream16(const uint8_t* p) {
@@ -115,8 +117,8 @@ __device__ __forceinline__ float seg_sum(float v) {
 }
 
 // ------------------------------------------------------------------ stage 1
-// t[m, k] = sum_i (s[k, i/grp] c[k, i]) x[m, i] for the rows k of V_c (k <
-// r_c) then of B_w.  One workgroup per (k, block of 8 tokens): the 256
+// (decode path) t[m, k] = sum_i (s[k, i/grp] c[k, i]) x[m, i] for the rows k
+// of V_c (k < r_c) then of B_w.  One workgroup per (k, block of 8 tokens): the 256
 // threads split d in 8-element pieces, every load of the row is issued before
 // the arithmetic, and the block sums the 256 partials.  s * c is exact in fp32
 // (11 x 8 significant bits).
@@ -131,8 +133,6 @@ struct Stage1Args {
   int64_t gb, rr;
   float* t;  // [M, rc + rr]
   int64_t mbase;  // first token of this launch
-  float* xs;      // [M, d/g] per-group sums of x (MFMA path), or null
-  int64_t g;
 };
 
 constexpr int kS1Tok = 8;
@@ -143,38 +143,6 @@ __global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
   const int64_t R = a.rc + a.rr;
   const int64_t k = blockIdx.x, m0 = a.mbase + int64_t(blockIdx.y) * kS1Tok;
-  if (k >= R) {
-    // per-group sums xs[m, j] = sum over group j of x[m, i] (bias of the MFMA
-    // kernel's offset-binary unpack); one workgroup per (group, token block)
-    const int64_t j = k - R, ngrp = a.d / a.g;
-    const int ntok = int(a.M - m0 < kS1Tok ? a.M - m0 : kS1Tok);
-    float acc[kS1Tok];
-#pragma unroll
-    for (int tt = 0; tt < kS1Tok; ++tt) acc[tt] = 0.f;
-    for (int64_t i = j * a.g + int64_t(threadIdx.x) * 8; i < (j + 1) * a.g; i += kBlock * 8) {
-#pragma unroll
-      for (int tt = 0; tt < kS1Tok; ++tt) {
-        if (tt < ntok) {
-          const uint4 xv = *reinterpret_cast<const uint4*>(a.x + (m0 + tt) * a.ldx + i);
-          acc[tt] += (bf16_lo(xv.x) + bf16_hi(xv.x)) + (bf16_lo(xv.y) + bf16_hi(xv.y)) +
-                     (bf16_lo(xv.z) + bf16_hi(xv.z)) + (bf16_lo(xv.w) + bf16_hi(xv.w));
-        }
-      }
-    }
-#pragma unroll
-    for (int tt = 0; tt < kS1Tok; ++tt) {
-      const float v = seg_sum<64>(acc[tt]);
-      if (lane == 0) red[wid][tt] = v;
-    }
-    __syncthreads();
-    if (threadIdx.x < ntok) {
-      const int tt = threadIdx.x;
-      float v = red[0][tt];
-      for (int w = 1; w < kWaves; ++w) v += red[w][tt];
-      a.xs[(m0 + tt) * ngrp + j] = v;
-    }
-    return;
-  }
   const bool core = k < a.rc;
   const int8_t* crow = core ? a.cv + k * a.d : a.cb + (k - a.rc) * a.d;
   const int64_t grp = core ? a.gv : a.gb;
@@ -727,46 +695,93 @@ void k_gemv(GemvArgs a) {
   }
 }
 
-// ------------------------------------------------------------ prefill MFMA
-// Tiled bf16 MFMA kernel for many tokens.  A workgroup owns a kTM x kTN tile
-// (tokens x vocabulary rows); its four waves own 64 x 64 quarters, each a
-// 4 x 4 grid of 16x16 MFMA tiles (v_mfma_f32_16x16x32_bf16: A lane l holds
-// row l%16, k = 8 (l/16) .. +7; B likewise by column; D lane l holds rows
-// 4 (l/16) .. +3 of column l%16).  The K loop runs over d in stages of KS
-// elements staged in double-buffered LDS (rows padded so fragment reads are
-// bank-conflict free).  Codes are unpacked to bf16 (136 + c) per wave; the
-// MFMA of the first chunk of every scale group starts from -136 * (sum of x
-// over the group), so the group partial is sum c x; the fp32 group scale then
-// multiplies it into the accumulator.  The rank-r expansion runs as extra
-// K-chunks with t split into three bf16 parts (hi + mid + lo = t to fp32
-// precision) against the int8 codes (exact in bf16), scaled by s_U / s_A.
+// ------------------------------------------------------------ many tokens: MFMA
+// Tiled bf16 MFMA path for many tokens.  A workgroup owns a kTM x kTN tile
+// (tokens x vocabulary rows); its eight waves own 64 x 64 blocks (2 along
+// the tokens, 4 along the vocabulary), each a 4 x 4 grid of 16x16 MFMA tiles
+// (v_mfma_f32_16x16x32_bf16: A lane l holds row l%16 and 8 k-slots of quarter
+// l/16; B likewise by column; D lane l holds rows 4 (l/16) .. +3 of column
+// l%16).  The K loop runs over d in stages of KS elements that direct
+// global-to-LDS buffer loads bring into a ring of kRing LDS stages, two
+// stages ahead of the compute, with no register staging.  Within a stage the
+// k-slots are assigned so that one lane's code dwords are contiguous: lane
+// quarter q takes code dwords q*KC .. q*KC+KC-1 of the stage (one per MFMA
+// K-chunk) and the x chunks with the same indices.  Token rows and
+// vocabulary rows are XOR-swizzled in 16-byte units so fragment reads are
+// bank-conflict free.
+//
+// Codes are unpacked per wave to bf16 (136 + c) (exact).  The MFMA of the
+// first K-chunk of each scale group starts from the group bias
+// -136 * (sum of x over the group), so the group partial is sum c x; at the
+// end of the group its fp32 scale multiplies the partial into the
+// accumulator.  The rank-r expansion runs as extra K-chunks with t split
+// into three bf16 parts (hi + mid + lo = t to fp32 precision) against the
+// int8 codes (exact in bf16), scaled by s_U / s_A.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
-constexpr int kTM = 128, kTN = 128;
+constexpr int kTM = 128, kTN = 256;          // tile: tokens x vocabulary rows
+constexpr int kMBlock = 512, kMWaves = 8;    // 2 x 4 waves of 64 x 64
+constexpr int kRing = 3;                     // LDS stages (two loads in flight)
+constexpr int kRasterGM = 4;                 // token tiles per raster group
+constexpr int kExpRow = 40;                  // bf16 per padded LDS row (expansion)
+constexpr int kExpBytes = (3 * kTM + kTN) * kExpRow * 2;
 
-struct MfmaArgs {
-  const uint8_t* codes;
-  const uint16_t* rs;
-  const int8_t* cu;
-  const uint16_t* su;
-  const int8_t* ca;
-  const uint16_t* sa;
-  const uint16_t* x;
-  int64_t ldx;
-  const float* t;    // [M, rc + rr]
-  const float* xs;   // [M, d/g]
-  int64_t M, V;
-  int d, g, rc, rr;
-  int64_t n_vt, n_tiles, tiles_per_xcd;
-  void* out;
-  int64_t ldo;
-  int out_bf16;
-  const void* tgt;
-  int tgt64;
-  float2* part;      // [M, n_vt]
-  float* tgt_logit;  // [M]
+template <int KS>
+struct MGeom {
+  static constexpr int KC = KS / 32;                  // MFMA K-chunks per stage
+  static constexpr int XBYTES = kTM * KS * 2;         // x [kTM][KS] bf16
+  static constexpr int CBYTES = kTN * KS / 2;         // codes [kTN][KS/2]
+  static constexpr int SCL = XBYTES + CBYTES;         // fp16 [kTN] group scales
+  static constexpr int BIAS = SCL + kTN * 2;          // fp32 [kTM] group biases
+  static constexpr int STAGE = BIAS + kTM * 4;
+  static constexpr int NX = XBYTES / 1024 / kMWaves;  // x loads per wave and stage
+  static constexpr int NC = CBYTES / 1024;            // code loads per workgroup and stage
+  static constexpr int NCW = NC >= kMWaves ? NC / kMWaves : 0;
+  static constexpr int NL = NX + NCW + 1;             // loads per wave and stage
+  static constexpr int RING = kRing * STAGE;
+  static constexpr int LDS = RING > kExpBytes ? RING : kExpBytes;
+  static_assert(NC >= kMWaves || NC == kMWaves / 2, "code loads must spread evenly");
+  static_assert(LDS <= 160 * 1024, "LDS budget");
 };
+
+// 16-byte unit swizzles (argument: row within the tile; only its low four
+// bits matter, so every lane's swizzle is fixed for all its fragments)
+template <int KS>
+__device__ __forceinline__ int swz_x(int r) {
+  if constexpr (KS == 128) return r & 15;
+  else if constexpr (KS == 64) return ((r & 15) ^ ((r & 15) >> 3)) & 7;
+  else return ((r >> 1) ^ (r >> 2)) & 3;
+}
+template <int KS>
+__device__ __forceinline__ int swz_c(int c) {
+  if constexpr (KS == 128) return ((c >> 1) ^ (c >> 2)) & 3;
+  else if constexpr (KS == 64) return (c >> 2) & 1;
+  else return 0;
+}
+
+__device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_u8* dst, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      r, reinterpret_cast<__attribute__((address_space(3))) void*>(dst), 16, voff, 0, 0, 0);
+}
+__device__ __forceinline__ void dma4(__amdgpu_buffer_rsrc_t r, lds_u8* dst, uint32_t voff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(
+      r, reinterpret_cast<__attribute__((address_space(3))) void*>(dst), 4, voff, 0, 0, 0);
+}
+
+// Wait until at most N of this wave's vector-memory loads are in flight and
+// its LDS reads are done, then meet the other waves.  The memory clobber
+// keeps LDS accesses on their side of it.
+template <int N>
+__device__ __forceinline__ void wait_loads_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+template <typename T>
+__device__ __forceinline__ T lds_load(const lds_u8* p) {
+  return *reinterpret_cast<const __attribute__((address_space(3))) T*>(p);
+}
 
 __device__ __forceinline__ bf16x8_t unpack8(uint32_t q, uint32_t kMask, uint32_t kMagic) {
   uint32_t p[4];
@@ -777,135 +792,182 @@ __device__ __forceinline__ bf16x8_t unpack8(uint32_t q, uint32_t kMask, uint32_t
   return __builtin_bit_cast(bf16x8_t, p);
 }
 
-template <int KS, bool CE>
-__global__ __launch_bounds__(kBlock) void k_mfma(MfmaArgs a) {
-  constexpr int KC = KS / 32;            // MFMA K-chunks per stage
-  constexpr int XROW = KS + 8;           // bf16 per LDS x row (16 bytes of padding)
-  constexpr int CROW = KS / 2 + 16;      // bytes per LDS code row (16 bytes of padding)
-  constexpr int XBUF = kTM * XROW * 2;   // bytes of one x buffer
-  constexpr int CBUF = kTN * CROW;       // bytes of one code buffer
-  constexpr int TROW = 32 + 4;           // floats per LDS t row (expansion)
-  constexpr int EROW = 32 + 8;           // bf16 per LDS expansion-code row
-  constexpr int TBYTES = kTM * TROW * 4, EBYTES = kTN * EROW * 2;   // expansion staging
-  constexpr int POOL = 2 * XBUF + 2 * CBUF > TBYTES + EBYTES ? 2 * XBUF + 2 * CBUF
-                                                              : TBYTES + EBYTES;
-  __shared__ __align__(16) unsigned char lds[POOL];
-  __shared__ float sscale[2][kTN];
-  __shared__ float sbias[2][kTM];
-  __shared__ int64_t sy[kTM];
-  __shared__ float2 sred[2][kTM];
+struct MfmaArgs {
+  const uint8_t* codes;
+  const int8_t* cu;
+  const uint16_t* su;
+  const int8_t* ca;
+  const uint16_t* sa;
+  const uint16_t* x;
+  int64_t ldx;
+  const float* t;        // [M, rc + rr]
+  const float* gbias;    // [n_mt][d/g][kTM]: -136 * (sum of x over group j)
+  const uint16_t* rsT;   // [n_vt][d/g][kTN]: residual group scales, tile-major
+  int64_t M, V;
+  int d, g, rc, rr;
+  int64_t n_mt, n_vt, n_tiles, tiles_per_xcd;
+  void* out;
+  int64_t ldo;
+  int out_bf16;
+  const void* tgt;
+  int tgt64;
+  float2* part;          // [M, n_vt]
+  float* tgt_logit;      // [M]
+};
 
-  // tile: workgroups are dealt to the 8 XCDs round-robin; give each XCD a
-  // contiguous run of tiles (vocabulary tiles fastest) so concurrent tiles on
-  // one XCD share the same token rows in its L2
+template <int KS, bool CE>
+__global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
+  using G = MGeom<KS>;
+  constexpr int KC = G::KC;
+  extern __shared__ __align__(16) uint8_t mfma_lds[];
+  lds_u8* const L = (lds_u8*)mfma_lds;
+
+  // tile: workgroups are dealt to the 8 XCDs round-robin, so XCD x runs
+  // blocks x, x+8, ...; it gets the contiguous run [x T, (x+1) T) of the tile
+  // order, which walks groups of kRasterGM token tiles across the vocabulary
+  // (token tile fastest): the tiles one XCD runs at once share a few token
+  // tiles and a few vocabulary tiles in its L2
   const int64_t b = blockIdx.x;
-  const int64_t lin = (b % 8) * a.tiles_per_xcd + b / 8;
+  const int64_t lin = (b & 7) * a.tiles_per_xcd + (b >> 3);
   if (lin >= a.n_tiles) return;
-  const int64_t mt = lin / a.n_vt, vt = lin - mt * a.n_vt;
+  const int64_t gsz = int64_t(kRasterGM) * a.n_vt;
+  const int64_t rg = lin / gsz, first = rg * kRasterGM;
+  const int64_t gm = a.n_mt - first < kRasterGM ? a.n_mt - first : kRasterGM;
+  const int64_t within = lin - rg * gsz;
+  const int64_t mt = first + within % gm, vt = within / gm;
   const int64_t m0 = mt * kTM, v0 = vt * kTN;
+  const int rows = int(a.M - m0 < kTM ? a.M - m0 : kTM);
+  const int cols = int(a.V - v0 < kTN ? a.V - v0 : kTN);
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wid >> 1, wn = wid & 1;
-  const int lr = lane & 15, lq = lane >> 4;
+  const int wm = wid >> 2, wn = wid & 3;
+  const int lr = lane & 15, q = lane >> 4;
   const uint32_t kMask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
   const uint32_t kMagic = __builtin_amdgcn_readfirstlane(0x43004300u);
   const int ngrp = a.d / a.g;
-  const int64_t rowbytes = a.d / 2;
-  const int R = a.rc + a.rr;
+  const uint32_t rowbytes = uint32_t(a.d) / 2;
+  const uint32_t ldx2 = uint32_t(a.ldx) * 2;
+
+  // buffer resources over exactly the bytes this tile may touch (loads past
+  // them return zero instead of reading other memory)
+  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.x + m0 * a.ldx), 0, int((rows - 1) * ldx2 + uint32_t(a.d) * 2),
+      kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint8_t*>(a.codes + v0 * int64_t(rowbytes)), 0, int(uint32_t(cols) * rowbytes),
+      kBufferWord3);
+  const int piece = wid & 3;   // auxiliary load of this wave: scales 0-1, biases 2-3
+  const __amdgpu_buffer_rsrc_t raux =
+      piece < 2 ? __builtin_amdgcn_make_buffer_rsrc(
+                      const_cast<uint16_t*>(a.rsT + vt * ngrp * kTN), 0, ngrp * kTN * 2,
+                      kBufferWord3)
+                : __builtin_amdgcn_make_buffer_rsrc(
+                      const_cast<float*>(a.gbias + mt * ngrp * kTM), 0, ngrp * kTM * 4,
+                      kBufferWord3);
+
+  // per-lane load offsets (the stage's k offset is added per stage)
+  uint32_t xo[G::NX];
+#pragma unroll
+  for (int i = 0; i < G::NX; ++i) {
+    const int off = (wid * G::NX + i) * 1024 + 16 * lane;
+    const int r = off / (2 * KS), p = (off % (2 * KS)) / 16;
+    const int rr_ = r < rows ? r : rows - 1;
+    xo[i] = uint32_t(rr_) * ldx2 + 16u * uint32_t(p ^ swz_x<KS>(r));
+  }
+  constexpr int NCO = G::NCW > 0 ? G::NCW : 1;
+  uint32_t co[NCO];
+#pragma unroll
+  for (int i = 0; i < NCO; ++i) {
+    const int j = G::NCW > 0 ? wid * G::NCW + i : (wid & 3);
+    const int off = j * 1024 + 16 * lane;
+    const int c = off / (KS / 2), p = (off % (KS / 2)) / 16;
+    const int cc = c < cols ? c : cols - 1;
+    co[i] = uint32_t(cc) * rowbytes + 16u * uint32_t(p ^ swz_c<KS>(c));
+  }
+  uint32_t ao;
+  int adst;
+  if (piece < 2) {
+    ao = uint32_t(piece * 128 + 2 * lane) * 2;
+    adst = G::SCL + piece * 256;
+  } else {
+    const int r = (piece - 2) * 64 + lane;
+    ao = uint32_t(r < rows ? r : rows - 1) * 4;
+    adst = G::BIAS + (piece - 2) * 256;
+  }
+
+  auto issue = [&](int s, int buf, int gj) {
+    lds_u8* base = L + buf * G::STAGE;
+    const uint32_t kx = uint32_t(s) * (KS * 2), kcb = uint32_t(s) * (KS / 2);
+#pragma unroll
+    for (int i = 0; i < G::NX; ++i) dma16(rx, base + (wid * G::NX + i) * 1024, xo[i] + kx);
+    if constexpr (G::NCW > 0) {
+#pragma unroll
+      for (int i = 0; i < G::NCW; ++i)
+        dma16(rc, base + G::XBYTES + (wid * G::NCW + i) * 1024, co[i] + kcb);
+      dma4(raux, base + adst, ao + uint32_t(gj) * 512u);
+    } else {
+      if (wid < 4) dma16(rc, base + G::XBYTES + wid * 1024, co[0] + kcb);
+      else dma4(raux, base + adst, ao + uint32_t(gj) * 512u);
+    }
+  };
+
+  // fragment offsets within a stage
+  uint32_t aoff[KC];
+#pragma unroll
+  for (int kc = 0; kc < KC; ++kc)
+    aoff[kc] = uint32_t(64 * wm + lr) * (2 * KS) + 16u * uint32_t((q * KC + kc) ^ swz_x<KS>(lr));
+  uint32_t boff;
+  if constexpr (KS == 128) boff = uint32_t(64 * wn + lr) * 64 + 16u * uint32_t(q ^ swz_c<KS>(lr));
+  else if constexpr (KS == 64)
+    boff = uint32_t(64 * wn + lr) * 32 + 16u * uint32_t((q >> 1) ^ swz_c<KS>(lr)) + 8u * (q & 1);
+  else boff = uint32_t(64 * wn + lr) * 16 + 4u * q;
+  boff += G::XBYTES;
 
   f32x4_t acc[4][4], D[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f}, D[i][j] = acc[i][j];
 
-  // ---- staging of one K stage: x [kTM x KS] bf16 and codes [kTN x KS/2]
-  constexpr int XU = kTM * KS / 8 / kBlock;   // 16-byte x units per thread
-  constexpr int CU = kTN * KS / 2 / 16;       // 16-byte code units in all
-  uint4 rx[XU], rcd;
-  auto gload = [&](int stage) {
-    const int64_t k0 = int64_t(stage) * KS;
+  const int nst = a.d / KS, spg = a.g / KS;
+  issue(0, 0, 0);
+  if (nst > 1) issue(1, 1, 1 / spg);
+  int buf = 0, sg = 0;   // ring slot of stage s; stage index within its group
+#pragma unroll 1
+  for (int s = 0; s < nst; ++s) {
+    if (s + 1 < nst) wait_loads_barrier<G::NL>();
+    else wait_loads_barrier<0>();
+    if (s + 2 < nst) issue(s + 2, buf == 0 ? 2 : buf - 1, (s + 2) / spg);
+    const lds_u8* base = L + buf * G::STAGE;
+    const bool gstart = sg == 0, gend = sg == spg - 1;
+
+    uint32_t braw[4][KC];
 #pragma unroll
-    for (int j = 0; j < XU; ++j) {
-      const int u = tid + j * kBlock, r = u / (KS / 8), c8 = u % (KS / 8);
-      const int64_t m = m0 + r < a.M ? m0 + r : a.M - 1;
-      rx[j] = *reinterpret_cast<const uint4*>(a.x + m * a.ldx + k0 + 8 * c8);
+    for (int ni = 0; ni < 4; ++ni) {
+      const lds_u8* p = base + boff + ni * 16 * (KS / 2);
+      if constexpr (KC == 4) {
+        const u32x4_t v = lds_load<u32x4_t>(p);
+        braw[ni][0] = v.x; braw[ni][KC > 1 ? 1 : 0] = v.y;
+        braw[ni][KC > 2 ? 2 : 0] = v.z; braw[ni][KC > 3 ? 3 : 0] = v.w;
+      } else if constexpr (KC == 2) {
+        const u32x2_t v = lds_load<u32x2_t>(p);
+        braw[ni][0] = v.x; braw[ni][KC > 1 ? 1 : 0] = v.y;
+      } else {
+        braw[ni][0] = lds_load<uint32_t>(p);
+      }
     }
-    if (tid < CU) {
-      const int r = tid / (KS / 32), c16 = tid % (KS / 32);
-      const int64_t v = v0 + r < a.V ? v0 + r : a.V - 1;
-      rcd = *reinterpret_cast<const uint4*>(a.codes + v * rowbytes + k0 / 2 + 16 * c16);
-    }
-  };
-  auto lstore = [&](int buf) {
-    uint16_t* sx = reinterpret_cast<uint16_t*>(lds + buf * XBUF);
-#pragma unroll
-    for (int j = 0; j < XU; ++j) {
-      const int u = tid + j * kBlock, r = u / (KS / 8), c8 = u % (KS / 8);
-      *reinterpret_cast<uint4*>(sx + r * XROW + 8 * c8) = rx[j];
-    }
-    if (tid < CU) {
-      const int r = tid / (KS / 32), c16 = tid % (KS / 32);
-      *reinterpret_cast<uint4*>(lds + 2 * XBUF + buf * CBUF + r * CROW + 16 * c16) = rcd;
-    }
-  };
-  // scale group j: scales of the tile's columns and -136 * xs of its rows
-  float gsc = 0.f, gbi = 0.f;
-  auto gload_group = [&](int j) {
-    if (tid < kTN) {
-      const int64_t v = v0 + tid < a.V ? v0 + tid : a.V - 1;
-      gsc = f16_to_f32(a.rs[v * ngrp + j]);
-    } else {
-      const int r = tid - kTN;
-      const int64_t m = m0 + r < a.M ? m0 + r : a.M - 1;
-      gbi = -float(archead::kInt4Bias) * a.xs[m * ngrp + j];
-    }
-  };
-  auto lstore_group = [&](int j) {
-    if (tid < kTN) sscale[j & 1][tid] = gsc;
-    else sbias[j & 1][tid - kTN] = gbi;
-  };
-  if (CE && tid < kTM) {
-    const int64_t m = m0 + tid < a.M ? m0 + tid : a.M - 1;
-    sy[tid] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m]
-                      : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m]);
-  }
-
-  const int nstage = a.d / KS;
-  const int spg = a.g / KS;   // stages per scale group
-  gload(0);
-  gload_group(0);
-  lstore(0);
-  lstore_group(0);
-  __syncthreads();
-
-  for (int s = 0; s < nstage; ++s) {
-    const int buf = s & 1, grp = s / spg;
-    const bool gstart = s % spg == 0, gend = (s + 1) % spg == 0;
-    if (s + 1 < nstage) {
-      gload(s + 1);
-      if ((s + 1) % spg == 0) gload_group((s + 1) / spg);
-    }
-    const uint16_t* sx = reinterpret_cast<const uint16_t*>(lds + buf * XBUF);
-    const unsigned char* scd = lds + 2 * XBUF + buf * CBUF;
 #pragma unroll
     for (int kc = 0; kc < KC; ++kc) {
       bf16x8_t A[4], B[4];
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi)
-        A[mi] = *reinterpret_cast<const bf16x8_t*>(sx + (64 * wm + 16 * mi + lr) * XROW +
-                                                   kc * 32 + 8 * lq);
+      for (int mi = 0; mi < 4; ++mi) A[mi] = lds_load<bf16x8_t>(base + aoff[kc] + mi * 32 * KS);
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
-        B[ni] = unpack8(*reinterpret_cast<const uint32_t*>(
-                            scd + (64 * wn + 16 * ni + lr) * CROW + kc * 16 + 4 * lq),
-                        kMask, kMagic);
-      if (gstart && kc == 0) {
+      for (int ni = 0; ni < 4; ++ni) B[ni] = unpack8(braw[ni][kc], kMask, kMagic);
+      if (kc == 0 && gstart) {
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi) {
-          const float* sb = sbias[grp & 1] + 64 * wm + 16 * mi + 4 * lq;
-          const f32x4_t bias = {sb[0], sb[1], sb[2], sb[3]};
+          const f32x4_t bias = lds_load<f32x4_t>(base + G::BIAS + (64 * wm + 16 * mi + 4 * q) * 4);
 #pragma unroll
           for (int ni = 0; ni < 4; ++ni)
             D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mi], B[ni], bias, 0, 0, 0);
@@ -921,19 +983,19 @@ __global__ __launch_bounds__(kBlock) void k_mfma(MfmaArgs a) {
     if (gend) {
 #pragma unroll
       for (int ni = 0; ni < 4; ++ni) {
-        const float sc = sscale[grp & 1][64 * wn + 16 * ni + lr];
+        const float sc = f16_to_f32(lds_load<uint16_t>(base + G::SCL + (64 * wn + 16 * ni + lr) * 2));
 #pragma unroll
         for (int mi = 0; mi < 4; ++mi) acc[mi][ni] += sc * D[mi][ni];
       }
     }
-    if (s + 1 < nstage) {
-      lstore(buf ^ 1);
-      if ((s + 1) % spg == 0) lstore_group((s + 1) / spg);
-    }
-    __syncthreads();
+    buf = buf == 2 ? 0 : buf + 1;
+    sg = gend ? 0 : sg + 1;
   }
 
-  // ---- rank-r expansion: two more "groups" (core U_c, correction A_w)
+  // ---- rank-r expansion: the core part (U_c, t_c) then the correction (A_w, t_w)
+  const int R = a.rc + a.rr;
+  lds_u8* const TH = L;                                  // [3][kTM][kExpRow] bf16 (hi, mid, lo)
+  lds_u8* const TE = L + 3 * kTM * kExpRow * 2;          // [kTN][kExpRow] bf16 codes
 #pragma unroll 1
   for (int part = 0; part < 2; ++part) {
     const int r = part ? a.rr : a.rc;
@@ -941,54 +1003,52 @@ __global__ __launch_bounds__(kBlock) void k_mfma(MfmaArgs a) {
     const int8_t* codes8 = part ? a.ca : a.cu;
     const uint16_t* rscale = part ? a.sa : a.su;
     const int toff = part ? a.rc : 0;
-    const int nchunk = (r + 31) / 32;
 #pragma unroll 1
-    for (int c = 0; c < nchunk; ++c) {
-      float* st = reinterpret_cast<float*>(lds);                       // [kTM][TROW]
-      __bf16* se = reinterpret_cast<__bf16*>(lds + TBYTES);            // [kTN][EROW]
-      for (int e = tid; e < kTM * 32; e += kBlock) {
-        const int row = e >> 5, k = e & 31, kk = c * 32 + k;
-        const int64_t m = m0 + row < a.M ? m0 + row : a.M - 1;
-        st[row * TROW + k] = kk < r ? a.t[m * R + toff + kk] : 0.f;
+    for (int c0 = 0; c0 < r; c0 += 32) {
+      __syncthreads();
+      for (int e = tid; e < kTM * 32; e += kMBlock) {
+        const int row = e >> 5, k = e & 31, kk = c0 + k;
+        const int64_t m = row < rows ? m0 + row : a.M - 1;
+        const float v = kk < r ? a.t[m * R + toff + kk] : 0.f;
+        const __bf16 h = (__bf16)v;
+        const float r1 = v - float(h);
+        const __bf16 md = (__bf16)r1;
+        const __bf16 lo = (__bf16)(r1 - float(md));
+        const int o = (row * kExpRow + k) * 2;
+        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TH + o) = h;
+        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TH + kTM * kExpRow * 2 + o) = md;
+        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TH + 2 * kTM * kExpRow * 2 + o) = lo;
       }
-      for (int e = tid; e < kTN * 32; e += kBlock) {
-        const int col = e >> 5, k = e & 31, kk = c * 32 + k;
-        const int64_t v = v0 + col < a.V ? v0 + col : a.V - 1;
-        se[col * EROW + k] = kk < r ? (__bf16)float(codes8[v * r + kk]) : (__bf16)0.f;
+      for (int e = tid; e < kTN * 32; e += kMBlock) {
+        const int col = e >> 5, k = e & 31, kk = c0 + k;
+        const int64_t v = col < cols ? v0 + col : a.V - 1;
+        const __bf16 cv = kk < r ? (__bf16)float(codes8[v * r + kk]) : (__bf16)0.f;
+        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TE + (col * kExpRow + k) * 2) = cv;
       }
       __syncthreads();
       bf16x8_t B[4];
 #pragma unroll
       for (int ni = 0; ni < 4; ++ni)
-        B[ni] = *reinterpret_cast<const bf16x8_t*>(se + (64 * wn + 16 * ni + lr) * EROW + 8 * lq);
+        B[ni] = lds_load<bf16x8_t>(TE + ((64 * wn + 16 * ni + lr) * kExpRow + 8 * q) * 2);
 #pragma unroll
       for (int mi = 0; mi < 4; ++mi) {
-        const float* tp = st + (64 * wm + 16 * mi + lr) * TROW + 8 * lq;
-        bf16x8_t hi, mid, lo;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float v = tp[j];
-          const __bf16 h = (__bf16)v;
-          const float r1 = v - float(h);
-          const __bf16 m_ = (__bf16)r1;
-          hi[j] = h;
-          mid[j] = m_;
-          lo[j] = (__bf16)(r1 - float(m_));
-        }
+        const int o = ((64 * wm + 16 * mi + lr) * kExpRow + 8 * q) * 2;
+        const bf16x8_t hi = lds_load<bf16x8_t>(TH + o);
+        const bf16x8_t md = lds_load<bf16x8_t>(TH + kTM * kExpRow * 2 + o);
+        const bf16x8_t lo = lds_load<bf16x8_t>(TH + 2 * kTM * kExpRow * 2 + o);
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni) {
-          f32x4_t dd = c == 0 ? f32x4_t{0.f, 0.f, 0.f, 0.f} : D[mi][ni];
+          f32x4_t dd = c0 == 0 ? f32x4_t{0.f, 0.f, 0.f, 0.f} : D[mi][ni];
           dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, B[ni], dd, 0, 0, 0);
-          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(mid, B[ni], dd, 0, 0, 0);
+          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(md, B[ni], dd, 0, 0, 0);
           D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, B[ni], dd, 0, 0, 0);
         }
       }
-      __syncthreads();
     }
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) {
-      const int64_t v = v0 + 64 * wn + 16 * ni + lr;
-      const float sc = f16_to_f32(rscale[v < a.V ? v : a.V - 1]);
+      const int col = 64 * wn + 16 * ni + lr;
+      const float sc = f16_to_f32(rscale[col < cols ? v0 + col : a.V - 1]);
 #pragma unroll
       for (int mi = 0; mi < 4; ++mi) acc[mi][ni] += sc * D[mi][ni];
     }
@@ -1000,53 +1060,223 @@ __global__ __launch_bounds__(kBlock) void k_mfma(MfmaArgs a) {
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int64_t m = m0 + 64 * wm + 16 * mi + 4 * lq + i;
-        if (m >= a.M) continue;
+        const int row = 64 * wm + 16 * mi + 4 * q + i;
+        if (row >= rows) continue;
+        const int64_t m = m0 + row;
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni) {
-          const int64_t v = v0 + 64 * wn + 16 * ni + lr;
-          if (v >= a.V) continue;
+          const int col = 64 * wn + 16 * ni + lr;
+          if (col >= cols) continue;
           const float l = acc[mi][ni][i];
           if (a.out_bf16)
-            reinterpret_cast<uint16_t*>(a.out)[m * a.ldo + v] = f32_to_bf16_rne(l);
+            reinterpret_cast<uint16_t*>(a.out)[m * a.ldo + v0 + col] = f32_to_bf16_rne(l);
           else
-            reinterpret_cast<float*>(a.out)[m * a.ldo + v] = l;
+            reinterpret_cast<float*>(a.out)[m * a.ldo + v0 + col] = l;
         }
       }
   } else {
-    // per-row (max, sum exp) over this tile's valid columns; the 16 lanes of a
-    // quarter-wave share rows, the two waves of a row half are merged in LDS
+    // per token row: (max, sum exp) over this tile's valid columns; the 16
+    // lanes of a quarter-wave share rows, the four waves along the
+    // vocabulary are merged through LDS in a fixed order
+    float2* sred = reinterpret_cast<float2*>(mfma_lds);   // [4][kTM]
+    __syncthreads();
 #pragma unroll
     for (int mi = 0; mi < 4; ++mi)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int rloc = 64 * wm + 16 * mi + 4 * lq + i;
+        const int row = 64 * wm + 16 * mi + 4 * q + i;
+        const int64_t m = m0 + (row < rows ? row : rows - 1);
+        const int64_t y = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m]
+                                  : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m]);
         float mx = -INFINITY;
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          const int64_t v = v0 + 64 * wn + 16 * ni + lr;
-          if (v < a.V) mx = fmaxf(mx, acc[mi][ni][i]);
-        }
+        for (int ni = 0; ni < 4; ++ni)
+          if (64 * wn + 16 * ni + lr < cols) mx = fmaxf(mx, acc[mi][ni][i]);
 #pragma unroll
         for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
         float se = 0.f;
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni) {
-          const int64_t v = v0 + 64 * wn + 16 * ni + lr;
-          if (v < a.V) {
+          const int col = 64 * wn + 16 * ni + lr;
+          if (col < cols) {
             se += fast_exp(acc[mi][ni][i] - mx);
-            if (v == sy[rloc] && m0 + rloc < a.M) a.tgt_logit[m0 + rloc] = acc[mi][ni][i];
+            if (v0 + col == y && row < rows) a.tgt_logit[m] = acc[mi][ni][i];
           }
         }
 #pragma unroll
         for (int off = 1; off < 16; off <<= 1) se += __shfl_xor(se, off, 64);
-        if (lr == 0) sred[wn][rloc] = make_float2(mx, se);
+        if (lr == 0) sred[wn * kTM + row] = make_float2(mx, se);
       }
     __syncthreads();
-    if (tid < kTM && m0 + tid < a.M) {
-      float m_ = sred[0][tid].x, s_ = sred[0][tid].y;
-      lse_merge(m_, s_, sred[1][tid].x, sred[1][tid].y);
+    if (tid < rows) {
+      float m_ = sred[tid].x, s_ = sred[tid].y;
+#pragma unroll
+      for (int w = 1; w < 4; ++w) lse_merge(m_, s_, sred[w * kTM + tid].x, sred[w * kTM + tid].y);
       a.part[(m0 + tid) * a.n_vt + vt] = make_float2(m_, s_);
+    }
+  }
+}
+
+// ---------------------------------------------------- MFMA path: prologue
+// Per call, before stage 1: (a) the residual group scales in tile-major
+// order, rsT[vt][j][c] = s_res[min(vt kTN + c, V - 1), j], so a tile's scales
+// of one group are 512 contiguous bytes; (b) the factor codes of V_c and
+// B_w as bf16 (exact), wbf[k][i] for the R = r_c + r_r rows.
+struct PrepArgs {
+  const uint16_t* rs;
+  int64_t V;
+  int ngrp;
+  int64_t n_vt;
+  uint16_t* rsT;
+  const int8_t* cv;
+  const int8_t* cb;
+  int rc, rr, d;
+  uint16_t* wbf;
+};
+
+__global__ __launch_bounds__(kBlock) void k_prep(PrepArgs a) {
+  const int64_t nthr = int64_t(gridDim.x) * kBlock;
+  const int64_t t0 = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  // (a) one thread per (vocabulary tile, column): read the row's scales,
+  // write one per group (lanes write consecutive columns)
+  for (int64_t e = t0; e < a.n_vt * kTN; e += nthr) {
+    const int64_t vt = e / kTN, c = e % kTN;
+    const int64_t v = vt * kTN + c < a.V ? vt * kTN + c : a.V - 1;
+    const uint16_t* src = a.rs + v * a.ngrp;
+    uint16_t* dst = a.rsT + vt * int64_t(a.ngrp) * kTN + c;
+    for (int j = 0; j < a.ngrp; ++j) dst[int64_t(j) * kTN] = src[j];
+  }
+  // (b) 8 codes per thread
+  const int64_t n8 = int64_t(a.rc + a.rr) * a.d / 8;
+  for (int64_t e = t0; e < n8; e += nthr) {
+    const int64_t k = e * 8 / a.d, i = e * 8 % a.d;
+    const int8_t* src = k < a.rc ? a.cv + k * a.d + i : a.cb + (k - a.rc) * a.d + i;
+    const uint2 w = *reinterpret_cast<const uint2*>(src);
+    uint32_t o[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const uint32_t wj = j < 2 ? w.x : w.y;
+      const int sh = 16 * (j & 1);
+      const float lo = float(int8_t(wj >> sh)), hi = float(int8_t(wj >> (sh + 8)));
+      o[j] = (__float_as_uint(lo) >> 16) | (__float_as_uint(hi) & 0xffff0000u);
+    }
+    *reinterpret_cast<uint4*>(a.wbf + e * 8) = make_uint4(o[0], o[1], o[2], o[3]);
+  }
+}
+
+// ---------------------------------------------------- MFMA path: stage 1
+// t[m, k] = sum over factor groups of s[k, grp] * (sum over the group of
+// c[k, i] x[m, i]) for the R factor rows (V_c then B_w), and the group biases
+// gbias[m / kTM][j][m % kTM] = -136 * (sum of x[m, i] over residual group j).
+// A workgroup takes 16 tokens and up to 64 factor rows (grid y); its eight
+// waves split d by residual groups and each holds 16 x 64 outputs as four
+// 16x16 MFMA tiles, loading the next K-chunk's fragments before the current
+// chunk's MFMAs; an extra MFMA against a column of ones gives the chunk sums
+// of x.  The eight partial results are summed in LDS in a fixed order.
+struct Stage1MArgs {
+  const uint16_t* x;
+  int64_t ldx, M;
+  int d, g;
+  const uint16_t* wbf;     // [R][d] bf16 factor codes
+  const uint16_t* sv;
+  int gv, rc;
+  const uint16_t* sb;
+  int gb, rr;
+  float* t;                // [M, R]
+  float* gbias;            // [n_mt][d/g][kTM]
+};
+
+constexpr int kS1MTok = 16, kS1MCols = 64, kS1MBlock = 512, kS1MWaves = kS1MBlock / 64;
+
+__global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
+  __shared__ float red[kS1MWaves][kS1MTok][kS1MCols + 1];
+  const int lane = threadIdx.x & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lr = lane & 15, q = lane >> 4;
+  const int R = a.rc + a.rr;
+  const int64_t tok0 = int64_t(blockIdx.x) * kS1MTok;
+  const int kb = blockIdx.y * kS1MCols;           // first factor row of this workgroup
+  const int ngrp = a.d / a.g, cpg = a.g / 32;
+  const int c0 = (wid * ngrp / kS1MWaves) * cpg, c1 = ((wid + 1) * ngrp / kS1MWaves) * cpg;
+  const int64_t mrow = tok0 + lr < a.M ? tok0 + lr : a.M - 1;
+  const uint16_t* xrow = a.x + mrow * a.ldx + 8 * q;
+  const bool do_bias = blockIdx.y == 0;
+  constexpr int NB = kS1MCols / 16;
+  const int nblk = R - kb >= kS1MCols ? NB : (R - kb + 15) / 16;
+
+  // this lane's factor row in each 16-column block (clamped; masked on store)
+  const uint16_t* wrow[NB];
+  const uint16_t* srow[NB];
+  int sgrp[NB];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    int k = kb + 16 * nb + lr;
+    k = k < R ? k : (R > 0 ? R - 1 : 0);
+    wrow[nb] = a.wbf + int64_t(k) * a.d + 8 * q;
+    const bool core = k < a.rc;
+    sgrp[nb] = core ? a.gv : a.gb;
+    srow[nb] = core ? a.sv + int64_t(k) * (a.d / a.gv) : a.sb + int64_t(k - a.rc) * (a.d / a.gb);
+  }
+  const bf16x8_t ones = {(__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f,
+                         (__bf16)1.f, (__bf16)1.f, (__bf16)1.f, (__bf16)1.f};
+  f32x4_t acc[NB], gs = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) acc[nb] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  bf16x8_t A, An, B[NB], Bn[NB];
+  float s[NB], sn[NB];
+  auto load = [&](int c, bf16x8_t& A_, bf16x8_t* B_, float* s_) {
+    const int k0 = 32 * c;
+    A_ = *reinterpret_cast<const bf16x8_t*>(xrow + k0);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      if (nb < nblk) {
+        B_[nb] = *reinterpret_cast<const bf16x8_t*>(wrow[nb] + k0);
+        s_[nb] = f16_to_f32(srow[nb][k0 / sgrp[nb]]);
+      }
+    }
+  };
+  if (c0 < c1) load(c0, A, B, s);
+  for (int c = c0; c < c1; ++c) {
+    if (c + 1 < c1) load(c + 1, An, Bn, sn);
+    if (do_bias) gs = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, ones, gs, 0, 0, 0);
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) {
+      if (nb < nblk) {
+        const f32x4_t z = {0.f, 0.f, 0.f, 0.f};
+        acc[nb] += s[nb] * __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[nb], z, 0, 0, 0);
+      }
+    }
+    if (do_bias && (c + 1) % cpg == 0) {
+      const int j = c / cpg;
+      if (lr == 0) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int64_t m = tok0 + 4 * q + i;
+          if (m < a.M)
+            a.gbias[((m / kTM) * ngrp + j) * kTM + m % kTM] = -float(archead::kInt4Bias) * gs[i];
+        }
+      }
+      gs = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    }
+    A = An;
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb) B[nb] = Bn[nb], s[nb] = sn[nb];
+  }
+  if (R == 0) return;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wid][4 * q + i][16 * nb + lr] = acc[nb][i];
+  __syncthreads();
+  for (int e = threadIdx.x; e < kS1MTok * kS1MCols; e += kS1MBlock) {
+    const int tt = e / kS1MCols, c = e % kS1MCols;
+    const int64_t m = tok0 + tt;
+    if (m < a.M && kb + c < R) {
+      float v = red[0][tt][c];
+#pragma unroll
+      for (int w = 1; w < kS1MWaves; ++w) v += red[w][tt][c];
+      a.t[m * R + kb + c] = v;
     }
   }
 }
@@ -1179,8 +1409,16 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
   const bool gemv = use_gemv(h, M);
   w.t_off = off;
   off = align256(off + sizeof(float) * size_t(M) * size_t(d.r_c + d.r_r));
-  w.xs_off = off;
-  if (!gemv) off = align256(off + sizeof(float) * size_t(M) * size_t(d.d / d.g));
+  if (!gemv) {
+    const size_t ngrp = size_t(d.d / d.g);
+    const size_t n_mt = size_t((M + kTM - 1) / kTM), n_vt = size_t((d.V + kTN - 1) / kTN);
+    w.gb_off = off;
+    off = align256(off + sizeof(float) * n_mt * ngrp * kTM);
+    w.rst_off = off;
+    off = align256(off + sizeof(uint16_t) * n_vt * ngrp * kTN);
+    w.wbf_off = off;
+    off = align256(off + sizeof(uint16_t) * size_t(d.r_c + d.r_r) * size_t(d.d));
+  }
   if (op == ARCHEAD_OP_LOGITS_CE) {
     // GEMV: all CE passes share one grid (the smallest of the variants
     // used) so every token row of the partials has the same number of
@@ -1226,11 +1464,10 @@ archead_status check_call(const archead_handle* h, const void* x, int64_t M, int
 }
 
 archead_status launch_stage1(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
-                             float* t, float* xs, hipStream_t s) {
+                             float* t, hipStream_t s) {
   const archead_desc& d = h->desc;
   const int64_t R = d.r_c + d.r_r;
-  const int64_t nx = xs ? d.d / d.g : 0;   // extra workgroups for the group sums
-  if (R + nx == 0) return ARCHEAD_OK;
+  if (R == 0) return ARCHEAD_OK;
   Stage1Args a;
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx; a.M = M; a.d = d.d;
@@ -1241,17 +1478,56 @@ archead_status launch_stage1(const archead_handle* h, const void* x, int64_t M, 
   a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
   a.gb = d.r_r ? d.g_b : d.d; a.rr = d.r_r;
   a.t = t;
-  a.xs = xs;
-  a.g = d.g;
   for (int64_t m0 = 0; m0 < M; m0 += kMaxGridY * kS1Tok) {
     const int64_t rest = M - m0;
     const int64_t mblocks = (rest < kMaxGridY * kS1Tok ? rest + kS1Tok - 1 : kMaxGridY * kS1Tok) / kS1Tok;
     a.mbase = m0;
-    hipLaunchKernelGGL(k_stage1, dim3(unsigned(R + nx), unsigned(mblocks)), dim3(kBlock), 0, s, a);
+    hipLaunchKernelGGL(k_stage1, dim3(unsigned(R), unsigned(mblocks)), dim3(kBlock), 0, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_fail(e, "stage-1 launch");
   }
   return ARCHEAD_OK;
+}
+
+// MFMA path prologue: the tile-major residual scales and the bf16 factor
+// codes, then stage 1 (t and the group biases).
+archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int64_t M,
+                                    int64_t ldx, const WsLayout& w, char* ws, hipStream_t s) {
+  const archead_desc& d = h->desc;
+  const int R = int(d.r_c + d.r_r);
+  PrepArgs p;
+  p.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
+  p.V = d.V;
+  p.ngrp = int(d.d / d.g);
+  p.n_vt = (d.V + kTN - 1) / kTN;
+  p.rsT = reinterpret_cast<uint16_t*>(ws + w.rst_off);
+  p.cv = static_cast<const int8_t*>(h->ptrs.core_v);
+  p.cb = static_cast<const int8_t*>(h->ptrs.corr_b);
+  p.rc = int(d.r_c); p.rr = int(d.r_r); p.d = int(d.d);
+  p.wbf = reinterpret_cast<uint16_t*>(ws + w.wbf_off);
+  const int64_t work = std::max<int64_t>(p.n_vt * kTN, int64_t(R) * d.d / 8);
+  const int64_t pblocks = std::min<int64_t>((work + kBlock - 1) / kBlock, 4 * int64_t(h->n_cu));
+  hipLaunchKernelGGL(k_prep, dim3(unsigned(pblocks)), dim3(kBlock), 0, s, p);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "prologue launch");
+
+  Stage1MArgs a;
+  a.x = static_cast<const uint16_t*>(x);
+  a.ldx = ldx; a.M = M; a.d = int(d.d); a.g = int(d.g);
+  a.wbf = p.wbf;
+  a.sv = static_cast<const uint16_t*>(h->ptrs.core_v_scale);
+  a.gv = int(d.r_c ? d.g_v : d.d); a.rc = int(d.r_c);
+  a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
+  a.gb = int(d.r_r ? d.g_b : d.d); a.rr = int(d.r_r);
+  a.t = reinterpret_cast<float*>(ws + w.t_off);
+  a.gbias = reinterpret_cast<float*>(ws + w.gb_off);
+  const int64_t mblocks = (M + kS1MTok - 1) / kS1MTok;
+  const int64_t rblocks = R > 0 ? (R + kS1MCols - 1) / kS1MCols : 1;
+  if (mblocks > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "M too large");
+  hipLaunchKernelGGL(k_stage1m, dim3(unsigned(mblocks), unsigned(rblocks)), dim3(kS1MBlock), 0,
+                     s, a);
+  e = hipGetLastError();
+  return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "stage-1 launch");
 }
 
 GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const float* t) {
@@ -1318,40 +1594,51 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
 }
 
 MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
-                   const float* t, const float* xs) {
+                   const WsLayout& w, char* ws) {
   const archead_desc& d = h->desc;
   MfmaArgs a;
   memset(&a, 0, sizeof a);
   a.codes = static_cast<const uint8_t*>(h->ptrs.res_codes);
-  a.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
   a.cu = static_cast<const int8_t*>(h->ptrs.core_u);
   a.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
   a.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
   a.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx;
-  a.t = t;
-  a.xs = xs;
+  a.t = reinterpret_cast<const float*>(ws + w.t_off);
+  a.gbias = reinterpret_cast<const float*>(ws + w.gb_off);
+  a.rsT = reinterpret_cast<const uint16_t*>(ws + w.rst_off);
   a.M = M; a.V = d.V;
   a.d = int(d.d); a.g = int(d.g); a.rc = int(d.r_c); a.rr = int(d.r_r);
+  a.n_mt = (M + kTM - 1) / kTM;
   a.n_vt = (d.V + kTN - 1) / kTN;
-  a.n_tiles = a.n_vt * ((M + kTM - 1) / kTM);
+  a.n_tiles = a.n_vt * a.n_mt;
   a.tiles_per_xcd = (a.n_tiles + 7) / 8;
   return a;
 }
 
-archead_status launch_mfma(const archead_handle* h, MfmaArgs a, bool ce, hipStream_t s) {
-  using Fn = void (*)(MfmaArgs);
-  const bool k64 = a.g % 64 == 0;
-  Fn fn = ce ? (k64 ? k_mfma<64, true> : k_mfma<32, true>)
-             : (k64 ? k_mfma<64, false> : k_mfma<32, false>);
+template <int KS, bool CE>
+archead_status launch_mfma_ks(const archead_handle* h, MfmaArgs& a, hipStream_t s) {
+  const void* fn = reinterpret_cast<const void*>(k_mfma<KS, CE>);
+  const int lds = MGeom<KS>::LDS;
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+  if (e != hipSuccess) return hip_fail(e, "MFMA LDS size attribute");
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
   hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
   void* args[] = {&a};
-  hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void*>(fn),
-                                    dim3(unsigned(8 * a.tiles_per_xcd)), dim3(kBlock), args, 0,
-                                    s, ev0, ev1, 0);
+  const int64_t grid = 8 * a.tiles_per_xcd;
+  if (grid > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "too many MFMA tiles");
+  e = hipExtLaunchKernel(fn, dim3(unsigned(grid)), dim3(kMBlock), args, size_t(lds), s, ev0, ev1, 0);
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "MFMA launch");
+}
+
+archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStream_t s) {
+  // x rows of a tile must lie within a 2 GiB buffer window
+  if (int64_t(kTM) * a.ldx * 2 >= (int64_t(1) << 31))
+    return fail(ARCHEAD_E_UNSUPPORTED, "ldx too large for the MFMA path");
+  if (a.g % 128 == 0) return ce ? launch_mfma_ks<128, true>(h, a, s) : launch_mfma_ks<128, false>(h, a, s);
+  if (a.g % 64 == 0) return ce ? launch_mfma_ks<64, true>(h, a, s) : launch_mfma_ks<64, false>(h, a, s);
+  return ce ? launch_mfma_ks<32, true>(h, a, s) : launch_mfma_ks<32, false>(h, a, s);
 }
 
 }  // namespace
@@ -1428,16 +1715,15 @@ archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
   const WsLayout w = ws_layout(h, M, ARCHEAD_OP_LOGITS);
   float* t = reinterpret_cast<float*>(static_cast<char*>(ws) + w.t_off);
   if (!use_gemv(h, M)) {
-    float* xs = reinterpret_cast<float*>(static_cast<char*>(ws) + w.xs_off);
-    st = launch_stage1(h, x, M, ldx, t, xs, s);
+    st = launch_mfma_prologue(h, x, M, ldx, w, static_cast<char*>(ws), s);
     if (st != ARCHEAD_OK) return st;
-    MfmaArgs a = mfma_args(h, x, M, ldx, t, xs);
+    MfmaArgs a = mfma_args(h, x, M, ldx, w, static_cast<char*>(ws));
     a.out = out;
     a.ldo = ldo;
     a.out_bf16 = out_dtype == ARCHEAD_BF16;
     return launch_mfma(h, a, false, s);
   }
-  st = launch_stage1(h, x, M, ldx, t, nullptr, s);
+  st = launch_stage1(h, x, M, ldx, t, s);
   if (st != ARCHEAD_OK) return st;
   GemvArgs a = gemv_args(h, x, ldx, t);
   a.out = out;
@@ -1466,17 +1752,16 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t
   float* tl = reinterpret_cast<float*>(base + w.tgt_off);
   const int64_t n_part = w.n_part;
   if (!use_gemv(h, M)) {
-    float* xs = reinterpret_cast<float*>(base + w.xs_off);
-    st = launch_stage1(h, x, M, ldx, t, xs, s);
+    st = launch_mfma_prologue(h, x, M, ldx, w, base, s);
     if (st != ARCHEAD_OK) return st;
-    MfmaArgs a = mfma_args(h, x, M, ldx, t, xs);
+    MfmaArgs a = mfma_args(h, x, M, ldx, w, base);
     a.tgt = targets;
     a.tgt64 = tgt_dtype == ARCHEAD_I64;
     a.part = part;
     a.tgt_logit = tl;
     st = launch_mfma(h, a, true, s);
   } else {
-    st = launch_stage1(h, x, M, ldx, t, nullptr, s);
+    st = launch_stage1(h, x, M, ldx, t, s);
     if (st != ARCHEAD_OK) return st;
     GemvArgs a = gemv_args(h, x, ldx, t);
     a.tgt = targets;

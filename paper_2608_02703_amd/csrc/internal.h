@@ -36,7 +36,9 @@ int lanes_per_row(int64_t d);
 // Workspace carve-up (byte offsets, each 256-aligned).
 struct WsLayout {
   size_t t_off = 0;      // fp32 [M, r_c + r_r]
-  size_t xs_off = 0;     // fp32 [M, d/g] (MFMA path)
+  size_t gb_off = 0;     // fp32 [n_mt][d/g][128] group biases (MFMA path)
+  size_t rst_off = 0;    // fp16 [n_vt][d/g][256] tile-major residual scales (MFMA path)
+  size_t wbf_off = 0;    // bf16 [r_c + r_r][d] factor codes (MFMA path)
   size_t part_off = 0;   // float2 [M, n_part] (CE)
   size_t tgt_off = 0;    // fp32 [M] (CE)
   size_t total = 0;
@@ -47,8 +49,5 @@ bool use_gemv(const archead_handle* h, int64_t M);
 
 // grid of the GEMV kernel: persistent workgroups, at most one per 8 rows
 int64_t gemv_grid(const archead_handle* h, int tok, bool ce);
-// rows handled by one MFMA workgroup tile
-constexpr int64_t kMfmaTileV = 128;
-constexpr int64_t kMfmaTileM = 128;
 
 }  // namespace archead
