@@ -152,9 +152,13 @@ archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs
 void archead_destroy(archead_handle* h);
 
 /* Bytes of workspace the call `op` needs for M tokens (0 for M == 0).  The
- * workspace holds the low-rank projections t (fp32 [M, r_c + r_r]), the
- * per-group sums of x and, for the CE call, the per-vocabulary-tile softmax
- * partials.  Returns 0 for a NULL handle or M < 0. */
+ * workspace holds the low-rank projections t (fp32 [M, r_c + r_r]; on the
+ * MFMA path split into two bf16 parts), on the MFMA path also per-call
+ * tables derived from the head (group-scale ratios, the per-group sums of x,
+ * the factor codes as bf16 and the U_c / A_w codes side by side: about
+ * V * (r_c + r_r + 4 * (d/g + 3)) bytes), and for the CE call the
+ * per-vocabulary-tile softmax partials.  Returns 0 for a NULL handle or
+ * M < 0. */
 size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op);
 
 /* logits[m, v] for m < M, v < V.
@@ -166,9 +170,13 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *            ARCHEAD_OP_LOGITS), 256-byte aligned; its contents on entry do
  *            not matter
  *   stream   hipStream_t to launch on (NULL = the default stream)
- * M == 0 returns ARCHEAD_OK without launching.  The kernels read the head
- * once per call whatever M is (decode GEMV for small M, tiled bf16 MFMA for
- * large M). */
+ * M == 0 returns ARCHEAD_OK without launching.  Small M (and heads with
+ * g % 64 != 0) run the decode GEMV, which reads the head once per pass of 4
+ * tokens; larger M run the tiled bf16 MFMA kernel (256 x 256 tiles of tokens
+ * x vocabulary rows).  Both produce fp32 logits from fp32 accumulation; the
+ * MFMA kernel carries its accumulator in units of the current scale group's
+ * scale, and feeds the rank-r expansion t as two bf16 parts (t to 2^-17
+ * relative), so its logits differ from the GEMV's in the last bits. */
 archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
                               int64_t ldx, void* out, archead_dtype out_dtype,
                               int64_t ldo, void* ws, size_t ws_bytes,
@@ -191,7 +199,8 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x,
                                  float* mean_ce, void* ws, size_t ws_bytes,
                                  void* stream);
 
-/* Largest M served by the decode GEMV kernel; larger M use the MFMA kernel.
+/* Largest M served by the decode GEMV kernel; larger M use the MFMA kernel
+ * (unless g % 64 != 0, which always takes the GEMV).
  * -1 restores the built-in threshold.  Not thread-safe with concurrent calls
  * on the same handle (set it once, after create). */
 archead_status archead_set_gemv_max_m(archead_handle* h, int64_t m);

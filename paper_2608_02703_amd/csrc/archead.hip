@@ -696,70 +696,62 @@ void k_gemv(GemvArgs a) {
 }
 
 // ------------------------------------------------------------ many tokens: MFMA
-// Tiled bf16 MFMA path for many tokens.  A workgroup owns a kTM x kTN tile
-// (tokens x vocabulary rows); its eight waves own 64 x 64 blocks (2 along
-// the tokens, 4 along the vocabulary), each a 4 x 4 grid of 16x16 MFMA tiles
-// (v_mfma_f32_16x16x32_bf16: A lane l holds row l%16 and 8 k-slots of quarter
-// l/16; B likewise by column; D lane l holds rows 4 (l/16) .. +3 of column
-// l%16).  The K loop runs over d in stages of KS elements that direct
-// global-to-LDS buffer loads bring into a ring of kRing LDS stages, two
-// stages ahead of the compute, with no register staging.  Within a stage the
-// k-slots are assigned so that one lane's code dwords are contiguous: lane
-// quarter q takes code dwords q*KC .. q*KC+KC-1 of the stage (one per MFMA
-// K-chunk) and the x chunks with the same indices.  Token rows and
-// vocabulary rows are XOR-swizzled in 16-byte units so fragment reads are
-// bank-conflict free.
+// Tiled bf16 MFMA path for many tokens (needs g % 64 == 0).  A workgroup owns
+// a kTM x kTN tile (tokens x vocabulary rows); its eight waves own 128 x 64
+// blocks (2 along the tokens, 4 along the vocabulary), each an 8 x 4 grid of
+// 16x16 MFMA tiles (v_mfma_f32_16x16x32_bf16: A lane l holds row l%16 and 8
+// k-slots of quarter l/16; B likewise by column; D lane l holds rows
+// 4 (l/16) .. +3 of column l%16).  The K loop runs in stages of kKS elements
+// that direct global-to-LDS buffer loads bring into a ring of kRing LDS
+// stages, two stages ahead of the compute, with no register staging.  Within
+// a stage lane quarter q takes code dwords 2q, 2q+1 (one per MFMA K-chunk)
+// and the x chunks with the same indices, so its codes are one 8-byte read.
+// Token rows and vocabulary rows are XOR-swizzled in 16-byte units so
+// fragment reads are bank-conflict free.
 //
-// Codes are unpacked per wave to bf16 (136 + c) (exact).  The MFMA of the
-// first K-chunk of each scale group starts from the group bias
-// -136 * (sum of x over the group), so the group partial is sum c x; at the
-// end of the group its fp32 scale multiplies the partial into the
-// accumulator.  The rank-r expansion runs as extra K-chunks with t split
-// into three bf16 parts (hi + mid + lo = t to fp32 precision) against the
-// int8 codes (exact in bf16), scaled by s_U / s_A.
+// Codes are unpacked per wave to bf16 (136 + c) (exact).  The accumulator is
+// kept in units of the current scale slot's scale: at the start of slot k it
+// becomes acc * (s'_{k-1} / s'_k) + bias_k, after which the MFMAs add the
+// slot's terms, so at the end s'_last * acc is the logit.  Slots are the
+// residual groups (bias -136 * (sum of x over the group), the MFMAs adding
+// sum (136 + c) x), then the rank-r expansion's core part (scale s_U) and
+// correction part (s_A).  s' is the scale with zero replaced by kZeroScale,
+// which pushes a zero-scale slot's contribution below fp32 resolution of the
+// result.  The expansion parts run as extra stages with the same geometry,
+// 16 rank dimensions per stage: the "x" rows hold t split into three bf16
+// parts (hi = bf16(t), mid = bf16(t - hi), lo = bf16(t - hi - mid); their sum
+// is t to fp32 precision) as [hi | mid | lo | 0], the "code" rows the int8
+// factor codes (exact in bf16) twice, [c | c], so MFMA K-chunk 0 adds
+// (hi + mid) c and K-chunk 1 adds lo c.
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) uint8_t lds_u8;
 
-constexpr int kTM = 128, kTN = 256;          // tile: tokens x vocabulary rows
-constexpr int kMBlock = 512, kMWaves = 8;    // 2 x 4 waves of 64 x 64
+constexpr int kTM = 256, kTN = 256;          // tile: tokens x vocabulary rows
+constexpr int kMBlock = 512, kMWaves = 8;    // 2 x 4 waves of 128 x 64
+constexpr int kKS = 64;                      // K elements per stage
 constexpr int kRing = 3;                     // LDS stages (two loads in flight)
-constexpr int kRasterGM = 4;                 // token tiles per raster group
-constexpr int kExpRow = 40;                  // bf16 per padded LDS row (expansion)
-constexpr int kExpBytes = (3 * kTM + kTN) * kExpRow * 2;
+constexpr int kRasterGM = 2;                 // token tiles per raster group
+constexpr float kZeroScale = 0x1p-60f;       // stand-in for a zero scale
+constexpr int kExpDims = 16;                 // rank dimensions per expansion stage
 
-template <int KS>
 struct MGeom {
-  static constexpr int KC = KS / 32;                  // MFMA K-chunks per stage
-  static constexpr int XBYTES = kTM * KS * 2;         // x [kTM][KS] bf16
-  static constexpr int CBYTES = kTN * KS / 2;         // codes [kTN][KS/2]
-  static constexpr int SCL = XBYTES + CBYTES;         // fp16 [kTN] group scales
-  static constexpr int BIAS = SCL + kTN * 2;          // fp32 [kTM] group biases
+  static constexpr int XBYTES = kTM * kKS * 2;        // x [kTM][kKS] bf16
+  static constexpr int CBYTES = kTN * kKS / 2;        // codes [kTN][kKS/2]
+  static constexpr int RAT = XBYTES + CBYTES;         // fp32 [kTN] scale ratios
+  static constexpr int BIAS = RAT + kTN * 4;          // fp32 [kTM] slot biases
   static constexpr int STAGE = BIAS + kTM * 4;
   static constexpr int NX = XBYTES / 1024 / kMWaves;  // x loads per wave and stage
-  static constexpr int NC = CBYTES / 1024;            // code loads per workgroup and stage
-  static constexpr int NCW = NC >= kMWaves ? NC / kMWaves : 0;
-  static constexpr int NL = NX + NCW + 1;             // loads per wave and stage
-  static constexpr int RING = kRing * STAGE;
-  static constexpr int LDS = RING > kExpBytes ? RING : kExpBytes;
-  static_assert(NC >= kMWaves || NC == kMWaves / 2, "code loads must spread evenly");
+  static constexpr int NL = NX + 2;                   // loads per wave and stage
+  static constexpr int LDS = kRing * STAGE;
+  static_assert(CBYTES / 1024 == kMWaves, "one code load per wave");
   static_assert(LDS <= 160 * 1024, "LDS budget");
 };
 
-// 16-byte unit swizzles (argument: row within the tile; only its low four
-// bits matter, so every lane's swizzle is fixed for all its fragments)
-template <int KS>
-__device__ __forceinline__ int swz_x(int r) {
-  if constexpr (KS == 128) return r & 15;
-  else if constexpr (KS == 64) return ((r & 15) ^ ((r & 15) >> 3)) & 7;
-  else return ((r >> 1) ^ (r >> 2)) & 3;
-}
-template <int KS>
-__device__ __forceinline__ int swz_c(int c) {
-  if constexpr (KS == 128) return ((c >> 1) ^ (c >> 2)) & 3;
-  else if constexpr (KS == 64) return (c >> 2) & 1;
-  else return 0;
-}
+// 16-byte unit swizzles; only the low four bits of the row matter, so every
+// lane's swizzle is fixed for all its fragments
+__device__ __forceinline__ int swz_x(int r) { return ((r & 15) ^ ((r & 15) >> 3)) & 7; }
+__device__ __forceinline__ int swz_c(int c) { return (c >> 2) & 1; }
 
 __device__ __forceinline__ void dma16(__amdgpu_buffer_rsrc_t r, lds_u8* dst, uint32_t voff) {
   __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -792,33 +784,43 @@ __device__ __forceinline__ bf16x8_t unpack8(uint32_t q, uint32_t kMask, uint32_t
   return __builtin_bit_cast(bf16x8_t, p);
 }
 
+// eight int8 codes (little-endian in two dwords) as bf16 (exact)
+__device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint32_t w0, uint32_t w1) {
+  uint32_t p[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const uint32_t w = j < 2 ? w0 : w1;
+    const int sh = 16 * (j & 1);
+    const float lo = float(int8_t(w >> sh)), hi = float(int8_t(w >> (sh + 8)));
+    p[j] = __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
+  }
+  return __builtin_bit_cast(bf16x8_t, p);
+}
+
 struct MfmaArgs {
   const uint8_t* codes;
-  const int8_t* cu;
-  const uint16_t* su;
-  const int8_t* ca;
-  const uint16_t* sa;
   const uint16_t* x;
   int64_t ldx;
-  const float* t;        // [M, rc + rr]
-  const float* gbias;    // [n_mt][d/g][kTM]: -136 * (sum of x over group j)
-  const uint16_t* rsT;   // [n_vt][d/g][kTN]: residual group scales, tile-major
+  const uint16_t* tsplit;  // [M][nch][4][16] bf16: t hi, mid, lo, 0 per 16 rank dimensions
+  const int8_t* ucodes;    // [V][nch][2][16] int8: U_c then A_w codes (each padded), twice
+  const float* gbias;      // [n_mt][nslot][kTM] slot biases
+  const float* ratio;      // [n_vt][nslot][kTN]: s'_{k-1} / s'_k (0 for k = 0)
+  const float* fin;        // [n_vt][kTN]: s' of the last slot
   int64_t M, V;
-  int d, g, rc, rr;
+  int d, g, nslot, nch, nch_u;
   int64_t n_mt, n_vt, n_tiles, tiles_per_xcd;
   void* out;
   int64_t ldo;
   int out_bf16;
   const void* tgt;
   int tgt64;
-  float2* part;          // [M, n_vt]
-  float* tgt_logit;      // [M]
+  float2* part;            // [M, n_vt]
+  float* tgt_logit;        // [M]
 };
 
-template <int KS, bool CE>
+template <bool CE>
 __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
-  using G = MGeom<KS>;
-  constexpr int KC = G::KC;
+  using G = MGeom;
   extern __shared__ __align__(16) uint8_t mfma_lds[];
   lds_u8* const L = (lds_u8*)mfma_lds;
 
@@ -848,6 +850,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   const int ngrp = a.d / a.g;
   const uint32_t rowbytes = uint32_t(a.d) / 2;
   const uint32_t ldx2 = uint32_t(a.ldx) * 2;
+  const uint32_t trow = uint32_t(a.nch) * 128, urow = uint32_t(a.nch) * 32;
 
   // buffer resources over exactly the bytes this tile may touch (loads past
   // them return zero instead of reading other memory)
@@ -857,210 +860,173 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint8_t*>(a.codes + v0 * int64_t(rowbytes)), 0, int(uint32_t(cols) * rowbytes),
       kBufferWord3);
-  const int piece = wid & 3;   // auxiliary load of this wave: scales 0-1, biases 2-3
+  const __amdgpu_buffer_rsrc_t rt = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.tsplit + m0 * int64_t(a.nch) * 64), 0, int(uint32_t(rows) * trow),
+      kBufferWord3);
+  const __amdgpu_buffer_rsrc_t ru = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<int8_t*>(a.ucodes + v0 * int64_t(urow)), 0, int(uint32_t(cols) * urow),
+      kBufferWord3);
+  // auxiliary load of this wave: scale ratios (waves 0-3, 64 columns each)
+  // or slot biases (waves 4-7, 64 token rows each)
+  const bool arat = wid < 4;
   const __amdgpu_buffer_rsrc_t raux =
-      piece < 2 ? __builtin_amdgcn_make_buffer_rsrc(
-                      const_cast<uint16_t*>(a.rsT + vt * ngrp * kTN), 0, ngrp * kTN * 2,
-                      kBufferWord3)
-                : __builtin_amdgcn_make_buffer_rsrc(
-                      const_cast<float*>(a.gbias + mt * ngrp * kTM), 0, ngrp * kTM * 4,
-                      kBufferWord3);
+      arat ? __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.ratio + vt * a.nslot * kTN),
+                                               0, a.nslot * kTN * 4, kBufferWord3)
+           : __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.gbias + mt * a.nslot * kTM),
+                                               0, a.nslot * kTM * 4, kBufferWord3);
 
-  // per-lane load offsets (the stage's k offset is added per stage)
+  // per-lane load offsets (row and swizzled 16-byte unit) of the residual
+  // stages; the expansion stages use the same units with their own row
+  // strides; the stage's k offset is added per stage
+  auto xunit = [&](int i, uint32_t stride) {
+    const int off = (wid * G::NX + i) * 1024 + 16 * lane;
+    const int r = off / (2 * kKS), p = (off % (2 * kKS)) / 16;
+    return uint32_t(r < rows ? r : rows - 1) * stride + 16u * uint32_t(p ^ swz_x(r));
+  };
+  auto cunit = [&](uint32_t stride) {
+    const int off = wid * 1024 + 16 * lane;
+    const int c = off / (kKS / 2), p = (off % (kKS / 2)) / 16;
+    return uint32_t(c < cols ? c : cols - 1) * stride + 16u * uint32_t(p ^ swz_c(c));
+  };
   uint32_t xo[G::NX];
 #pragma unroll
-  for (int i = 0; i < G::NX; ++i) {
-    const int off = (wid * G::NX + i) * 1024 + 16 * lane;
-    const int r = off / (2 * KS), p = (off % (2 * KS)) / 16;
-    const int rr_ = r < rows ? r : rows - 1;
-    xo[i] = uint32_t(rr_) * ldx2 + 16u * uint32_t(p ^ swz_x<KS>(r));
-  }
-  constexpr int NCO = G::NCW > 0 ? G::NCW : 1;
-  uint32_t co[NCO];
-#pragma unroll
-  for (int i = 0; i < NCO; ++i) {
-    const int j = G::NCW > 0 ? wid * G::NCW + i : (wid & 3);
-    const int off = j * 1024 + 16 * lane;
-    const int c = off / (KS / 2), p = (off % (KS / 2)) / 16;
-    const int cc = c < cols ? c : cols - 1;
-    co[i] = uint32_t(cc) * rowbytes + 16u * uint32_t(p ^ swz_c<KS>(c));
-  }
+  for (int i = 0; i < G::NX; ++i) xo[i] = xunit(i, ldx2);
+  const uint32_t co = cunit(rowbytes);
   uint32_t ao;
   int adst;
-  if (piece < 2) {
-    ao = uint32_t(piece * 128 + 2 * lane) * 2;
-    adst = G::SCL + piece * 256;
+  if (arat) {
+    ao = uint32_t(wid * 64 + lane) * 4;
+    adst = G::RAT + wid * 256;
   } else {
-    const int r = (piece - 2) * 64 + lane;
+    const int r = (wid - 4) * 64 + lane;
     ao = uint32_t(r < rows ? r : rows - 1) * 4;
-    adst = G::BIAS + (piece - 2) * 256;
+    adst = G::BIAS + (wid - 4) * 256;
   }
 
-  auto issue = [&](int s, int buf, int gj) {
+  const int nst = a.d / kKS, spg = a.g / kKS, ntot = nst + a.nch;
+  const int slot_u = ngrp, slot_a = ngrp + (a.nch_u > 0 ? 1 : 0);
+  auto slot_of = [&](int s) {
+    return s < nst ? s / spg : (s - nst < a.nch_u ? slot_u : slot_a);
+  };
+  auto issue = [&](int s, int buf) {
     lds_u8* base = L + buf * G::STAGE;
-    const uint32_t kx = uint32_t(s) * (KS * 2), kcb = uint32_t(s) * (KS / 2);
+    if (s < nst) {
+      const uint32_t kx = uint32_t(s) * (kKS * 2), kcb = uint32_t(s) * (kKS / 2);
 #pragma unroll
-    for (int i = 0; i < G::NX; ++i) dma16(rx, base + (wid * G::NX + i) * 1024, xo[i] + kx);
-    if constexpr (G::NCW > 0) {
-#pragma unroll
-      for (int i = 0; i < G::NCW; ++i)
-        dma16(rc, base + G::XBYTES + (wid * G::NCW + i) * 1024, co[i] + kcb);
-      dma4(raux, base + adst, ao + uint32_t(gj) * 512u);
+      for (int i = 0; i < G::NX; ++i) dma16(rx, base + (wid * G::NX + i) * 1024, xo[i] + kx);
+      dma16(rc, base + G::XBYTES + wid * 1024, co + kcb);
     } else {
-      if (wid < 4) dma16(rc, base + G::XBYTES + wid * 1024, co[0] + kcb);
-      else dma4(raux, base + adst, ao + uint32_t(gj) * 512u);
+      const uint32_t c = uint32_t(s - nst);
+#pragma unroll
+      for (int i = 0; i < G::NX; ++i)
+        dma16(rt, base + (wid * G::NX + i) * 1024, xunit(i, trow) + c * 128);
+      dma16(ru, base + G::XBYTES + wid * 1024, cunit(urow) + c * 32);
+    }
+    dma4(raux, base + adst, ao + uint32_t(slot_of(s)) * 1024u);
+  };
+
+  // fragment offsets within a stage: residual stages take x chunks 2q + kc,
+  // expansion stages chunk 4 kc + q ([hi | mid] for kc = 0, [lo | 0] for
+  // kc = 1), matched by code dimensions 8 (q % 2) .. +7 of [c | c]
+  const uint32_t arow = uint32_t(128 * wm + lr) * (2 * kKS);
+  uint32_t aoff[2];
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc) aoff[kc] = arow + 16u * uint32_t((2 * q + kc) ^ swz_x(lr));
+  const uint32_t boff =
+      G::XBYTES + uint32_t(64 * wn + lr) * 32 + 16u * uint32_t((q >> 1) ^ swz_c(lr)) + 8u * (q & 1);
+
+  f32x4_t acc[8][4];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+
+  issue(0, 0);
+  if (ntot > 1) issue(1, 1);
+  int buf = 0;   // ring slot of stage s
+  auto next_stage = [&](int s) {
+    if (s + 1 < ntot) wait_loads_barrier<G::NL>();
+    else wait_loads_barrier<0>();
+    if (s + 2 < ntot) issue(s + 2, buf == 0 ? 2 : buf - 1);
+    const lds_u8* base = L + buf * G::STAGE;
+    buf = buf == 2 ? 0 : buf + 1;
+    return base;
+  };
+  // slot start: rescale to the slot's scale and add its bias
+  auto rescale = [&](const lds_u8* base) {
+    float rat[4];
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) rat[ni] = lds_load<float>(base + G::RAT + (64 * wn + 16 * ni + lr) * 4);
+#pragma unroll
+    for (int mi = 0; mi < 8; ++mi) {
+      const f32x4_t bias = lds_load<f32x4_t>(base + G::BIAS + (128 * wm + 16 * mi + 4 * q) * 4);
+#pragma unroll
+      for (int ni = 0; ni < 4; ++ni) acc[mi][ni] = acc[mi][ni] * rat[ni] + bias;
     }
   };
 
-  // fragment offsets within a stage
-  uint32_t aoff[KC];
-#pragma unroll
-  for (int kc = 0; kc < KC; ++kc)
-    aoff[kc] = uint32_t(64 * wm + lr) * (2 * KS) + 16u * uint32_t((q * KC + kc) ^ swz_x<KS>(lr));
-  uint32_t boff;
-  if constexpr (KS == 128) boff = uint32_t(64 * wn + lr) * 64 + 16u * uint32_t(q ^ swz_c<KS>(lr));
-  else if constexpr (KS == 64)
-    boff = uint32_t(64 * wn + lr) * 32 + 16u * uint32_t((q >> 1) ^ swz_c<KS>(lr)) + 8u * (q & 1);
-  else boff = uint32_t(64 * wn + lr) * 16 + 4u * q;
-  boff += G::XBYTES;
-
-  f32x4_t acc[4][4], D[4][4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f}, D[i][j] = acc[i][j];
-
-  const int nst = a.d / KS, spg = a.g / KS;
-  issue(0, 0, 0);
-  if (nst > 1) issue(1, 1, 1 / spg);
-  int buf = 0, sg = 0;   // ring slot of stage s; stage index within its group
+  int sg = 0;   // stage index within its scale group
 #pragma unroll 1
   for (int s = 0; s < nst; ++s) {
-    if (s + 1 < nst) wait_loads_barrier<G::NL>();
-    else wait_loads_barrier<0>();
-    if (s + 2 < nst) issue(s + 2, buf == 0 ? 2 : buf - 1, (s + 2) / spg);
-    const lds_u8* base = L + buf * G::STAGE;
-    const bool gstart = sg == 0, gend = sg == spg - 1;
-
-    uint32_t braw[4][KC];
+    const lds_u8* base = next_stage(s);
+    u32x2_t braw[4];
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      const lds_u8* p = base + boff + ni * 16 * (KS / 2);
-      if constexpr (KC == 4) {
-        const u32x4_t v = lds_load<u32x4_t>(p);
-        braw[ni][0] = v.x; braw[ni][KC > 1 ? 1 : 0] = v.y;
-        braw[ni][KC > 2 ? 2 : 0] = v.z; braw[ni][KC > 3 ? 3 : 0] = v.w;
-      } else if constexpr (KC == 2) {
-        const u32x2_t v = lds_load<u32x2_t>(p);
-        braw[ni][0] = v.x; braw[ni][KC > 1 ? 1 : 0] = v.y;
-      } else {
-        braw[ni][0] = lds_load<uint32_t>(p);
-      }
-    }
+    for (int ni = 0; ni < 4; ++ni) braw[ni] = lds_load<u32x2_t>(base + boff + ni * 16 * (kKS / 2));
+    if (sg == 0) rescale(base);
 #pragma unroll
-    for (int kc = 0; kc < KC; ++kc) {
-      bf16x8_t A[4], B[4];
-#pragma unroll
-      for (int mi = 0; mi < 4; ++mi) A[mi] = lds_load<bf16x8_t>(base + aoff[kc] + mi * 32 * KS);
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) B[ni] = unpack8(braw[ni][kc], kMask, kMagic);
-      if (kc == 0 && gstart) {
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi) {
-          const f32x4_t bias = lds_load<f32x4_t>(base + G::BIAS + (64 * wm + 16 * mi + 4 * q) * 4);
-#pragma unroll
-          for (int ni = 0; ni < 4; ++ni)
-            D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mi], B[ni], bias, 0, 0, 0);
-        }
-      } else {
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-          for (int ni = 0; ni < 4; ++ni)
-            D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[mi], B[ni], D[mi][ni], 0, 0, 0);
-      }
-    }
-    if (gend) {
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) {
-        const float sc = f16_to_f32(lds_load<uint16_t>(base + G::SCL + (64 * wn + 16 * ni + lr) * 2));
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi) acc[mi][ni] += sc * D[mi][ni];
-      }
-    }
-    buf = buf == 2 ? 0 : buf + 1;
-    sg = gend ? 0 : sg + 1;
-  }
-
-  // ---- rank-r expansion: the core part (U_c, t_c) then the correction (A_w, t_w)
-  const int R = a.rc + a.rr;
-  lds_u8* const TH = L;                                  // [3][kTM][kExpRow] bf16 (hi, mid, lo)
-  lds_u8* const TE = L + 3 * kTM * kExpRow * 2;          // [kTN][kExpRow] bf16 codes
-#pragma unroll 1
-  for (int part = 0; part < 2; ++part) {
-    const int r = part ? a.rr : a.rc;
-    if (r == 0) continue;
-    const int8_t* codes8 = part ? a.ca : a.cu;
-    const uint16_t* rscale = part ? a.sa : a.su;
-    const int toff = part ? a.rc : 0;
-#pragma unroll 1
-    for (int c0 = 0; c0 < r; c0 += 32) {
-      __syncthreads();
-      for (int e = tid; e < kTM * 32; e += kMBlock) {
-        const int row = e >> 5, k = e & 31, kk = c0 + k;
-        const int64_t m = row < rows ? m0 + row : a.M - 1;
-        const float v = kk < r ? a.t[m * R + toff + kk] : 0.f;
-        const __bf16 h = (__bf16)v;
-        const float r1 = v - float(h);
-        const __bf16 md = (__bf16)r1;
-        const __bf16 lo = (__bf16)(r1 - float(md));
-        const int o = (row * kExpRow + k) * 2;
-        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TH + o) = h;
-        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TH + kTM * kExpRow * 2 + o) = md;
-        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TH + 2 * kTM * kExpRow * 2 + o) = lo;
-      }
-      for (int e = tid; e < kTN * 32; e += kMBlock) {
-        const int col = e >> 5, k = e & 31, kk = c0 + k;
-        const int64_t v = col < cols ? v0 + col : a.V - 1;
-        const __bf16 cv = kk < r ? (__bf16)float(codes8[v * r + kk]) : (__bf16)0.f;
-        *reinterpret_cast<__attribute__((address_space(3))) __bf16*>(TE + (col * kExpRow + k) * 2) = cv;
-      }
-      __syncthreads();
+    for (int kc = 0; kc < 2; ++kc) {
       bf16x8_t B[4];
 #pragma unroll
-      for (int ni = 0; ni < 4; ++ni)
-        B[ni] = lds_load<bf16x8_t>(TE + ((64 * wn + 16 * ni + lr) * kExpRow + 8 * q) * 2);
+      for (int ni = 0; ni < 4; ++ni) B[ni] = unpack8(braw[ni][kc], kMask, kMagic);
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) {
-        const int o = ((64 * wm + 16 * mi + lr) * kExpRow + 8 * q) * 2;
-        const bf16x8_t hi = lds_load<bf16x8_t>(TH + o);
-        const bf16x8_t md = lds_load<bf16x8_t>(TH + kTM * kExpRow * 2 + o);
-        const bf16x8_t lo = lds_load<bf16x8_t>(TH + 2 * kTM * kExpRow * 2 + o);
+      for (int mi = 0; mi < 8; ++mi) {
+        const bf16x8_t A = lds_load<bf16x8_t>(base + aoff[kc] + mi * 32 * kKS);
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          f32x4_t dd = c0 == 0 ? f32x4_t{0.f, 0.f, 0.f, 0.f} : D[mi][ni];
-          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(hi, B[ni], dd, 0, 0, 0);
-          dd = __builtin_amdgcn_mfma_f32_16x16x32_bf16(md, B[ni], dd, 0, 0, 0);
-          D[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lo, B[ni], dd, 0, 0, 0);
-        }
+        for (int ni = 0; ni < 4; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
       }
     }
+    sg = sg == spg - 1 ? 0 : sg + 1;
+  }
+#pragma unroll 1
+  for (int s = nst; s < ntot; ++s) {
+    const lds_u8* base = next_stage(s);
+    u32x2_t braw[4];
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) braw[ni] = lds_load<u32x2_t>(base + boff + ni * 16 * (kKS / 2));
+    if (s == nst || s == nst + a.nch_u) rescale(base);
+    bf16x8_t B[4];
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) B[ni] = int8x8_to_bf16(braw[ni].x, braw[ni].y);
+#pragma unroll
+    for (int kc = 0; kc < 2; ++kc) {
+      const uint32_t eoff = arow + 16u * uint32_t((4 * kc + q) ^ swz_x(lr));
+#pragma unroll
+      for (int mi = 0; mi < 8; ++mi) {
+        const bf16x8_t A = lds_load<bf16x8_t>(base + eoff + mi * 32 * kKS);
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
+      }
+    }
+  }
+  {
+    const float* fin = a.fin + vt * kTN + 64 * wn + lr;
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) {
-      const int col = 64 * wn + 16 * ni + lr;
-      const float sc = f16_to_f32(rscale[col < cols ? v0 + col : a.V - 1]);
+      const float f = fin[16 * ni];
 #pragma unroll
-      for (int mi = 0; mi < 4; ++mi) acc[mi][ni] += sc * D[mi][ni];
+      for (int mi = 0; mi < 8; ++mi) acc[mi][ni] *= f;
     }
   }
 
   // ---- epilogue
   if constexpr (!CE) {
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+    for (int mi = 0; mi < 8; ++mi)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int row = 64 * wm + 16 * mi + 4 * q + i;
+        const int row = 128 * wm + 16 * mi + 4 * q + i;
         if (row >= rows) continue;
         const int64_t m = m0 + row;
 #pragma unroll
@@ -1077,17 +1043,28 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   } else {
     // per token row: (max, sum exp) over this tile's valid columns; the 16
     // lanes of a quarter-wave share rows, the four waves along the
-    // vocabulary are merged through LDS in a fixed order
-    float2* sred = reinterpret_cast<float2*>(mfma_lds);   // [4][kTM]
+    // vocabulary are merged through LDS in a fixed order.  Targets are
+    // staged in LDS as tile-local columns (-1: not in this tile).
+    float2* sred = reinterpret_cast<float2*>(mfma_lds);               // [4][kTM]
+    int* sy = reinterpret_cast<int*>(mfma_lds + 4 * kTM * sizeof(float2));   // [kTM]
     __syncthreads();
-#pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 64 * wm + 16 * mi + 4 * q + i;
-        const int64_t m = m0 + (row < rows ? row : rows - 1);
+    if (tid < kTM) {
+      int yl = -1;
+      if (tid < rows) {
+        const int64_t m = m0 + tid;
         const int64_t y = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m]
                                   : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m]);
+        if (y >= v0 && y < v0 + cols) yl = int(y - v0);
+      }
+      sy[tid] = yl;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mi = 0; mi < 8; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = 128 * wm + 16 * mi + 4 * q + i;
+        const int yl = sy[row];
         float mx = -INFINITY;
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
@@ -1100,7 +1077,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
           const int col = 64 * wn + 16 * ni + lr;
           if (col < cols) {
             se += fast_exp(acc[mi][ni][i] - mx);
-            if (v0 + col == y && row < rows) a.tgt_logit[m] = acc[mi][ni][i];
+            if (col == yl) a.tgt_logit[m0 + row] = acc[mi][ni][i];
           }
         }
 #pragma unroll
@@ -1118,33 +1095,67 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 }
 
 // ---------------------------------------------------- MFMA path: prologue
-// Per call, before stage 1: (a) the residual group scales in tile-major
-// order, rsT[vt][j][c] = s_res[min(vt kTN + c, V - 1), j], so a tile's scales
-// of one group are 512 contiguous bytes; (b) the factor codes of V_c and
-// B_w as bf16 (exact), wbf[k][i] for the R = r_c + r_r rows.
+// Per call, before stage 1: (a) per vocabulary tile and column the scale
+// ratios of the accumulator's scale slots (residual groups 0 .. d/g-1, then
+// s_U if r_c > 0, then s_A if r_r > 0): ratio[vt][k][c] = s'_{k-1} / s'_k
+// (0 for k = 0) and fin[vt][c] = s' of the last slot, where s' is the fp16
+// scale with zero replaced by kZeroScale; columns past V repeat row V-1;
+// (b) the factor codes of V_c and B_w as bf16 (exact), wbf[k][i] for the
+// R = r_c + r_r rows; (c) the codes of U_c and A_w side by side per
+// vocabulary row, each part zero-padded to a multiple of 16 dimensions, each
+// block of 16 stored twice.
 struct PrepArgs {
   const uint16_t* rs;
+  const uint16_t* su;
+  const uint16_t* sa;
   int64_t V;
-  int ngrp;
+  int ngrp, nslot;
   int64_t n_vt;
-  uint16_t* rsT;
+  float* ratio;
+  float* fin;
   const int8_t* cv;
   const int8_t* cb;
   int rc, rr, d;
   uint16_t* wbf;
+  const int8_t* cu;
+  const int8_t* ca;
+  int urow, rc_pad;      // bytes per ucodes row; padded dimensions of the U part
+  int8_t* ucodes;
 };
+
+__device__ __forceinline__ float nz_scale(uint16_t h) {
+  const float s = f16_to_f32(h);
+  return s == 0.f ? kZeroScale : s;
+}
 
 __global__ __launch_bounds__(kBlock) void k_prep(PrepArgs a) {
   const int64_t nthr = int64_t(gridDim.x) * kBlock;
   const int64_t t0 = int64_t(blockIdx.x) * kBlock + threadIdx.x;
-  // (a) one thread per (vocabulary tile, column): read the row's scales,
-  // write one per group (lanes write consecutive columns)
+  // (a) one thread per (vocabulary tile, column): walk the slots of the row
+  // (lanes write consecutive columns)
   for (int64_t e = t0; e < a.n_vt * kTN; e += nthr) {
     const int64_t vt = e / kTN, c = e % kTN;
     const int64_t v = vt * kTN + c < a.V ? vt * kTN + c : a.V - 1;
     const uint16_t* src = a.rs + v * a.ngrp;
-    uint16_t* dst = a.rsT + vt * int64_t(a.ngrp) * kTN + c;
-    for (int j = 0; j < a.ngrp; ++j) dst[int64_t(j) * kTN] = src[j];
+    float* dst = a.ratio + vt * int64_t(a.nslot) * kTN + c;
+    float prev = 0.f;
+    int k = 0;
+    for (; k < a.ngrp; ++k) {
+      const float s = nz_scale(src[k]);
+      dst[int64_t(k) * kTN] = k ? prev / s : 0.f;
+      prev = s;
+    }
+    if (a.rc) {
+      const float s = nz_scale(a.su[v]);
+      dst[int64_t(k++) * kTN] = prev / s;
+      prev = s;
+    }
+    if (a.rr) {
+      const float s = nz_scale(a.sa[v]);
+      dst[int64_t(k++) * kTN] = prev / s;
+      prev = s;
+    }
+    a.fin[vt * kTN + c] = prev;
   }
   // (b) 8 codes per thread
   const int64_t n8 = int64_t(a.rc + a.rr) * a.d / 8;
@@ -1162,12 +1173,35 @@ __global__ __launch_bounds__(kBlock) void k_prep(PrepArgs a) {
     }
     *reinterpret_cast<uint4*>(a.wbf + e * 8) = make_uint4(o[0], o[1], o[2], o[3]);
   }
+  // (c) 16 bytes per thread (row-major, so lanes write consecutive chunks)
+  const int64_t n16 = a.V * (a.urow / 16);
+  for (int64_t e = t0; e < n16; e += nthr) {
+    const int64_t v = e / (a.urow / 16);
+    const int j0 = int(e % (a.urow / 16)) * 16;
+    uint32_t w[4] = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int jj = 0; jj < 16; ++jj) {
+      const int j = (j0 / 32) * 16 + jj;   // dimension (both copies of a block)
+      int8_t c = 0;
+      if (j < a.rc_pad) {
+        if (j < a.rc) c = a.cu[v * a.rc + j];
+      } else if (j - a.rc_pad < a.rr) {
+        c = a.ca[v * a.rr + (j - a.rc_pad)];
+      }
+      w[jj / 4] |= uint32_t(uint8_t(c)) << (8 * (jj % 4));
+    }
+    *reinterpret_cast<uint4*>(a.ucodes + v * a.urow + j0) = make_uint4(w[0], w[1], w[2], w[3]);
+  }
 }
 
 // ---------------------------------------------------- MFMA path: stage 1
 // t[m, k] = sum over factor groups of s[k, grp] * (sum over the group of
 // c[k, i] x[m, i]) for the R factor rows (V_c then B_w), and the group biases
-// gbias[m / kTM][j][m % kTM] = -136 * (sum of x[m, i] over residual group j).
+// gbias[m / kTM][j][m % kTM] = -136 * (sum of x[m, i] over residual group j)
+// (0 for the expansion slots).  t leaves as three bf16 parts hi = bf16(t),
+// mid = bf16(t - hi), lo = bf16(t - hi - mid), laid out per block of 16 rank
+// dimensions as [hi | mid | lo | 0], the U_c part's blocks first, each part
+// zero-padded to whole blocks.
 // A workgroup takes 16 tokens and up to 64 factor rows (grid y); its eight
 // waves split d by residual groups and each holds 16 x 64 outputs as four
 // 16x16 MFMA tiles, loading the next K-chunk's fragments before the current
@@ -1182,8 +1216,10 @@ struct Stage1MArgs {
   int gv, rc;
   const uint16_t* sb;
   int gb, rr;
-  float* t;                // [M, R]
-  float* gbias;            // [n_mt][d/g][kTM]
+  uint16_t* tsplit;        // [M][nch][4][16] bf16 (hi, mid, lo, 0)
+  int nch, nch_u;
+  float* gbias;            // [n_mt][nslot][kTM]
+  int nslot;
 };
 
 constexpr int kS1MTok = 16, kS1MCols = 64, kS1MBlock = 512, kS1MWaves = kS1MBlock / 64;
@@ -1254,7 +1290,7 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
         for (int i = 0; i < 4; ++i) {
           const int64_t m = tok0 + 4 * q + i;
           if (m < a.M)
-            a.gbias[((m / kTM) * ngrp + j) * kTM + m % kTM] = -float(archead::kInt4Bias) * gs[i];
+            a.gbias[((m / kTM) * a.nslot + j) * kTM + m % kTM] = -float(archead::kInt4Bias) * gs[i];
         }
       }
       gs = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -1262,6 +1298,22 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
     A = An;
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) B[nb] = Bn[nb], s[nb] = sn[nb];
+  }
+  if (do_bias) {
+    // zero biases of the expansion slots and zero padding of the split t
+    const int nz = a.nslot - ngrp;
+    for (int e = threadIdx.x; e < kS1MTok * nz; e += kS1MBlock) {
+      const int64_t m = tok0 + e / nz;
+      if (m < a.M) a.gbias[((m / kTM) * a.nslot + ngrp + e % nz) * kTM + m % kTM] = 0.f;
+    }
+    const int pu = kExpDims * a.nch_u;   // padded dimensions of the U_c part
+    for (int e = threadIdx.x; e < kS1MTok * a.nch * 64; e += kS1MBlock) {
+      const int tt = e / (a.nch * 64), j = e % (a.nch * 64), blk = j / 64, w = j % 64;
+      const int dim = blk * kExpDims + w % kExpDims;
+      const bool pad = w >= 48 || (dim < pu ? dim >= a.rc : dim - pu >= a.rr);
+      const int64_t m = tok0 + tt;
+      if (m < a.M && pad) a.tsplit[(m * a.nch + blk) * 64 + w] = 0;
+    }
   }
   if (R == 0) return;
 #pragma unroll
@@ -1272,11 +1324,20 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
   for (int e = threadIdx.x; e < kS1MTok * kS1MCols; e += kS1MBlock) {
     const int tt = e / kS1MCols, c = e % kS1MCols;
     const int64_t m = tok0 + tt;
-    if (m < a.M && kb + c < R) {
+    const int k = kb + c;
+    if (m < a.M && k < R) {
       float v = red[0][tt][c];
 #pragma unroll
       for (int w = 1; w < kS1MWaves; ++w) v += red[w][tt][c];
-      a.t[m * R + kb + c] = v;
+      const __bf16 hi = (__bf16)v;
+      const float r1 = v - float(hi);
+      const __bf16 md = (__bf16)r1;
+      const __bf16 lo = (__bf16)(r1 - float(md));
+      const int dim = k < a.rc ? k : kExpDims * a.nch_u + (k - a.rc);
+      uint16_t* dst = a.tsplit + (m * a.nch + dim / kExpDims) * 64 + dim % kExpDims;
+      dst[0] = __builtin_bit_cast(uint16_t, hi);
+      dst[16] = __builtin_bit_cast(uint16_t, md);
+      dst[32] = __builtin_bit_cast(uint16_t, lo);
     }
   }
 }
@@ -1401,23 +1462,34 @@ int64_t gemv_grid(const archead_handle* h, int tok, bool ce) {
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
+int exp_chunks(int64_t r) { return int((r + kExpDims - 1) / kExpDims); }   // stages per part
+
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
   WsLayout w;
   if (!h || M <= 0) return w;
   const archead_desc& d = h->desc;
   size_t off = 0;
   const bool gemv = use_gemv(h, M);
-  w.t_off = off;
-  off = align256(off + sizeof(float) * size_t(M) * size_t(d.r_c + d.r_r));
-  if (!gemv) {
+  if (gemv) {
+    w.t_off = off;
+    off = align256(off + sizeof(float) * size_t(M) * size_t(d.r_c + d.r_r));
+  } else {
     const size_t ngrp = size_t(d.d / d.g);
+    const size_t nslot = ngrp + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
+    const size_t nch = size_t(exp_chunks(d.r_c) + exp_chunks(d.r_r));
     const size_t n_mt = size_t((M + kTM - 1) / kTM), n_vt = size_t((d.V + kTN - 1) / kTN);
+    w.ts_off = off;
+    off = align256(off + sizeof(uint16_t) * size_t(M) * nch * 64);   // [hi|mid|lo|0] x 16
     w.gb_off = off;
-    off = align256(off + sizeof(float) * n_mt * ngrp * kTM);
-    w.rst_off = off;
-    off = align256(off + sizeof(uint16_t) * n_vt * ngrp * kTN);
+    off = align256(off + sizeof(float) * n_mt * nslot * kTM);
+    w.rat_off = off;
+    off = align256(off + sizeof(float) * n_vt * nslot * kTN);
+    w.fin_off = off;
+    off = align256(off + sizeof(float) * n_vt * kTN);
     w.wbf_off = off;
     off = align256(off + sizeof(uint16_t) * size_t(d.r_c + d.r_r) * size_t(d.d));
+    w.uc_off = off;
+    off = align256(off + size_t(d.V) * nch * 32);                    // [c|c] x 16
   }
   if (op == ARCHEAD_OP_LOGITS_CE) {
     // GEMV: all CE passes share one grid (the smallest of the variants
@@ -1495,18 +1567,29 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
                                     int64_t ldx, const WsLayout& w, char* ws, hipStream_t s) {
   const archead_desc& d = h->desc;
   const int R = int(d.r_c + d.r_r);
+  const int nch_u = exp_chunks(d.r_c), nch = nch_u + exp_chunks(d.r_r);
   PrepArgs p;
   p.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
+  p.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
+  p.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
   p.V = d.V;
   p.ngrp = int(d.d / d.g);
+  p.nslot = p.ngrp + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
   p.n_vt = (d.V + kTN - 1) / kTN;
-  p.rsT = reinterpret_cast<uint16_t*>(ws + w.rst_off);
+  p.ratio = reinterpret_cast<float*>(ws + w.rat_off);
+  p.fin = reinterpret_cast<float*>(ws + w.fin_off);
   p.cv = static_cast<const int8_t*>(h->ptrs.core_v);
   p.cb = static_cast<const int8_t*>(h->ptrs.corr_b);
   p.rc = int(d.r_c); p.rr = int(d.r_r); p.d = int(d.d);
   p.wbf = reinterpret_cast<uint16_t*>(ws + w.wbf_off);
-  const int64_t work = std::max<int64_t>(p.n_vt * kTN, int64_t(R) * d.d / 8);
-  const int64_t pblocks = std::min<int64_t>((work + kBlock - 1) / kBlock, 4 * int64_t(h->n_cu));
+  p.cu = static_cast<const int8_t*>(h->ptrs.core_u);
+  p.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
+  p.urow = nch * 32;
+  p.rc_pad = nch_u * kExpDims;
+  p.ucodes = reinterpret_cast<int8_t*>(ws + w.uc_off);
+  const int64_t work = std::max({p.n_vt * kTN, int64_t(R) * d.d / 8, d.V * (p.urow / 16)});
+  const int64_t pblocks =
+      std::max<int64_t>(1, std::min<int64_t>((work + kBlock - 1) / kBlock, 4 * int64_t(h->n_cu)));
   hipLaunchKernelGGL(k_prep, dim3(unsigned(pblocks)), dim3(kBlock), 0, s, p);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "prologue launch");
@@ -1519,8 +1602,10 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
   a.gv = int(d.r_c ? d.g_v : d.d); a.rc = int(d.r_c);
   a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
   a.gb = int(d.r_r ? d.g_b : d.d); a.rr = int(d.r_r);
-  a.t = reinterpret_cast<float*>(ws + w.t_off);
+  a.tsplit = reinterpret_cast<uint16_t*>(ws + w.ts_off);
+  a.nch = nch; a.nch_u = nch_u;
   a.gbias = reinterpret_cast<float*>(ws + w.gb_off);
+  a.nslot = p.nslot;
   const int64_t mblocks = (M + kS1MTok - 1) / kS1MTok;
   const int64_t rblocks = R > 0 ? (R + kS1MCols - 1) / kS1MCols : 1;
   if (mblocks > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "M too large");
@@ -1599,17 +1684,18 @@ MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ld
   MfmaArgs a;
   memset(&a, 0, sizeof a);
   a.codes = static_cast<const uint8_t*>(h->ptrs.res_codes);
-  a.cu = static_cast<const int8_t*>(h->ptrs.core_u);
-  a.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
-  a.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
-  a.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx;
-  a.t = reinterpret_cast<const float*>(ws + w.t_off);
+  a.tsplit = reinterpret_cast<const uint16_t*>(ws + w.ts_off);
+  a.ucodes = reinterpret_cast<const int8_t*>(ws + w.uc_off);
   a.gbias = reinterpret_cast<const float*>(ws + w.gb_off);
-  a.rsT = reinterpret_cast<const uint16_t*>(ws + w.rst_off);
+  a.ratio = reinterpret_cast<const float*>(ws + w.rat_off);
+  a.fin = reinterpret_cast<const float*>(ws + w.fin_off);
   a.M = M; a.V = d.V;
-  a.d = int(d.d); a.g = int(d.g); a.rc = int(d.r_c); a.rr = int(d.r_r);
+  a.d = int(d.d); a.g = int(d.g);
+  a.nslot = int(d.d / d.g) + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
+  a.nch_u = exp_chunks(d.r_c);
+  a.nch = a.nch_u + exp_chunks(d.r_r);
   a.n_mt = (M + kTM - 1) / kTM;
   a.n_vt = (d.V + kTN - 1) / kTN;
   a.n_tiles = a.n_vt * a.n_mt;
@@ -1617,10 +1703,13 @@ MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ld
   return a;
 }
 
-template <int KS, bool CE>
-archead_status launch_mfma_ks(const archead_handle* h, MfmaArgs& a, hipStream_t s) {
-  const void* fn = reinterpret_cast<const void*>(k_mfma<KS, CE>);
-  const int lds = MGeom<KS>::LDS;
+archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStream_t s) {
+  // byte ranges of one tile's buffers must stay below 2 GiB
+  if (int64_t(kTM) * a.ldx * 2 >= (int64_t(1) << 31))
+    return fail(ARCHEAD_E_UNSUPPORTED, "ldx too large for the many-token kernel");
+  const void* fn = ce ? reinterpret_cast<const void*>(k_mfma<true>)
+                      : reinterpret_cast<const void*>(k_mfma<false>);
+  const int lds = MGeom::LDS;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return hip_fail(e, "MFMA LDS size attribute");
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
@@ -1630,15 +1719,6 @@ archead_status launch_mfma_ks(const archead_handle* h, MfmaArgs& a, hipStream_t 
   if (grid > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "too many MFMA tiles");
   e = hipExtLaunchKernel(fn, dim3(unsigned(grid)), dim3(kMBlock), args, size_t(lds), s, ev0, ev1, 0);
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "MFMA launch");
-}
-
-archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStream_t s) {
-  // x rows of a tile must lie within a 2 GiB buffer window
-  if (int64_t(kTM) * a.ldx * 2 >= (int64_t(1) << 31))
-    return fail(ARCHEAD_E_UNSUPPORTED, "ldx too large for the MFMA path");
-  if (a.g % 128 == 0) return ce ? launch_mfma_ks<128, true>(h, a, s) : launch_mfma_ks<128, false>(h, a, s);
-  if (a.g % 64 == 0) return ce ? launch_mfma_ks<64, true>(h, a, s) : launch_mfma_ks<64, false>(h, a, s);
-  return ce ? launch_mfma_ks<32, true>(h, a, s) : launch_mfma_ks<32, false>(h, a, s);
 }
 
 }  // namespace

@@ -29,7 +29,8 @@ int lanes_per_row(int64_t d) {
 }
 
 bool use_gemv(const archead_handle* h, int64_t M) {
-  return M <= h->gemv_max_m.load(std::memory_order_relaxed);
+  // the many-token kernel stages 64 codes of one scale group at a time
+  return M <= h->gemv_max_m.load(std::memory_order_relaxed) || h->desc.g % 64 != 0;
 }
 
 }  // namespace archead

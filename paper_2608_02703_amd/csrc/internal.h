@@ -35,10 +35,14 @@ int lanes_per_row(int64_t d);
 
 // Workspace carve-up (byte offsets, each 256-aligned).
 struct WsLayout {
-  size_t t_off = 0;      // fp32 [M, r_c + r_r]
-  size_t gb_off = 0;     // fp32 [n_mt][d/g][128] group biases (MFMA path)
-  size_t rst_off = 0;    // fp16 [n_vt][d/g][256] tile-major residual scales (MFMA path)
-  size_t wbf_off = 0;    // bf16 [r_c + r_r][d] factor codes (MFMA path)
+  size_t t_off = 0;      // fp32 [M, r_c + r_r] (decode path)
+  // many-token (MFMA) path only:
+  size_t ts_off = 0;     // bf16 [M][blocks][4][16] t split into hi, mid, lo (and 0)
+  size_t gb_off = 0;     // fp32 [n_mt][slots][256] slot biases
+  size_t rat_off = 0;    // fp32 [n_vt][slots][256] scale ratios
+  size_t fin_off = 0;    // fp32 [n_vt][256] final scales
+  size_t wbf_off = 0;    // bf16 [r_c + r_r][d] factor codes of V_c and B_w
+  size_t uc_off = 0;     // int8 [V][blocks][2][16] codes of U_c and A_w, padded, twice
   size_t part_off = 0;   // float2 [M, n_part] (CE)
   size_t tgt_off = 0;    // fp32 [M] (CE)
   size_t total = 0;
