@@ -784,6 +784,26 @@ __device__ __forceinline__ bf16x8_t unpack8(uint32_t q, uint32_t kMask, uint32_t
   return __builtin_bit_cast(bf16x8_t, p);
 }
 
+// max / sum over the 16 lanes of a row (DPP lane swaps within the row:
+// quad_perm [1,0,3,2], quad_perm [2,3,0,1], row_half_mirror, row_mirror)
+template <int CTRL>
+__device__ __forceinline__ float dpp_swap(float v) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+__device__ __forceinline__ float row16_max(float v) {
+  v = fmaxf(v, dpp_swap<0xB1>(v));
+  v = fmaxf(v, dpp_swap<0x4E>(v));
+  v = fmaxf(v, dpp_swap<0x141>(v));
+  return fmaxf(v, dpp_swap<0x140>(v));
+}
+__device__ __forceinline__ float row16_sum(float v) {
+  v += dpp_swap<0xB1>(v);
+  v += dpp_swap<0x4E>(v);
+  v += dpp_swap<0x141>(v);
+  return v + dpp_swap<0x140>(v);
+}
+
 // eight int8 codes (little-endian in two dwords) as bf16 (exact)
 __device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint32_t w0, uint32_t w1) {
   uint32_t p[4];
@@ -908,21 +928,35 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   auto slot_of = [&](int s) {
     return s < nst ? s / spg : (s - nst < a.nch_u ? slot_u : slot_a);
   };
-  auto issue = [&](int s, int buf) {
+  // load PART (0 .. NL-1) of this wave's share of stage s into ring slot buf
+  auto issue_part = [&](int s, int buf, int part) {
     lds_u8* base = L + buf * G::STAGE;
-    if (s < nst) {
-      const uint32_t kx = uint32_t(s) * (kKS * 2), kcb = uint32_t(s) * (kKS / 2);
-#pragma unroll
-      for (int i = 0; i < G::NX; ++i) dma16(rx, base + (wid * G::NX + i) * 1024, xo[i] + kx);
-      dma16(rc, base + G::XBYTES + wid * 1024, co + kcb);
+    if (part < G::NX) {
+      if (s < nst) dma16(rx, base + (wid * G::NX + part) * 1024, xo[part] + uint32_t(s) * (kKS * 2));
+      else dma16(rt, base + (wid * G::NX + part) * 1024, xunit(part, trow) + uint32_t(s - nst) * 128);
+    } else if (part == G::NX) {
+      if (s < nst) dma16(rc, base + G::XBYTES + wid * 1024, co + uint32_t(s) * (kKS / 2));
+      else dma16(ru, base + G::XBYTES + wid * 1024, cunit(urow) + uint32_t(s - nst) * 32);
     } else {
-      const uint32_t c = uint32_t(s - nst);
-#pragma unroll
-      for (int i = 0; i < G::NX; ++i)
-        dma16(rt, base + (wid * G::NX + i) * 1024, xunit(i, trow) + c * 128);
-      dma16(ru, base + G::XBYTES + wid * 1024, cunit(urow) + c * 32);
+      dma4(raux, base + adst, ao + uint32_t(slot_of(s)) * 1024u);
     }
-    dma4(raux, base + adst, ao + uint32_t(slot_of(s)) * 1024u);
+  };
+  auto issue = [&](int s, int buf) {
+#pragma unroll
+    for (int part = 0; part < G::NL; ++part) issue_part(s, buf, part);
+  };
+  // the same for a stage known to be a residual / an expansion stage
+  auto issue_main = [&](int s, int buf, int part) {
+    lds_u8* base = L + buf * G::STAGE;
+    if (part < G::NX) dma16(rx, base + (wid * G::NX + part) * 1024, xo[part] + uint32_t(s) * (kKS * 2));
+    else if (part == G::NX) dma16(rc, base + G::XBYTES + wid * 1024, co + uint32_t(s) * (kKS / 2));
+    else dma4(raux, base + adst, ao + uint32_t(s / spg) * 1024u);
+  };
+  auto issue_exp = [&](int s, int buf, int part) {
+    lds_u8* base = L + buf * G::STAGE;
+    if (part < G::NX) dma16(rt, base + (wid * G::NX + part) * 1024, xunit(part, trow) + uint32_t(s - nst) * 128);
+    else if (part == G::NX) dma16(ru, base + G::XBYTES + wid * 1024, cunit(urow) + uint32_t(s - nst) * 32);
+    else dma4(raux, base + adst, ao + uint32_t(slot_of(s)) * 1024u);
   };
 
   // fragment offsets within a stage: residual stages take x chunks 2q + kc,
@@ -943,15 +977,18 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 
   issue(0, 0);
   if (ntot > 1) issue(1, 1);
-  int buf = 0;   // ring slot of stage s
+  // The loads of stage s + 2 are issued one part at a time between the
+  // MFMAs of stage s's first K-chunk, so the waves' vector-memory traffic
+  // does not queue up in one burst after the barrier.
+  int buf = 0;   // ring slot of the next stage to compute
   auto next_stage = [&](int s) {
     if (s + 1 < ntot) wait_loads_barrier<G::NL>();
     else wait_loads_barrier<0>();
-    if (s + 2 < ntot) issue(s + 2, buf == 0 ? 2 : buf - 1);
     const lds_u8* base = L + buf * G::STAGE;
     buf = buf == 2 ? 0 : buf + 1;
     return base;
   };
+  static_assert(G::NL <= 8, "one load per MFMA row block of the first K-chunk");
   // slot start: rescale to the slot's scale and add its bias
   auto rescale = [&](const lds_u8* base) {
     float rat[4];
@@ -965,13 +1002,19 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
     }
   };
 
+  // Stage bodies; ISSUE says how the loads of stage s + 2 are issued:
+  // 0 none, 1 residual source, 2 expansion source, 3 either (checked).
   int sg = 0;   // stage index within its scale group
-#pragma unroll 1
-  for (int s = 0; s < nst; ++s) {
+  auto main_stage = [&](int s, auto issue_kind) {
+    constexpr int ISSUE = decltype(issue_kind)::value;
     const lds_u8* base = next_stage(s);
+    const int nb = buf == 2 ? 0 : buf + 1;   // ring slot of stage s + 2
     u32x2_t braw[4];
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) braw[ni] = lds_load<u32x2_t>(base + boff + ni * 16 * (kKS / 2));
+    bf16x8_t A[8];
+#pragma unroll
+    for (int mi = 0; mi < 8; ++mi) A[mi] = lds_load<bf16x8_t>(base + aoff[0] + mi * 32 * kKS);
     if (sg == 0) rescale(base);
 #pragma unroll
     for (int kc = 0; kc < 2; ++kc) {
@@ -980,17 +1023,23 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
       for (int ni = 0; ni < 4; ++ni) B[ni] = unpack8(braw[ni][kc], kMask, kMagic);
 #pragma unroll
       for (int mi = 0; mi < 8; ++mi) {
-        const bf16x8_t A = lds_load<bf16x8_t>(base + aoff[kc] + mi * 32 * kKS);
+        const bf16x8_t Am = A[mi];
+        if (kc == 0) A[mi] = lds_load<bf16x8_t>(base + aoff[1] + mi * 32 * kKS);
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
-          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
+          acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Am, B[ni], acc[mi][ni], 0, 0, 0);
+        if (kc == 0 && mi < G::NL) {
+          if constexpr (ISSUE == 1) issue_main(s + 2, nb, mi);
+          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi);
+        }
       }
     }
     sg = sg == spg - 1 ? 0 : sg + 1;
-  }
-#pragma unroll 1
-  for (int s = nst; s < ntot; ++s) {
+  };
+  auto exp_stage = [&](int s, auto issue_kind) {
+    constexpr int ISSUE = decltype(issue_kind)::value;
     const lds_u8* base = next_stage(s);
+    const int nb = buf == 2 ? 0 : buf + 1;
     u32x2_t braw[4];
 #pragma unroll
     for (int ni = 0; ni < 4; ++ni) braw[ni] = lds_load<u32x2_t>(base + boff + ni * 16 * (kKS / 2));
@@ -1007,9 +1056,26 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
+        if (kc == 0 && mi < G::NL) {
+          if constexpr (ISSUE == 2) issue_exp(s + 2, nb, mi);
+          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi);
+        }
       }
     }
-  }
+  };
+  using kNone = std::integral_constant<int, 0>;
+  using kMain = std::integral_constant<int, 1>;
+  using kExp = std::integral_constant<int, 2>;
+  using kAny = std::integral_constant<int, 3>;
+  int s = 0;
+#pragma unroll 1
+  for (; s + 2 < nst; ++s) main_stage(s, kMain{});
+#pragma unroll 1
+  for (; s < nst; ++s) main_stage(s, kAny{});
+#pragma unroll 1
+  for (; s + 2 < ntot; ++s) exp_stage(s, kExp{});
+#pragma unroll 1
+  for (; s < ntot; ++s) exp_stage(s, kNone{});
   {
     const float* fin = a.fin + vt * kTN + 64 * wn + lr;
 #pragma unroll
@@ -1069,8 +1135,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
           if (64 * wn + 16 * ni + lr < cols) mx = fmaxf(mx, acc[mi][ni][i]);
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+        mx = row16_max(mx);
         float se = 0.f;
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni) {
@@ -1080,8 +1145,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
             if (col == yl) a.tgt_logit[m0 + row] = acc[mi][ni][i];
           }
         }
-#pragma unroll
-        for (int off = 1; off < 16; off <<= 1) se += __shfl_xor(se, off, 64);
+        se = row16_sum(se);
         if (lr == 0) sred[wn * kTM + row] = make_float2(mx, se);
       }
     __syncthreads();
