@@ -8,16 +8,21 @@ expansion, logit store) for one decode token (M=1), with every input already
 resident in HBM.  The step rotates over three copies of the packed head
 (3 x 336 MB > the 256 MB Infinity Cache), so each step streams its head from
 HBM.  The headline value is decode GB/s over the packed bytes.  Secondary
-lines: decode M=4 and M=16, and the M=4096 prefill fused-CE pass (tok/s).
+lines: decode M=4 and M=16, and the M=4096 prefill fused-CE pass (tok/s and
+the many-token kernel's MFMA throughput).
 
 Prints one JSON line (rank 0, N=1).  --gpus N > 1 is refused: this build
-runs on one GPU.
+runs on one GPU.  --profile decode|prefill runs the same work without timing
+or JSON, for rocprofv3 (the decode form first copies 256 MiB once, the
+calibration kernel for the HBM byte counters).
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -28,7 +33,11 @@ sys.path.insert(0, ROOT)
 
 METRIC = "ARCHead head fwd: decode HBM GB/s (% peak) + prefill tok/s, V=151936 d=4096"
 PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
 N_COPIES = 3
+CALIBRATION_BYTES = 256 << 20
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_qwen_decode_traffic.md")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_02703_amd", "csrc", "archead.hip")
 
 
 def log(*a):
@@ -51,14 +60,38 @@ def gemv_algorithmic_bytes(h, M):
     """Bytes the head-streaming kernel must move once: residual codes and
     scales, the vocabulary-side factors and their scales, x, t and the fp32
     logits it writes."""
-    R = h.rc + h.rr
     return (h.V * h.d // 2 + h.V * (h.d // h.g) * 2 + h.V * (h.rc + h.rr) +
             (2 * h.V if h.rc else 0) + (2 * h.V if h.rr else 0) +
-            M * h.d * 2 + M * R * 4 + M * h.V * 4)
+            M * h.d * 2 + M * (h.rc + h.rr) * 4 + M * h.V * 4)
+
+
+def mfma_algorithmic_flops(h, M):
+    """Multiply-adds x 2 of one many-token pass: the residual contraction
+    over d and the rank-r expansion over r_c + r_r."""
+    return 2.0 * M * h.V * (h.d + h.rc + h.rr)
+
+
+def source_sha256():
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per decode launch from the committed counter summary, or
+    None if it is missing or was taken on a different kernel source."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    h = re.search(r"source_sha256:\s*([0-9a-f]{64})", text)
+    t = re.search(r"traffic_bytes_per_launch:\s*([0-9]+)", text)
+    if not h or not t or h.group(1) != source_sha256():
+        return None
+    return int(t.group(1))
 
 
 def time_decode(heads, x, steps, warmup, ws=None):
-    """(ms per step, mean head-kernel ms) for `steps` logits calls."""
+    """(ms per step, mean head-kernel ms, median head-kernel ms)."""
     import torch
     M = x.shape[0]
     outs = [torch.empty((M, heads[0].V), device="cuda") for _ in heads]
@@ -89,22 +122,33 @@ def time_decode(heads, x, steps, warmup, ws=None):
 
 
 def time_prefill(heads, x, y, steps, warmup):
+    """(ms per step, mean CE, mean many-token kernel ms)."""
     import torch
-    M = x.shape[0]
-    ws = [hd.workspace(M, 1, x.device) for hd in heads]
+    ws = [hd.workspace(x.shape[0], 1, x.device) for hd in heads]
     for i in range(warmup):
         heads[i % len(heads)].logits_ce(x, y, ws=ws[i % len(heads)])
     torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        b.record()
     t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
     t0.record()
     for i in range(steps):
-        ce, mean = heads[i % len(heads)].logits_ce(x, y, ws=ws[i % len(heads)])
+        k = i % len(heads)
+        heads[k].set_timing_events(*ev[i])
+        ce, mean = heads[k].logits_ce(x, y, ws=ws[k])
     t1.record()
     torch.cuda.synchronize()
-    return t0.elapsed_time(t1) / steps, float(mean.cpu()[0])
+    for hd in heads:
+        hd.set_timing_events(None, None)
+    kern = [a.elapsed_time(b) for a, b in ev]
+    return t0.elapsed_time(t1) / steps, float(mean.cpu()[0]), float(np.mean(kern))
 
 
-def cpu_baseline(h, xb, budget_s):
+def cpu_baseline(h, xb):
     """The fp64 oracle on the host cores: full head, one token (M=1)."""
     from oracle import head as ohead
     from oracle.bytes import head_bytes
@@ -119,6 +163,30 @@ def cpu_baseline(h, xb, budget_s):
                       f"({1 / sec:.3f} tok/s)"}
 
 
+def profile_run(kind, steps):
+    """The bench's work without timing, for rocprofv3."""
+    import torch
+    from synth import CONFIGS, make_head, make_targets, make_x
+    h = make_head("qwen_decode")
+    heads = upload_copies(h, N_COPIES)
+    if kind == "decode":
+        src = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda").fill_(3)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
+        x = torch.from_numpy(make_x("qwen_decode", 1).view(np.int16)).view(torch.bfloat16).cuda()
+        time_decode(heads, x, steps, 5)
+    else:
+        Mp = CONFIGS["qwen_prefill"]["Ms"][0]
+        x = torch.from_numpy(make_x("qwen_prefill", Mp).view(np.int16)).view(
+            torch.bfloat16).cuda()
+        y = torch.from_numpy(make_targets("qwen_prefill", Mp)).cuda()
+        time_prefill(heads, x, y, steps, 1)
+    torch.cuda.synchronize()
+    print(f"profile run {kind}: done", flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -127,6 +195,7 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--profile", choices=["decode", "prefill"])
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; multi-GPU (vocab-parallel) "
@@ -139,6 +208,9 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.profile:
+        profile_run(args.profile, args.steps if args.profile == "decode" else args.prefill_steps)
+        return
     cfg = "qwen_decode"
     log("generating the packed head ...")
     h = make_head(cfg)
@@ -163,10 +235,19 @@ def main():
         xp = torch.from_numpy(make_x("qwen_prefill", Mp).view(np.int16)).view(
             torch.bfloat16).cuda()
         yp = torch.from_numpy(make_targets("qwen_prefill", Mp)).cuda()
-        ms_p, mean_ce = time_prefill(heads, xp, yp, args.prefill_steps, 1)
-        prefill = {"M": Mp, "ms_per_step": ms_p, "tok_s": Mp / ms_p * 1e3,
-                   "mean_ce": mean_ce}
-        log(f"prefill CE M={Mp}: {ms_p:.2f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s")
+        ms_p, mean_ce, kern_p = time_prefill(heads, xp, yp, args.prefill_steps, 1)
+        flops = mfma_algorithmic_flops(h, Mp)
+        tflops = flops / (kern_p * 1e-3) / 1e12
+        prefill = {"M": Mp, "ms_per_step": round(ms_p, 4), "tok_s": round(Mp / ms_p * 1e3, 1),
+                   "mean_ce": mean_ce,
+                   "mfma_kernel": {"kernel": "k_mfma<true>", "kernel_ms": round(kern_p, 4),
+                                   "algorithmic_flops": flops,
+                                   "achieved_tflops": round(tflops, 1),
+                                   "peak_tflops": PEAK_BF16_TFLOPS,
+                                   "frac": round(tflops / PEAK_BF16_TFLOPS, 4)}}
+        log(f"prefill CE M={Mp}: {ms_p:.2f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s; "
+            f"many-token kernel {kern_p:.3f} ms = {tflops:.0f} TFLOP/s "
+            f"({100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak)")
 
     ms1, kern1, _ = res[1]
     value = pbytes / ms1 / 1e6          # GB/s
@@ -192,7 +273,7 @@ def main():
         "pct_peak_hbm": round(100 * value / PEAK_HBM_GBS, 2),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                     "traffic": None, "kernel": "k_gemv<1,64,false>",
+                     "traffic": measured_traffic(), "kernel": "k_gemv<1,64,false>",
                      "kernel_us": round(kern1 * 1e3, 2), "algorithmic_bytes": alg},
         "decode": {str(M): {"us_per_step": round(v[0] * 1e3, 2),
                             "kernel_us": round(v[1] * 1e3, 2),
@@ -202,7 +283,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (1 token, full head) ...")
-        out["cpu_baseline"] = cpu_baseline(h, xb, 30)
+        out["cpu_baseline"] = cpu_baseline(h, xb)
     print(json.dumps(out), flush=True)
 
 

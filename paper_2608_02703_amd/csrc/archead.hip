@@ -975,6 +975,15 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
+  // final scales and (CE) the targets of the tile's rows, loaded before the
+  // stage loads so they have arrived by the epilogue
+  float fin[4];
+#pragma unroll
+  for (int ni = 0; ni < 4; ++ni) fin[ni] = a.fin[vt * kTN + 64 * wn + 16 * ni + lr];
+  int64_t y_row = -1;
+  if (CE && tid < rows)
+    y_row = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m0 + tid]
+                    : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m0 + tid]);
   issue(0, 0);
   if (ntot > 1) issue(1, 1);
   // The loads of stage s + 2 are issued one part at a time between the
@@ -1076,15 +1085,10 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   for (; s + 2 < ntot; ++s) exp_stage(s, kExp{});
 #pragma unroll 1
   for (; s < ntot; ++s) exp_stage(s, kNone{});
-  {
-    const float* fin = a.fin + vt * kTN + 64 * wn + lr;
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) {
-      const float f = fin[16 * ni];
+  for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
-      for (int mi = 0; mi < 8; ++mi) acc[mi][ni] *= f;
-    }
-  }
+    for (int mi = 0; mi < 8; ++mi) acc[mi][ni] *= fin[ni];
 
   // ---- epilogue
   if constexpr (!CE) {
@@ -1114,16 +1118,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
     float2* sred = reinterpret_cast<float2*>(mfma_lds);               // [4][kTM]
     int* sy = reinterpret_cast<int*>(mfma_lds + 4 * kTM * sizeof(float2));   // [kTM]
     __syncthreads();
-    if (tid < kTM) {
-      int yl = -1;
-      if (tid < rows) {
-        const int64_t m = m0 + tid;
-        const int64_t y = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m]
-                                  : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m]);
-        if (y >= v0 && y < v0 + cols) yl = int(y - v0);
-      }
-      sy[tid] = yl;
-    }
+    if (tid < kTM) sy[tid] = y_row >= v0 && y_row < v0 + cols ? int(y_row - v0) : -1;
     __syncthreads();
 #pragma unroll
     for (int mi = 0; mi < 8; ++mi)

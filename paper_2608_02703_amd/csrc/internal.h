@@ -24,7 +24,7 @@ struct archead_handle {
 
 namespace archead {
 
-constexpr int64_t kDefaultGemvMaxM = 4;   // tokens per GEMV pass
+constexpr int64_t kDefaultGemvMaxM = 15;  // largest M on the decode kernel (measured crossover)
 constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
 
 archead_status fail(archead_status s, const char* fmt, ...);
