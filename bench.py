@@ -90,62 +90,71 @@ def measured_traffic():
     return int(t.group(1))
 
 
+def _timed_loop(fn, steps):
+    """ms per call of `steps` calls, bracketed by synchronize + events (no
+    per-call instrumentation)."""
+    import torch
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for i in range(steps):
+        fn(i)
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def _kernel_times(heads, fn, steps):
+    """Per-call durations (ms) of the head-streaming kernel: HIP events
+    attached to its dispatch (a separate pass; the markers cost a few us per
+    call, so the step time is measured without them)."""
+    import torch
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:        # create the underlying HIP events
+        a.record()
+        b.record()
+    torch.cuda.synchronize()
+    for i in range(steps):
+        heads[i % len(heads)].set_timing_events(*ev[i])
+        fn(i)
+    torch.cuda.synchronize()
+    for hd in heads:
+        hd.set_timing_events(None, None)
+    return [a.elapsed_time(b) for a, b in ev]
+
+
 def time_decode(heads, x, steps, warmup, ws=None):
     """(ms per step, mean head-kernel ms, median head-kernel ms)."""
     import torch
     M = x.shape[0]
     outs = [torch.empty((M, heads[0].V), device="cuda") for _ in heads]
     wss = [hd.workspace(M, 0, x.device) for hd in heads]
+
+    def step(i):
+        k = i % len(heads)
+        heads[k].logits(x, out=outs[k], ws=wss[k])
     for i in range(warmup):
-        k = i % len(heads)
-        heads[k].logits(x, out=outs[k], ws=wss[k])
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    for a, b in ev:        # create the underlying HIP events
-        a.record()
-        b.record()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record()
-    for i in range(steps):
-        k = i % len(heads)
-        heads[k].set_timing_events(*ev[i])
-        heads[k].logits(x, out=outs[k], ws=wss[k])
-    t1.record()
-    torch.cuda.synchronize()
-    for hd in heads:
-        hd.set_timing_events(None, None)
-    total = t0.elapsed_time(t1)
-    kern = [a.elapsed_time(b) for a, b in ev]
-    return total / steps, float(np.mean(kern)), float(np.median(kern))
+        step(i)
+    ms = _timed_loop(step, steps)
+    kern = _kernel_times(heads, step, min(steps, 100))
+    return ms, float(np.mean(kern)), float(np.median(kern))
 
 
 def time_prefill(heads, x, y, steps, warmup):
     """(ms per step, mean CE, mean many-token kernel ms)."""
     import torch
     ws = [hd.workspace(x.shape[0], 1, x.device) for hd in heads]
-    for i in range(warmup):
-        heads[i % len(heads)].logits_ce(x, y, ws=ws[i % len(heads)])
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(steps)]
-    for a, b in ev:
-        a.record()
-        b.record()
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    t0.record()
-    for i in range(steps):
+    res = {}
+
+    def step(i):
         k = i % len(heads)
-        heads[k].set_timing_events(*ev[i])
-        ce, mean = heads[k].logits_ce(x, y, ws=ws[k])
-    t1.record()
-    torch.cuda.synchronize()
-    for hd in heads:
-        hd.set_timing_events(None, None)
-    kern = [a.elapsed_time(b) for a, b in ev]
-    return t0.elapsed_time(t1) / steps, float(mean.cpu()[0]), float(np.mean(kern))
+        res["ce"] = heads[k].logits_ce(x, y, ws=ws[k])
+    for i in range(warmup):
+        step(i)
+    ms = _timed_loop(step, steps)
+    kern = _kernel_times(heads, step, steps)
+    return ms, float(res["ce"][1].cpu()[0]), float(np.mean(kern))
 
 
 def cpu_baseline(h, xb):
