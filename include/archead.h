@@ -139,7 +139,7 @@ archead_status archead_validate_desc(const archead_desc* desc);
 
 /* Create a handle for the head described by desc whose buffers are at ptrs
  * on the current HIP device.  The handle is host memory, immutable after
- * creation apart from archead_set_gemv_max_m, and may be used from several
+ * creation apart from the archead_set_* tuning calls, and may be used from several
  * threads and streams at once (each call with its own workspace).  Fails
  * with ARCHEAD_E_UNSUPPORTED if the current device is not gfx950 or there is
  * no device.  *out is set to NULL on failure. */
@@ -153,7 +153,8 @@ void archead_destroy(archead_handle* h);
 
 /* Bytes of workspace the call `op` needs for M tokens (0 for M == 0).  The
  * workspace holds the low-rank projections t (fp32 [M, r_c + r_r]; on the
- * MFMA path split into two bf16 parts), on the MFMA path also per-call
+ * MFMA decode path with a 32-bit call stamp beside each value; on the tiled
+ * MFMA path split into three bf16 parts), on the tiled path also per-call
  * tables derived from the head (group-scale ratios, the per-group sums of x,
  * the factor codes as bf16 and the U_c / A_w codes side by side: about
  * V * (r_c + r_r + 4 * (d/g + 3)) bytes), and for the CE call the
@@ -170,13 +171,25 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *            ARCHEAD_OP_LOGITS), 256-byte aligned; its contents on entry do
  *            not matter
  *   stream   hipStream_t to launch on (NULL = the default stream)
- * M == 0 returns ARCHEAD_OK without launching.  Small M (and heads with
- * g % 64 != 0) run the decode GEMV, which reads the head once per pass of 4
- * tokens; larger M run the tiled bf16 MFMA kernel (256 x 256 tiles of tokens
- * x vocabulary rows).  Both produce fp32 logits from fp32 accumulation; the
- * MFMA kernel carries its accumulator in units of the current scale group's
- * scale, and feeds the rank-r expansion t as two bf16 parts (t to 2^-17
- * relative), so its logits differ from the GEMV's in the last bits. */
+ * M == 0 returns ARCHEAD_OK without launching.  Three kernels serve the
+ * call, chosen by M and the head shape:
+ *   - M in the range of archead_set_dec_range (default 2 .. 32) with g in
+ *     {32, 64, 128}, (d/g) % 4 == 0, d/g <= 64, r_c and r_r multiples of 4
+ *     and at most 128 each, and V * d / 2 < 2^31: the MFMA decode kernel,
+ *     which streams the head once per pass of up to 16 tokens (fewer when
+ *     16 rows of x do not fit in LDS);
+ *   - otherwise M <= archead_get_gemv_max_m (default 15), or g % 64 != 0:
+ *     the decode GEMV (VALU dot products), one pass per 4 tokens;
+ * Both decode kernels compute t = x V_c^T, x B_w^T inside the same launch
+ * (a few leading workgroups publish t with a per-call stamp in the
+ * workspace; the others wait for it a bounded time and otherwise compute it
+ * themselves), so a decode step is a single kernel launch;
+ *   - otherwise the tiled bf16 MFMA kernel (256 x 256 tiles of tokens x
+ *     vocabulary rows).
+ * All produce fp32 logits from fp32 accumulation.  The tiled kernel carries
+ * its accumulator in units of the current scale group's scale and feeds the
+ * rank-r expansion t as three bf16 parts (t to fp32 precision), so its
+ * logits differ from the others' in the last bits. */
 archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
                               int64_t ldx, void* out, archead_dtype out_dtype,
                               int64_t ldo, void* ws, size_t ws_bytes,
@@ -199,12 +212,20 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x,
                                  float* mean_ce, void* ws, size_t ws_bytes,
                                  void* stream);
 
-/* Largest M served by the decode GEMV kernel; larger M use the MFMA kernel
- * (unless g % 64 != 0, which always takes the GEMV).
+/* Largest M served by the decode GEMV kernel when the MFMA decode kernel
+ * does not take the call; larger M use the tiled MFMA kernel (unless
+ * g % 64 != 0, which always takes the GEMV).
  * -1 restores the built-in threshold.  Not thread-safe with concurrent calls
  * on the same handle (set it once, after create). */
 archead_status archead_set_gemv_max_m(archead_handle* h, int64_t m);
 int64_t archead_get_gemv_max_m(const archead_handle* h);
+
+/* Range of M served by the MFMA decode kernel, min_m <= M <= max_m (an
+ * empty range, e.g. max_m = 0, never uses it; -1 restores the built-in
+ * bound, 2 and 32).  Same threading rule as archead_set_gemv_max_m.  get
+ * returns ARCHEAD_E_INVALID_ARG for a NULL argument. */
+archead_status archead_set_dec_range(archead_handle* h, int64_t min_m, int64_t max_m);
+archead_status archead_get_dec_range(const archead_handle* h, int64_t* min_m, int64_t* max_m);
 
 /* Profiling hook: when start and stop are non-NULL hipEvent_t handles
  * (created by the caller on the handle's device), every later compute call

@@ -21,6 +21,8 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <type_traits>
 #include <stdint.h>
 #include <string.h>
@@ -74,13 +76,18 @@ __device__ __forceinline__ float f16_to_f32(uint16_t h) {
 __device__ __forceinline__ float bf16_lo(uint32_t p) { return __uint_as_float(p << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
-// (x & m) | o in one VALU op.  The compiler splits it into v_and + v_or when
-// both constants are literals (gfx9 VOP3 has no literal operand), so the
-// constants are kept in registers and the fused instruction is named here.
+// (x & m) | o, selected as one v_and_or_b32.  With literal m and o the
+// compiler would split it into v_and + v_or (gfx9 VOP3 takes no literal), so
+// callers pass m and o through opaque_vgpr(), which hides their values and
+// keeps them in registers.  Plain C rather than inline asm: the hazard
+// recognizer does not see into inline asm, and a VALU write into a register
+// an in-flight MFMA still reads needs wait states it would then not insert.
+__device__ __forceinline__ uint32_t opaque_vgpr(uint32_t v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 __device__ __forceinline__ uint32_t and_or(uint32_t x, uint32_t m, uint32_t o) {
-  uint32_t r;
-  asm("v_and_or_b32 %0, %1, %2, %3" : "=v"(r) : "v"(x), "v"(m), "v"(o));
-  return r;
+  return (x & m) | o;
 }
 
 // Bf16 pair (136 + c) of INT4_V1 elements (8w + 2k, 8w + 2k + 1) of word q.
@@ -116,76 +123,125 @@ __device__ __forceinline__ float seg_sum(float v) {
   return v;
 }
 
-// ------------------------------------------------------------------ stage 1
-// (decode path) t[m, k] = sum_i (s[k, i/grp] c[k, i]) x[m, i] for the rows k
-// of V_c (k < r_c) then of B_w.  One workgroup per (k, block of 8 tokens): the 256
-// threads split d in 8-element pieces, every load of the row is issued before
-// the arithmetic, and the block sums the 256 partials.  s * c is exact in fp32
-// (11 x 8 significant bits).
-struct Stage1Args {
-  const uint16_t* x;
-  int64_t ldx, M, d;
-  const int8_t* cv;
+// ------------------------------------------------ stage 1 inside the launch
+// Both decode kernels compute t = x V_c^T, x B_w^T in the same launch as the
+// head stream: the first workgroups of the grid ("producers") take one rank
+// row per wave and publish each value t[m][k] together with the call's
+// epoch in one 64-bit store (agent scope, so the value and its stamp become
+// visible together on every XCD).  The other waves need t only at the end of
+// their first vocabulary step; they read the stamped values, poll a bounded
+// number of times until every stamp equals the epoch, and compute any value
+// whose stamp has not arrived by then themselves, so every wave finishes
+// whatever the scheduling of the producers.
+struct Stage1Ops {
+  const int8_t* cv;      // V_c codes [r_c, d], group scales [r_c, d / gv]
   const uint16_t* sv;
-  int64_t gv, rc;
-  const int8_t* cb;
+  const int8_t* cb;      // B_w codes [r_r, d], group scales [r_r, d / gb]
   const uint16_t* sb;
-  int64_t gb, rr;
-  float* t;  // [M, rc + rr]
-  int64_t mbase;  // first token of this launch
+  int gv, gb, rc, rr, d;
+  unsigned long long* tst;   // [tokens][r_c + r_r]: float bits | epoch << 32
+  uint32_t epoch;
+  int spin_limit;            // polls before the fallback
 };
 
-constexpr int kS1Tok = 8;
-constexpr int64_t kMaxGridY = 65535;
+__device__ __forceinline__ unsigned long long load_stamped(const unsigned long long* p) {
+  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
-__global__ __launch_bounds__(kBlock) void k_stage1(Stage1Args a) {
-  __shared__ float red[kWaves][kS1Tok];
-  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  const int64_t R = a.rc + a.rr;
-  const int64_t k = blockIdx.x, m0 = a.mbase + int64_t(blockIdx.y) * kS1Tok;
-  const bool core = k < a.rc;
-  const int8_t* crow = core ? a.cv + k * a.d : a.cb + (k - a.rc) * a.d;
-  const int64_t grp = core ? a.gv : a.gb;
-  const uint16_t* srow = core ? a.sv + k * (a.d / a.gv) : a.sb + (k - a.rc) * (a.d / a.gb);
-  const int ntok = int(a.M - m0 < kS1Tok ? a.M - m0 : kS1Tok);
-  float acc[kS1Tok];
+// Producer: t[tok0 + tt][k] for tt < M of rank row k (V_c rows first, then
+// B_w), one wave; x8(tt, i) gives the 8 bf16 values x[tt][i .. i + 7].
+// s * c is exact in fp32 (11 x 8 significant bits); fp32 accumulation.
+template <int TOKMAX, typename X8>
+__device__ __forceinline__ void s1_produce(const Stage1Ops& s, int k, int M, int64_t tok0,
+                                           X8 x8, int lane) {
+  const int d = s.d, R = s.rc + s.rr;
+  const bool core = k < s.rc;
+  const int8_t* crow = core ? s.cv + int64_t(k) * d : s.cb + int64_t(k - s.rc) * d;
+  const int grp = core ? s.gv : s.gb;
+  const uint16_t* srow =
+      core ? s.sv + int64_t(k) * (d / s.gv) : s.sb + int64_t(k - s.rc) * (d / s.gb);
+  float acc[TOKMAX];
 #pragma unroll
-  for (int j = 0; j < kS1Tok; ++j) acc[j] = 0.f;
-#pragma unroll 4
-  for (int64_t i = int64_t(threadIdx.x) * 8; i < a.d; i += kBlock * 8) {
-    const uint2 cw = *reinterpret_cast<const uint2*>(crow + i);
-    const float s = f16_to_f32(srow[i / grp]);
-    float w[8];
+  for (int tt = 0; tt < TOKMAX; ++tt) acc[tt] = 0.f;
+  // 8 pieces of 8 codes per lane at a time, all loads issued before the
+  // arithmetic (the head stream keeps the memory busy, so each round trip is
+  // long)
+  constexpr int kPieces = 8;
+  for (int base = lane * 8; base < d; base += 512 * kPieces) {
+    uint2 cw[kPieces];
+    uint16_t sw[kPieces];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      w[j] = float(int8_t(cw.x >> (8 * j))) * s;
-      w[4 + j] = float(int8_t(cw.y >> (8 * j))) * s;
+    for (int p = 0; p < kPieces; ++p) {
+      const int i = base + 512 * p;
+      const int ic = i < d ? i : base;
+      cw[p] = *reinterpret_cast<const uint2*>(crow + ic);
+      sw[p] = srow[ic / grp];
     }
 #pragma unroll
-    for (int tt = 0; tt < kS1Tok; ++tt) {
-      if (tt < ntok) {
-        const uint4 xv = *reinterpret_cast<const uint4*>(a.x + (m0 + tt) * a.ldx + i);
-        const uint32_t xs[4] = {xv.x, xv.y, xv.z, xv.w};
+    for (int p = 0; p < kPieces; ++p) {
+      const int i = base + 512 * p;
+      if (i < d) {
+        const float sc = f16_to_f32(sw[p]);
+        float w[8];
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-          acc[tt] = fmaf(bf16_lo(xs[j]), w[2 * j], acc[tt]);
-          acc[tt] = fmaf(bf16_hi(xs[j]), w[2 * j + 1], acc[tt]);
+          w[j] = float(int8_t(cw[p].x >> (8 * j))) * sc;
+          w[4 + j] = float(int8_t(cw[p].y >> (8 * j))) * sc;
+        }
+#pragma unroll
+        for (int tt = 0; tt < TOKMAX; ++tt) {
+          if (tt < M) {
+            const u32x4_t xv = x8(tt, i);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+              acc[tt] = fmaf(bf16_lo(xv[j]), w[2 * j], acc[tt]);
+              acc[tt] = fmaf(bf16_hi(xv[j]), w[2 * j + 1], acc[tt]);
+            }
+          }
         }
       }
     }
   }
 #pragma unroll
-  for (int tt = 0; tt < kS1Tok; ++tt) {
-    const float v = seg_sum<64>(acc[tt]);
-    if (lane == 0) red[wid][tt] = v;
+  for (int tt = 0; tt < TOKMAX; ++tt) {
+    if (tt < M) {
+      const float v = seg_sum<64>(acc[tt]);
+      if (lane == tt) {
+        const unsigned long long word =
+            (static_cast<unsigned long long>(s.epoch) << 32) | __float_as_uint(v);
+        __hip_atomic_store(s.tst + (tok0 + tt) * R + k, word, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
   }
-  __syncthreads();
-  if (threadIdx.x < ntok) {
-    const int tt = threadIdx.x;
-    float v = red[0][tt];
-    for (int w = 1; w < kWaves; ++w) v += red[w][tt];
-    a.t[(m0 + tt) * R + k] = v;
+}
+
+// Consumer: t[tok0 + tt][k], from its stamped word once the stamp equals the
+// epoch, else (after spin_limit polls) computed here by one thread in
+// element order; x2(tt, i) gives the bf16 pair x[tt][i], x[tt][i + 1].
+template <typename X2>
+__device__ float s1_value(const Stage1Ops& s, int64_t tok0, int tt, int k, X2 x2) {
+  const int R = s.rc + s.rr;
+  const unsigned long long* p = s.tst + (tok0 + tt) * R + k;
+  unsigned long long w = load_stamped(p);
+  for (int it = 0; uint32_t(w >> 32) != s.epoch && it < s.spin_limit; ++it) {
+    __builtin_amdgcn_s_sleep(2);
+    w = load_stamped(p);
   }
+  if (uint32_t(w >> 32) == s.epoch) return __uint_as_float(uint32_t(w));
+  const bool core = k < s.rc;
+  const int8_t* crow = core ? s.cv + int64_t(k) * s.d : s.cb + int64_t(k - s.rc) * s.d;
+  const int grp = core ? s.gv : s.gb;
+  const uint16_t* srow =
+      core ? s.sv + int64_t(k) * (s.d / s.gv) : s.sb + int64_t(k - s.rc) * (s.d / s.gb);
+  float acc = 0.f;
+  for (int i = 0; i < s.d; i += 2) {
+    const float sc = f16_to_f32(srow[i / grp]);
+    const uint32_t xp = x2(tt, i);
+    acc = fmaf(bf16_lo(xp), float(crow[i]) * sc, acc);
+    acc = fmaf(bf16_hi(xp), float(crow[i + 1]) * sc, acc);
+  }
+  return acc;
 }
 
 // ------------------------------------------------------------ decode GEMV
@@ -206,7 +262,8 @@ struct GemvArgs {
   const uint16_t* sa;
   const uint16_t* x;
   int64_t ldx;
-  const float* t;  // [M, rc + rr]
+  Stage1Ops s1;    // t of the pass's tokens, computed in the launch
+  int n_prod_blocks;  // leading workgroups that compute t
   int64_t tok0;    // first token of this pass
   int64_t V;
   int d, g, rc, rr;
@@ -328,6 +385,9 @@ __device__ __forceinline__ void apply_expansion(float (&acc)[RB][TOK], const Exp
         du = fmaf(float(int8_t(u >> 8)), t4.y, du);
         du = fmaf(float(int8_t(u >> 16)), t4.z, du);
         du = fmaf(float(int8_t(u >> 24)), t4.w, du);
+        // a lane without a dword read t4 from t[0..3], or with r_c + r_r = 0
+        // from LDS past t (stale bits, possibly NaN): drop du, not just its scale
+        du = valid ? du : 0.f;
         const float sc = valid ? f16_to_f32(uint16_t(e.s[rb][kd])) : 0.f;
         acc[rb][tt] = fmaf(sc, du, acc[rb][tt]);
       }
@@ -455,9 +515,12 @@ __device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvA
 #ifndef ARCHEAD_GEMV_WAVES
 #define ARCHEAD_GEMV_WAVES 3
 #endif
+#ifndef ARCHEAD_GEMV_WAVES_NARROW
+#define ARCHEAD_GEMV_WAVES_NARROW 2   // segments narrower than the wave
+#endif
 template <int TOK, int LPR, bool CE>
 __global__ __launch_bounds__(kBlock)
-__attribute__((amdgpu_waves_per_eu(TOK == 1 ? (LPR >= 64 ? ARCHEAD_GEMV_WAVES : 2) : 1)))
+__attribute__((amdgpu_waves_per_eu(TOK == 1 ? (LPR >= 64 ? ARCHEAD_GEMV_WAVES : ARCHEAD_GEMV_WAVES_NARROW) : 1)))
 void k_gemv(GemvArgs a) {
   constexpr int SEG = 64 / LPR;              // rows in flight per wave
   constexpr int RB = LPR < kRowsPerStep ? LPR : kRowsPerStep;
@@ -470,18 +533,28 @@ void k_gemv(GemvArgs a) {
   const int R = a.rc + a.rr;
   uint16_t* sx = reinterpret_cast<uint16_t*>(smem);          // [TOK][d]
   float* sxb = reinterpret_cast<float*>(sx + TOK * d);        // [TOK][C]
-  float* st = sxb + TOK * C;                                  // [TOK][R]
+  const int wid = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
+  float* st = sxb + TOK * C + wid * TOK * R;                  // this wave's t [TOK][R]
+  // x[tt][i .. i + 7] and x[tt][i], x[tt][i + 1] in the chunked LDS layout
+  auto x8 = [&](int tt, int i) {
+    return *reinterpret_cast<const u32x4_t*>(
+        reinterpret_cast<const uint4*>(sx) + (tt * 4 + ((i >> 3) & 3)) * C + (i >> 5));
+  };
+  auto x2 = [&](int tt, int i) {
+    return *reinterpret_cast<const uint32_t*>(
+        reinterpret_cast<const uint8_t*>(reinterpret_cast<const uint4*>(sx) +
+                                         (tt * 4 + ((i >> 3) & 3)) * C + (i >> 5)) +
+        2 * (i & 7));
+  };
 
-  {
-    const int x8 = d / 8;   // 16-byte units per token: unit u = chunk u/4, part u%4
-    for (int i = threadIdx.x; i < TOK * x8; i += kBlock) {
-      const int tt = i / x8, u = i - tt * x8;
+  // x into LDS (chunked layout) and the chunk biases -136 * (sum of x over
+  // the chunk); every wave of the workgroup calls this once
+  auto prologue = [&]() {
+    const int x8n = d / 8;  // 16-byte units per token: unit u = chunk u/4, part u%4
+    for (int i = threadIdx.x; i < TOK * x8n; i += kBlock) {
+      const int tt = i / x8n, u = i - tt * x8n;
       reinterpret_cast<uint4*>(sx)[(tt * 4 + (u & 3)) * C + (u >> 2)] =
           *reinterpret_cast<const uint4*>(a.x + (a.tok0 + tt) * a.ldx + u * 8);
-    }
-    for (int i = threadIdx.x; i < TOK * R; i += kBlock) {
-      const int tt = i / R;
-      st[i] = a.t[(a.tok0 + tt) * R + (i - tt * R)];
     }
     __syncthreads();
     for (int i = threadIdx.x; i < TOK * C; i += kBlock) {
@@ -495,22 +568,39 @@ void k_gemv(GemvArgs a) {
       sxb[i] = -float(archead::kInt4Bias) * s;
     }
     __syncthreads();
-  }
+  };
 
   const int lane = threadIdx.x & 63;
+  // stage-1 producers: one rank row per wave, the pass's tokens
+  if (int(blockIdx.x) < a.n_prod_blocks) {
+    prologue();
+    const int k = int(blockIdx.x) * kWaves + wid;
+    if (k < R) s1_produce<TOK>(a.s1, k, TOK, a.tok0, x8, lane);
+    return;
+  }
+  // this wave's copy of t, fetched when first needed (end of its first step)
+  bool t_ready = R == 0;
+  auto fetch_t = [&]() {
+    for (int e = lane; e < TOK * R; e += 64) {
+      const int tt = e / R;
+      st[e] = s1_value(a.s1, a.tok0, tt, e - tt * R, x2);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    t_ready = true;
+  };
+
   const int seg = lane / LPR, sl = lane % LPR;
   // Steps are dealt out grid-stride (wave gw takes steps gw, gw + W, ...), so
   // at any moment the whole grid streams one compact window of the head.
-  const int64_t W = int64_t(gridDim.x) * kWaves;
-  const int wid = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
-  const int64_t gw = int64_t(blockIdx.x) * kWaves + wid;
+  const int64_t W = int64_t(gridDim.x - a.n_prod_blocks) * kWaves;
+  const int64_t gw = int64_t(blockIdx.x - a.n_prod_blocks) * kWaves + wid;
   const uint32_t rowbytes = uint32_t(d) / 2;
   const uint32_t ngrp = uint32_t(d / a.g);
   const int my_row = row_of_lane<LPR, RB>(lane);   // row this lane ends up with
   const bool writer = (sl & (LPR / RB - 1)) == 0;
   // nibble-pair mask and bf16 128.0 bit pattern, held in registers
-  const uint32_t kMask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
-  const uint32_t kMagic = __builtin_amdgcn_readfirstlane(0x43004300u);
+  const uint32_t kMask = opaque_vgpr(0x000F000Fu);
+  const uint32_t kMagic = opaque_vgpr(0x43004300u);
 
   CeState<TOK> ce;
 #pragma unroll
@@ -533,7 +623,7 @@ void k_gemv(GemvArgs a) {
   // computes; codes and scales are read through buffer resources whose base
   // and per-row offsets live in scalar registers.
   const int64_t full_steps = a.vec_exp ? a.V / WR : 0;
-  if (gw < full_steps) {
+  {
     constexpr int kPD = ARCHEAD_GEMV_PREFETCH;
     constexpr int NB = kPD + 1;
     const uint32_t voff = uint32_t(seg) * rowbytes + uint32_t(sl) * 16u;
@@ -599,13 +689,18 @@ void k_gemv(GemvArgs a) {
     };
     int64_t cstep = gw, lstep = gw;   // compute and load cursors
     int cit = 0, lit = 0;
+    // the first loads of the head go out before the prologue, so the memory
+    // works while x and the chunk biases are set up
+    if (gw < full_steps) {
 #pragma unroll
-    for (int j = 0; j < kPD; ++j) {
-      const bool ok = lstep < full_steps;
-      load(ok ? lstep : last_step, ok ? lit : a.nit - 1, q[j], sc[j]);
-      advance(lstep, lit);
+      for (int j = 0; j < kPD; ++j) {
+        const bool ok = lstep < full_steps;
+        load(ok ? lstep : last_step, ok ? lit : a.nit - 1, q[j], sc[j]);
+        advance(lstep, lit);
+      }
+      load_exp(cstep, e);
     }
-    load_exp(cstep, e);
+    prologue();
     bool done = false;
     auto body = [&](auto J) {
       constexpr int j = decltype(J)::value;
@@ -616,21 +711,24 @@ void k_gemv(GemvArgs a) {
         advance(lstep, lit);
       }
       asm volatile("" ::: "memory");  // keep the loads ahead of the work below
-      if (cit == 0) apply_expansion<TOK, RB, KD, LPR>(acc, e, st, R, sl);
       int64_t nstep = cstep;
       int nit = cit;
       advance(nstep, nit);
       const bool more = nstep < full_steps;
-      if (nit == 0) load_exp(more ? nstep : cstep, e);
       gemv_chunk<TOK, RB>(acc, q[j], sc[j], sx, sxb, d, C, cit * LPR + sl, kMask, kMagic);
-      if (cit == a.nit - 1)
+      if (cit == a.nit - 1) {
+        // the step's rank-r expansion, then the next step's operands
+        if (!t_ready) fetch_t();
+        apply_expansion<TOK, RB, KD, LPR>(acc, e, st, R, sl);
+        load_exp(more ? nstep : cstep, e);
         gemv_epilogue<TOK, LPR, RB, CE, false>(acc, a, cstep * WR, uint32_t(WR - 1), seg, sl,
                                                lane, my_row, writer, st, ce);
+      }
       cstep = nstep;
       cit = nit;
       done = !more;
     };
-    while (true) {
+    while (gw < full_steps) {
       body(std::integral_constant<int, 0>{});
       if (done) break;
       body(std::integral_constant<int, 1>{});
@@ -670,6 +768,7 @@ void k_gemv(GemvArgs a) {
       }
       gemv_chunk<TOK, RB>(acc, q, sc, sx, sxb, d, C, int(c), kMask, kMagic);
     }
+    if (!t_ready) fetch_t();
     gemv_epilogue<TOK, LPR, RB, CE, true>(acc, a, row0, lim, seg, sl, lane, my_row, writer, st,
                                           ce);
   }
@@ -690,7 +789,7 @@ void k_gemv(GemvArgs a) {
       const int tt = threadIdx.x;
       float m = red[0][tt].x, s = red[0][tt].y;
       for (int w = 1; w < kWaves; ++w) lse_merge(m, s, red[w][tt].x, red[w][tt].y);
-      a.part[(a.tok0 + tt) * a.n_part + blockIdx.x] = make_float2(m, s);
+      a.part[(a.tok0 + tt) * a.n_part + (blockIdx.x - a.n_prod_blocks)] = make_float2(m, s);
     }
   }
 }
@@ -865,8 +964,8 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wid >> 2, wn = wid & 3;
   const int lr = lane & 15, q = lane >> 4;
-  const uint32_t kMask = __builtin_amdgcn_readfirstlane(0x000F000Fu);
-  const uint32_t kMagic = __builtin_amdgcn_readfirstlane(0x43004300u);
+  const uint32_t kMask = opaque_vgpr(0x000F000Fu);
+  const uint32_t kMagic = opaque_vgpr(0x43004300u);
   const int ngrp = a.d / a.g;
   const uint32_t rowbytes = uint32_t(a.d) / 2;
   const uint32_t ldx2 = uint32_t(a.ldx) * 2;
@@ -1448,6 +1547,405 @@ __global__ __launch_bounds__(kBlock) void k_mean(const float* v, int64_t n, floa
   if (threadIdx.x == 0) *out = s[0] / float(n);
 }
 
+// ------------------------------------------------------------ decode: MFMA
+// Decode-shaped kernel for up to 16 tokens per pass: the packed head is
+// streamed once per pass while bf16 MFMAs (v_mfma_f32_16x16x32_bf16) do the
+// dot products, so the vector ALUs only unpack codes and apply scales, and
+// the cost per pass is the same for 1 and for 16 tokens.
+//
+// A wave owns units of 16 vocabulary rows (grid-stride over the units, every
+// wave the same number but for the last round).  Lane l holds row j = l % 16
+// of the unit and quarter q = l / 16.  A unit is walked in iterations:
+//  * one per residual group G (GW = g / 32 code words per lane): lane (j, q)
+//    loads words q GW .. q GW + GW - 1 of group G of its row, MFMA kc takes
+//    word q GW + kc, i.e. the 8 elements G g + 8 (q GW + kc) .. +7, whose
+//    INT4 codes unpack to the bf16 values 136 + c (the same element order as
+//    the x fragment read from LDS).  The first MFMA's accumulator input is
+//    the group's offset bias -136 * (sum of x over the group), so the chain
+//    yields the group partial sum c x; the fp16 group scale multiplies it
+//    into the running fp32 total.
+//  * then the rank-r expansion, 16 GW rank dimensions per iteration (U_c
+//    part first, then A_w; each zero-padded): lane (j, q) loads the int8
+//    codes of dims q 4GW .. +4GW-1 and fp32 MFMAs (v_mfma_f32_16x16x4_f32)
+//    multiply them with t (fp32, exact codes); the row scale s_U or s_A
+//    multiplies the result into the total.
+// Output lane (j, q) holds tokens 4q .. 4q+3 of row j.
+//
+// Stage 1 (t = x V_c^T, x B_w^T) runs in the same launch: the first
+// n_prod_blocks workgroups compute one rank row per wave and publish each
+// value together with the call's epoch in one 64-bit store.  The other
+// workgroups need t only at their first expansion iteration; there each
+// thread reads its share of the stamped values, waits (a bounded number of
+// polls) until every stamp equals the epoch, and copies them to LDS.  A
+// value whose stamp never arrives within the bound is computed by the
+// waiting thread itself, so every wave finishes whatever the scheduling.
+constexpr int kDBlock = 512, kDWaves = kDBlock / 64;
+constexpr int kDTok = 16;                    // tokens per pass (MFMA rows)
+#ifndef ARCHEAD_DEC_PREFETCH
+#define ARCHEAD_DEC_PREFETCH 3
+#endif
+constexpr int kDecPD = ARCHEAD_DEC_PREFETCH;  // steps of loads in flight
+constexpr int kDecSG = 4;                     // residual groups per step
+#ifndef ARCHEAD_DEC_CPOL
+#define ARCHEAD_DEC_CPOL 2
+#endif
+constexpr int kDecCpol = ARCHEAD_DEC_CPOL;     // cache policy of the code loads
+
+struct DecArgs {
+  const uint8_t* codes;
+  const uint16_t* rs;
+  const int8_t* cu;
+  const uint16_t* su;
+  const int8_t* ca;
+  const uint16_t* sa;
+  Stage1Ops s1;
+  const uint16_t* x;
+  int64_t ldx;
+  int64_t tok0;          // first token of this pass
+  int M;                 // tokens of this pass (1 .. 16)
+  int64_t V;
+  int d, g, rc, rr;
+  int ngrp, kcu, kca;    // residual groups; expansion K-chunks (32 dims) of U_c / A_w
+  int64_t n_units;       // ceil(V / 16)
+  int64_t n_waves;       // consumer waves (grid-stride over units)
+  int n_prod_blocks;     // leading workgroups that compute t
+  int xstr;              // LDS: bytes per token row of x
+  int tstr;              // LDS: bf16 elements per token row of each part of t
+  int off_bias, off_t, off_red;   // LDS byte offsets
+  void* out;
+  int64_t ldo;
+  int out_bf16;
+  const void* tgt;
+  int tgt64;
+  float2* part;          // [tokens, n_part]
+  int64_t n_part;
+  float* tgt_logit;
+};
+
+// Calls f(integral_constant<J>) for J = I .. N-1 until one returns true.
+template <int I, int N, typename F>
+__device__ __forceinline__ bool unroll_until(F& f) {
+  if constexpr (I < N) {
+    if (f(std::integral_constant<int, I>{})) return true;
+    return unroll_until<I + 1, N>(f);
+  }
+  return false;
+}
+
+template <int GW, bool CE>
+__global__ __launch_bounds__(kDBlock) __attribute__((amdgpu_waves_per_eu(2)))
+void k_dec(DecArgs a) {
+  static_assert(GW == 1 || GW == 2 || GW == 4, "code words per lane and group");
+  extern __shared__ __align__(16) uint8_t dec_lds[];
+  lds_u8* const L = (lds_u8*)dec_lds;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int lr = lane & 15, q = lane >> 4;
+  const int M = a.M, d = a.d, g = a.g;
+  const int R = a.rc + a.rr;
+  const int ngrp = a.ngrp;
+
+  // ---- prologue: x rows of the pass -> LDS, offset biases, zero t padding
+  // (every wave of the workgroup calls this once)
+  auto prologue = [&]() {
+    const int x16 = d / 8;
+    for (int e = tid; e < M * x16; e += kDBlock) {
+      const int tt = e / x16, u = e - tt * x16;
+      *reinterpret_cast<__attribute__((address_space(3))) u32x4_t*>(L + tt * a.xstr + 16 * u) =
+          *reinterpret_cast<const u32x4_t*>(a.x + (a.tok0 + tt) * a.ldx + 8 * u);
+    }
+    __syncthreads();
+    auto* sb = reinterpret_cast<__attribute__((address_space(3))) float*>(L + a.off_bias);
+    for (int e = tid; e < ngrp * kDTok; e += kDBlock) {
+      const int G = e / kDTok, tt = e % kDTok;
+      float s = 0.f;
+      if (tt < M) {
+        const lds_u8* p = L + tt * a.xstr + 2 * G * g;
+        for (int i = 0; i < g / 8; ++i) {
+          const u32x4_t u = lds_load<u32x4_t>(p + 16 * i);
+          s += bf16_lo(u.x) + bf16_hi(u.x) + bf16_lo(u.y) + bf16_hi(u.y) + bf16_lo(u.z) +
+               bf16_hi(u.z) + bf16_lo(u.w) + bf16_hi(u.w);
+        }
+      }
+      sb[e] = -float(archead::kInt4Bias) * s;
+    }
+    auto* st = reinterpret_cast<__attribute__((address_space(3))) uint16_t*>(L + a.off_t);
+    for (int e = tid; e < 3 * M * a.tstr; e += kDBlock) st[e] = 0;
+    __syncthreads();
+  };
+
+  // ---- stage-1 producers: one rank row per wave, all tokens of the pass
+  if (int(blockIdx.x) < a.n_prod_blocks) {
+    prologue();
+    const int k = int(blockIdx.x) * kDWaves + wid;
+    if (k < R)
+      s1_produce<kDTok>(a.s1, k, M, a.tok0,
+                        [&](int tt, int i) { return lds_load<u32x4_t>(L + tt * a.xstr + 2 * i); },
+                        lane);
+    return;
+  }
+
+  // ---- consumers
+  const int64_t cw = int64_t(blockIdx.x - a.n_prod_blocks) * kDWaves + wid;
+  const int64_t W = a.n_waves;
+  const int nu = cw < W ? int((a.n_units - cw + W - 1) / W) : 0;   // units of this wave
+  const int kcu = a.kcu, kca = a.kca;      // expansion K-chunks (32 rank dims) of U_c, A_w
+  const uint32_t rowbytes = uint32_t(d) / 2;
+  const uint32_t kMask = opaque_vgpr(0x000F000Fu);
+  const uint32_t kMagic = opaque_vgpr(0x43004300u);
+  const int xr = lr < M ? lr : M - 1;                  // token row of this lane's A fragments
+  const lds_u8* const xrow = L + xr * a.xstr + 16 * q * GW;
+  const lds_u8* const brow = L + a.off_bias + 16 * q;
+  const int tpart = M * a.tstr;                        // bf16 elements per part of t in LDS
+  const lds_u8* const trow = L + a.off_t + 2 * (xr * a.tstr);
+  // this lane's byte offsets within a unit's rows
+  const int voff_c = int(uint32_t(lr) * rowbytes) + q * (4 * GW);        // codes: row lr, quarter q
+  const int voff_sc = (lane >> 2) * (2 * ngrp) + 16 * (lane & 3);       // scales: row lane/4
+  const int voff_u = lr * a.rc + q * (8 * kcu);
+  const int voff_a = lr * a.rr + q * (8 * kca);
+
+  CeState<4> ce;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    ce.mx[r] = -INFINITY;
+    ce.se[r] = 0.f;
+    ce.y[r] = -1;
+    if (CE && 4 * q + r < M)
+      ce.y[r] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + 4 * q + r]
+                        : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + 4 * q + r]);
+  }
+
+  // buffer resource over the rows of unit u of an array with `stride` bytes
+  // per vocabulary row (rows past V read as zero)
+  auto unit_rsrc = [&](const void* base, int64_t u, uint32_t stride) {
+    const int64_t v0 = u * 16;
+    const uint32_t rows = uint32_t(a.V - v0 < 16 ? a.V - v0 : 16);
+    return __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<char*>(static_cast<const char*>(base)) + v0 * stride, 0, int(rows * stride),
+        kBufferWord3);
+  };
+  // The residual scales of a unit (16 rows x d/g fp16, contiguous) arrive as
+  // one 16-byte load per lane and 32 groups (lane l: row l/4, groups
+  // 8 (l % 4) .. +7); a lane takes the scale of its own row from the lane
+  // holding it with ds_bpermute.
+  auto load_scales = [&](int64_t u, u32x4_t (&dst)[2]) {
+    const __amdgpu_buffer_rsrc_t r_ = unit_rsrc(a.rs, u, 2u * ngrp);
+    dst[0] = __builtin_amdgcn_raw_buffer_load_b128(r_, voff_sc, 0, 0);
+    if (ngrp > 32) dst[1] = __builtin_amdgcn_raw_buffer_load_b128(r_, voff_sc, 64, 0);
+  };
+
+  // The head is walked in steps of kDecSG residual groups (one code load
+  // per group).
+  constexpr int SG = kDecSG;
+  const int nsg = ngrp / SG;                     // steps per unit
+  constexpr int NB = kDecPD + 1;
+  u32x4_t cbuf[NB][SG];
+  // load cursor: unit lu (the lk-th of this wave), step lS
+  int64_t lu = cw;
+  int lk = 0, lS = 0;
+  __amdgpu_buffer_rsrc_t lrc = unit_rsrc(a.codes, lu, rowbytes);
+  auto load_next = [&](int slot) {
+#pragma unroll
+    for (int k = 0; k < SG; ++k) {
+      const int so = (lS * SG + k) * (g / 2);
+      if constexpr (GW == 4) {
+        cbuf[slot][k] = __builtin_amdgcn_raw_buffer_load_b128(lrc, voff_c, so, kDecCpol);
+      } else if constexpr (GW == 2) {
+        const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(lrc, voff_c, so, kDecCpol);
+        cbuf[slot][k] = u32x4_t{v.x, v.y, 0u, 0u};
+      } else {
+        cbuf[slot][k] = u32x4_t{__builtin_amdgcn_raw_buffer_load_b32(lrc, voff_c, so, kDecCpol),
+                                0u, 0u, 0u};
+      }
+    }
+    // past the wave's last step the cursor stays there (repeated, unused)
+    if (++lS == nsg) {
+      if (lk + 1 < nu) {
+        lS = 0;
+        ++lk;
+        lu += W;
+        lrc = unit_rsrc(a.codes, lu, rowbytes);
+      } else {
+        lS = nsg - 1;
+      }
+    }
+  };
+  u32x4_t scur[2], snext[2];
+  // the first loads of the head go out before the prologue, so the memory
+  // works while x, the biases and the t padding are set up
+  if (nu > 0) {
+    load_scales(cw, scur);
+#pragma unroll
+    for (int j = 0; j < kDecPD; ++j) load_next(j);
+  }
+  prologue();
+
+  // t from the producers into LDS, split into three bf16 parts hi = bf16(t),
+  // mid = bf16(t - hi), lo = bf16(t - hi - mid) (their sum is t to fp32
+  // precision) for the bf16 MFMAs of the expansion.  Every consumer wave
+  // takes a share, then a workgroup barrier.  A wave does this when it
+  // first needs t, at the end of its first unit (the producers have long
+  // finished by then), or at its end if it has no unit.
+  bool t_ready = R == 0;
+  auto fetch_t = [&]() {
+    auto* st = reinterpret_cast<__attribute__((address_space(3))) uint16_t*>(L + a.off_t);
+    for (int e = tid; e < M * R; e += kDBlock) {
+      const int tt = e / R, k = e - tt * R;
+      const float v = s1_value(a.s1, a.tok0, tt, k, [&](int t2, int i) {
+        return lds_load<uint32_t>(L + t2 * a.xstr + 2 * i);
+      });
+      const __bf16 hi = (__bf16)v;
+      const float r1 = v - float(hi);
+      const __bf16 md = (__bf16)r1;
+      const __bf16 lo = (__bf16)(r1 - float(md));
+      const int o = tt * a.tstr + (k < a.rc ? k : 32 * kcu + (k - a.rc));
+      st[o] = __builtin_bit_cast(uint16_t, hi);
+      st[tpart + o] = __builtin_bit_cast(uint16_t, md);
+      st[2 * tpart + o] = __builtin_bit_cast(uint16_t, lo);
+    }
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    t_ready = true;
+  };
+
+  if (nu > 0) {
+    const int64_t n_it = int64_t(nu) * nsg;
+    const int s_issue = nsg > kDecPD ? nsg - kDecPD : 0;   // step that loads the next unit's operands
+    int64_t cu_ = cw;   // compute cursor: unit (the ck-th of this wave) and step
+    int ck = 0, cS = 0;
+    int64_t done_it = 0;
+    f32x4_t tot = {0.f, 0.f, 0.f, 0.f};
+    // expansion operands of the unit being computed (codes of dims
+    // q 8 kc .. +8 kc - 1 of the lane's row, kc K-chunks per part) and its
+    // row scales, loaded s_issue steps into the unit
+    u32x2_t eu[4], ea[4];
+    uint32_t esu = 0, esa = 0;
+    auto load_exp = [&]() {
+      const __amdgpu_buffer_rsrc_t ru = unit_rsrc(a.cu, cu_, uint32_t(a.rc));
+      const __amdgpu_buffer_rsrc_t ra = unit_rsrc(a.ca, cu_, uint32_t(a.rr));
+#pragma unroll
+      for (int kc = 0; kc < 4; ++kc) {
+        if (kc < kcu) eu[kc] = __builtin_amdgcn_raw_buffer_load_b64(ru, voff_u, 8 * kc, 0);
+        if (kc < kca) ea[kc] = __builtin_amdgcn_raw_buffer_load_b64(ra, voff_a, 8 * kc, 0);
+      }
+      if (kcu) esu = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.su, cu_, 2u), 2 * lr, 0, 0);
+      if (kca) esa = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.sa, cu_, 2u), 2 * lr, 0, 0);
+    };
+    auto finish_unit = [&]() {
+      if (!t_ready) fetch_t();
+      if (kcu + kca > 0) {
+        f32x4_t au = {0.f, 0.f, 0.f, 0.f}, aa = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kc = 0; kc < 4; ++kc) {
+          if (kc < kcu) {
+            const bf16x8_t B = int8x8_to_bf16(eu[kc].x, eu[kc].y);
+            const lds_u8* tp = trow + 2 * (q * 8 * kcu + 8 * kc);
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+              au = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_load<bf16x8_t>(tp + 2 * p * tpart),
+                                                           B, au, 0, 0, 0);
+          }
+          if (kc < kca) {
+            const bf16x8_t B = int8x8_to_bf16(ea[kc].x, ea[kc].y);
+            const lds_u8* tp = trow + 2 * (32 * kcu + q * 8 * kca + 8 * kc);
+#pragma unroll
+            for (int p = 0; p < 3; ++p)
+              aa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(lds_load<bf16x8_t>(tp + 2 * p * tpart),
+                                                           B, aa, 0, 0, 0);
+          }
+        }
+        tot += f16_to_f32(uint16_t(esu)) * au + f16_to_f32(uint16_t(esa)) * aa;
+      }
+      const int64_t v = cu_ * 16 + lr;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int tt = 4 * q + r;
+        if (tt < M && v < a.V) {
+          const float l = tot[r];
+          if constexpr (!CE) {
+            const int64_t o = (a.tok0 + tt) * a.ldo + v;
+            if (a.out_bf16)
+              reinterpret_cast<uint16_t*>(a.out)[o] = f32_to_bf16_rne(l);
+            else
+              reinterpret_cast<float*>(a.out)[o] = l;
+          } else {
+            if (l > ce.mx[r]) {
+              ce.se[r] = ce.se[r] * fast_exp(ce.mx[r] - l) + 1.f;
+              ce.mx[r] = l;
+            } else {
+              ce.se[r] += fast_exp(l - ce.mx[r]);
+            }
+            if (v == ce.y[r]) a.tgt_logit[a.tok0 + tt] = l;
+          }
+        }
+      }
+      tot = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    };
+    auto body = [&](auto J) {
+      constexpr int j = decltype(J)::value;
+      load_next((j + kDecPD) % NB);
+      asm volatile("" ::: "memory");
+      if (cS == s_issue) {
+        if (kcu + kca > 0) load_exp();
+        if (ck + 1 < nu) load_scales(cu_ + W, snext);
+      }
+      // scales of this step's groups 4 cS .. 4 cS + 3 of row lr: dwords
+      // 2 (cS % 2) and 2 (cS % 2) + 1 of lane 4 lr + (cS / 2) % 4's set cS / 8
+      const u32x4_t sv = cS >= 8 ? scur[1] : scur[0];
+      const bool odd = cS & 1;
+      const int src = 4 * (4 * lr + ((cS >> 1) & 3));
+      const uint32_t s01 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(odd ? sv[2] : sv[0])));
+      const uint32_t s23 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(odd ? sv[3] : sv[1])));
+      f32x4_t acc[SG];
+#pragma unroll
+      for (int k = 0; k < SG; ++k) acc[k] = lds_load<f32x4_t>(brow + 64 * (cS * SG + k));
+#pragma unroll
+      for (int kc = 0; kc < GW; ++kc) {
+#pragma unroll
+        for (int k = 0; k < SG; ++k) {
+          const bf16x8_t A = lds_load<bf16x8_t>(xrow + 2 * (cS * SG + k) * g + 16 * kc);
+          acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+              A, unpack8(cbuf[j][k][kc], kMask, kMagic), acc[k], 0, 0, 0);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < SG; ++k) {
+        const uint32_t sw = k < 2 ? s01 : s23;
+        tot += f16_to_f32(uint16_t(k & 1 ? sw >> 16 : sw)) * acc[k];
+      }
+      if (++cS == nsg) {
+        finish_unit();
+        cS = 0;
+        cu_ += W;
+        ++ck;
+        scur[0] = snext[0];
+        scur[1] = snext[1];
+      }
+      return ++done_it == n_it;
+    };
+    while (!unroll_until<0, NB>(body)) {
+    }
+  }
+  if (!t_ready) fetch_t();
+
+  if constexpr (CE) {
+    // per token: merge the 16 rows' states of each quarter, then the waves
+    float2* red = reinterpret_cast<float2*>(dec_lds + a.off_red);   // [kDWaves][kDTok]
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float m = row16_max(ce.mx[r]);
+      float se = m == -INFINITY ? 0.f : ce.se[r] * fast_exp(ce.mx[r] - m);
+      se = row16_sum(se);
+      if (lr == 0) red[wid * kDTok + 4 * q + r] = make_float2(m, se);
+    }
+    __syncthreads();
+    if (tid < M) {
+      float m = red[tid].x, s = red[tid].y;
+      for (int w = 1; w < kDWaves; ++w) lse_merge(m, s, red[w * kDTok + tid].x, red[w * kDTok + tid].y);
+      a.part[(a.tok0 + tid) * a.n_part + (blockIdx.x - a.n_prod_blocks)] = make_float2(m, s);
+    }
+  }
+}
+
 // ------------------------------------------------------------ dispatch
 using GemvFn = void (*)(GemvArgs);
 
@@ -1475,11 +1973,13 @@ GemvFn gemv_fn(int tok, int lpr) {
 }
 
 size_t gemv_lds_bytes(const archead_desc& d, int tok) {
-  return size_t(tok) * (size_t(d.d) * 2 + size_t(d.d / 32) * 4 + size_t(d.r_c + d.r_r) * 4);
+  // x, the chunk biases, and one copy of t per wave
+  return size_t(tok) * (size_t(d.d) * 2 + size_t(d.d / 32) * 4 +
+                        size_t(kWaves) * size_t(d.r_c + d.r_r) * 4);
 }
 
 int64_t gemv_rows_per_step(const archead_desc& d) {
-  const int lpr = archead::lanes_per_row(d.d);
+  const int lpr = archead::lanes_per_row(d);
   return int64_t(lpr < kRowsPerStep ? lpr : kRowsPerStep) * (64 / lpr);
 }
 
@@ -1500,7 +2000,7 @@ int64_t gemv_grid(const archead_handle* h, int tok, bool ce) {
   const int64_t steps = (h->desc.V + gemv_rows_per_step(h->desc) - 1) / gemv_rows_per_step(h->desc);
   const int64_t max_blocks = (steps + kWaves - 1) / kWaves;
   if (cached <= 0) {
-    const int lpr = lanes_per_row(h->desc.d);
+    const int lpr = lanes_per_row(h->desc);
     GemvFn fn = ce ? gemv_fn<true>(tok, lpr) : gemv_fn<false>(tok, lpr);
     int nb = 0;
     const size_t lds = gemv_lds_bytes(h->desc, tok);
@@ -1513,10 +2013,33 @@ int64_t gemv_grid(const archead_handle* h, int tok, bool ce) {
     int want = kGemvBlocksPerCu;
     if (const char* e = getenv("ARCHEAD_GEMV_BLOCKS_PER_CU")) want = atoi(e) > 0 ? atoi(e) : want;
     if (nb > want) nb = want;
+    // every resident wave (measured faster than fewer waves with an even
+    // split of the steps)
     cached = nb * h->n_cu;
+    if (const char* e = getenv("ARCHEAD_GEMV_GRID")) cached = atoi(e) > 0 ? atoi(e) : cached;
     mh->grid_cache[slot].store(cached, std::memory_order_relaxed);
   }
   return cached < max_blocks ? cached : max_blocks;
+}
+
+// MFMA decode kernel grid: stage-1 producer workgroups (one rank row per
+// wave) first, then one consumer workgroup per remaining CU at most, with
+// the consumer wave count chosen so the 16-row units divide evenly into
+// rounds (every wave gets the same number of units, but for the last round).
+DecGrid dec_grid(const archead_handle* h) {
+  DecGrid gr;
+  const archead_desc& d = h->desc;
+  const int64_t R = d.r_c + d.r_r;
+  gr.prod_blocks = int((R + kDecWaves - 1) / kDecWaves);
+  gr.n_units = (d.V + 15) / 16;
+  int64_t cap = int64_t(h->n_cu) - gr.prod_blocks;
+  if (cap < 1) cap = 1;
+  if (const char* e = getenv("ARCHEAD_DEC_BLOCKS")) cap = atoi(e) > 0 ? atoi(e) : cap;
+  const int64_t wmax = cap * kDecWaves;
+  const int64_t rounds = (gr.n_units + wmax - 1) / wmax;
+  gr.n_waves = (gr.n_units + rounds - 1) / rounds;
+  gr.consumer_blocks = (gr.n_waves + kDecWaves - 1) / kDecWaves;
+  return gr;
 }
 
 static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
@@ -1528,10 +2051,14 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
   if (!h || M <= 0) return w;
   const archead_desc& d = h->desc;
   size_t off = 0;
-  const bool gemv = use_gemv(h, M);
-  if (gemv) {
-    w.t_off = off;
-    off = align256(off + sizeof(float) * size_t(M) * size_t(d.r_c + d.r_r));
+  const bool dec = use_dec(h, M);
+  const bool gemv = !dec && use_gemv(h, M);
+  if (dec) {
+    w.tst_off = off;
+    off = align256(off + sizeof(uint64_t) * size_t(M) * size_t(d.r_c + d.r_r));
+  } else if (gemv) {
+    w.tst_off = off;
+    off = align256(off + sizeof(uint64_t) * size_t(M) * size_t(d.r_c + d.r_r));
   } else {
     const size_t ngrp = size_t(d.d / d.g);
     const size_t nslot = ngrp + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
@@ -1555,7 +2082,9 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
     // used) so every token row of the partials has the same number of
     // slots.  MFMA: one slot per vocabulary tile.
     int64_t np = 0;
-    if (gemv) {
+    if (dec) {
+      np = dec_grid(h).consumer_blocks;
+    } else if (gemv) {
       const int64_t full = M / 4, rem = M % 4;
       if (full) np = gemv_grid(h, 4, true);
       if (rem) { const int64_t g = gemv_grid(h, int(rem), true); np = (np == 0 || g < np) ? g : np; }
@@ -1591,32 +2120,6 @@ archead_status check_call(const archead_handle* h, const void* x, int64_t M, int
   if (ws_bytes < need) return fail(ARCHEAD_E_WORKSPACE, "workspace %zu < %zu bytes", ws_bytes, need);
   if (need && !ws) return fail(ARCHEAD_E_INVALID_ARG, "workspace is NULL");
   if (!aligned(ws, 256)) return fail(ARCHEAD_E_MISALIGNED, "workspace must be 256-byte aligned");
-  return ARCHEAD_OK;
-}
-
-archead_status launch_stage1(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
-                             float* t, hipStream_t s) {
-  const archead_desc& d = h->desc;
-  const int64_t R = d.r_c + d.r_r;
-  if (R == 0) return ARCHEAD_OK;
-  Stage1Args a;
-  a.x = static_cast<const uint16_t*>(x);
-  a.ldx = ldx; a.M = M; a.d = d.d;
-  a.cv = static_cast<const int8_t*>(h->ptrs.core_v);
-  a.sv = static_cast<const uint16_t*>(h->ptrs.core_v_scale);
-  a.gv = d.r_c ? d.g_v : d.d; a.rc = d.r_c;
-  a.cb = static_cast<const int8_t*>(h->ptrs.corr_b);
-  a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
-  a.gb = d.r_r ? d.g_b : d.d; a.rr = d.r_r;
-  a.t = t;
-  for (int64_t m0 = 0; m0 < M; m0 += kMaxGridY * kS1Tok) {
-    const int64_t rest = M - m0;
-    const int64_t mblocks = (rest < kMaxGridY * kS1Tok ? rest + kS1Tok - 1 : kMaxGridY * kS1Tok) / kS1Tok;
-    a.mbase = m0;
-    hipLaunchKernelGGL(k_stage1, dim3(unsigned(R), unsigned(mblocks)), dim3(kBlock), 0, s, a);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return hip_fail(e, "stage-1 launch");
-  }
   return ARCHEAD_OK;
 }
 
@@ -1674,7 +2177,37 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "stage-1 launch");
 }
 
-GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const float* t) {
+// Call stamp of the decode kernels' stage-1 exchange: unique per call
+// within the process (the low bits count calls, the start value is drawn
+// from the clock so stamps left in reused memory by another process are
+// unlikely to match).
+uint32_t next_epoch() {
+  static std::atomic<uint32_t> counter{uint32_t(
+      std::chrono::steady_clock::now().time_since_epoch().count() * 2654435761ull)};
+  return counter.fetch_add(1, std::memory_order_relaxed) + 1u;
+}
+
+// Stage-1 operands of a call (V_c, B_w and their scales, the stamped t in
+// the workspace, a fresh epoch).
+Stage1Ops stage1_ops(const archead_handle* h, uint64_t* tst) {
+  const archead_desc& d = h->desc;
+  Stage1Ops o;
+  o.cv = static_cast<const int8_t*>(h->ptrs.core_v);
+  o.sv = static_cast<const uint16_t*>(h->ptrs.core_v_scale);
+  o.cb = static_cast<const int8_t*>(h->ptrs.corr_b);
+  o.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
+  o.gv = int(d.r_c ? d.g_v : d.d);
+  o.gb = int(d.r_r ? d.g_b : d.d);
+  o.rc = int(d.r_c);
+  o.rr = int(d.r_r);
+  o.d = int(d.d);
+  o.tst = reinterpret_cast<unsigned long long*>(tst);
+  o.epoch = next_epoch();
+  o.spin_limit = h->t_spin_limit;
+  return o;
+}
+
+GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, uint64_t* tst) {
   const archead_desc& d = h->desc;
   GemvArgs a;
   memset(&a, 0, sizeof a);
@@ -1686,11 +2219,12 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const fl
   a.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx;
-  a.t = t;
+  a.s1 = stage1_ops(h, tst);
+  a.n_prod_blocks = int((d.r_c + d.r_r + kWaves - 1) / kWaves);
   a.V = d.V; a.d = int(d.d); a.g = int(d.g); a.rc = int(d.r_c); a.rr = int(d.r_r);
   const int64_t cpg = d.g / 32;
   a.gshift = (cpg & (cpg - 1)) == 0 ? __builtin_ctzll(uint64_t(cpg)) : -1;
-  const int lpr = lanes_per_row(d.d);
+  const int lpr = lanes_per_row(d);
   const int kd = lpr >= 64 ? 1 : 2;   // ExpLanes<LPR>::KD
   a.vec_exp = d.r_c % 4 == 0 && d.r_r % 4 == 0 && (d.r_c + d.r_r) / 4 <= int64_t(kd) * lpr &&
               (d.r_c == 0 || aligned(h->ptrs.core_u, 4)) &&
@@ -1703,7 +2237,7 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const fl
   if (!d.r_r) { a.ca = reinterpret_cast<const int8_t*>(a.codes); a.sa = a.rs; }
   const int64_t wr = gemv_rows_per_step(d);
   a.nsteps = (d.V + wr - 1) / wr;
-  a.nit = int((d.d / 32) / lanes_per_row(d.d));
+  a.nit = int((d.d / 32) / lanes_per_row(d));
   return a;
 }
 
@@ -1711,7 +2245,7 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, const fl
 // (the CE passes, whose partials are indexed by workgroup).
 archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M, bool ce,
                                   int64_t forced_grid, hipStream_t s) {
-  const int lpr = lanes_per_row(h->desc.d);
+  const int lpr = lanes_per_row(h->desc);
   // timing events (if set) are attached to the first and last dispatch
   // packets themselves, so they bracket exactly the kernel execution
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
@@ -1719,7 +2253,7 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
   for (int64_t m0 = 0; m0 < M; m0 += 4) {
     const int tok = int(M - m0 < 4 ? M - m0 : 4);
     GemvFn fn = ce ? gemv_fn<true>(tok, lpr) : gemv_fn<false>(tok, lpr);
-    const int64_t grid = forced_grid > 0 ? forced_grid : gemv_grid(h, tok, ce);
+    const int64_t grid = a.n_prod_blocks + (forced_grid > 0 ? forced_grid : gemv_grid(h, tok, ce));
     a.tok0 = m0;
     const size_t lds = gemv_lds_bytes(h->desc, tok);
     if (lds > 65536) {
@@ -1733,6 +2267,67 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
                                       dim3(kBlock), args, lds, s, first ? ev0 : nullptr,
                                       last ? ev1 : nullptr, 0);
     if (e != hipSuccess) return hip_fail(e, "GEMV launch");
+  }
+  return ARCHEAD_OK;
+}
+
+using DecFn = void (*)(DecArgs);
+
+template <bool CE>
+DecFn dec_fn(int gw) {
+  switch (gw) {
+    case 1: return k_dec<1, CE>;
+    case 2: return k_dec<2, CE>;
+    default: return k_dec<4, CE>;
+  }
+}
+
+// One launch per pass of up to dec_tokens_per_pass tokens.  The CE form
+// writes one softmax partial per consumer workgroup.
+archead_status launch_dec(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
+                          uint64_t* tst, DecArgs a, bool ce, hipStream_t s) {
+  const archead_desc& d = h->desc;
+  const DecGrid gr = dec_grid(h);
+  const int tpp = dec_tokens_per_pass(d);
+  a.codes = static_cast<const uint8_t*>(h->ptrs.res_codes);
+  a.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
+  a.cu = static_cast<const int8_t*>(h->ptrs.core_u);
+  a.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
+  a.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
+  a.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
+  a.s1 = stage1_ops(h, tst);
+  a.x = static_cast<const uint16_t*>(x);
+  a.ldx = ldx;
+  a.V = d.V;
+  a.d = int(d.d); a.g = int(d.g); a.rc = int(d.r_c); a.rr = int(d.r_r);
+  a.ngrp = int(d.d / d.g);
+  a.n_units = gr.n_units;
+  a.n_waves = gr.n_waves;
+  a.n_prod_blocks = gr.prod_blocks;
+  const int gw = int(d.g / 32);
+  DecFn fn = ce ? dec_fn<true>(gw) : dec_fn<false>(gw);
+  hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
+  hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
+  const int64_t grid = gr.prod_blocks + gr.consumer_blocks;
+  for (int64_t m0 = 0; m0 < M; m0 += tpp) {
+    const int tok = int(M - m0 < tpp ? M - m0 : tpp);
+    const DecLds l = dec_lds(d, tok);
+    a.tok0 = m0;
+    a.M = tok;
+    a.kcu = l.kcu; a.kca = l.kca;
+    a.xstr = l.xstr; a.tstr = l.tstr;
+    a.off_bias = l.off_bias; a.off_t = l.off_t; a.off_red = l.off_red;
+    if (l.total > 65536) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, l.total);
+      if (e != hipSuccess) return hip_fail(e, "decode LDS size attribute");
+    }
+    void* args[] = {&a};
+    const bool first = m0 == 0, last = m0 + tpp >= M;
+    hipError_t e = hipExtLaunchKernel(reinterpret_cast<const void*>(fn), dim3(unsigned(grid)),
+                                      dim3(kDBlock), args, size_t(l.total), s,
+                                      first ? ev0 : nullptr, last ? ev1 : nullptr, 0);
+    if (e != hipSuccess) return hip_fail(e, "MFMA decode launch");
   }
   return ARCHEAD_OK;
 }
@@ -1824,6 +2419,12 @@ archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs
   h->device = dev;
   h->n_cu = prop.multiProcessorCount;
   h->gemv_max_m.store(kDefaultGemvMaxM);
+  h->dec_min_m.store(kDefaultDecMinM);
+  h->dec_max_m.store(kDefaultDecMaxM);
+  // polls of the stage-1 exchange before the fallback (ARCHEAD_T_SPIN_LIMIT
+  // overrides; 0 makes every value take the fallback, for its tests)
+  h->t_spin_limit = 1 << 16;
+  if (const char* e = getenv("ARCHEAD_T_SPIN_LIMIT")) h->t_spin_limit = atoi(e) >= 0 ? atoi(e) : h->t_spin_limit;
   for (auto& c : h->grid_cache) c.store(0);
   h->ev_start.store(nullptr);
   h->ev_stop.store(nullptr);
@@ -1852,7 +2453,16 @@ archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
     return fail(ARCHEAD_E_MISALIGNED, "out is not aligned to its element size");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const WsLayout w = ws_layout(h, M, ARCHEAD_OP_LOGITS);
-  float* t = reinterpret_cast<float*>(static_cast<char*>(ws) + w.t_off);
+  if (use_dec(h, M)) {
+    DecArgs a;
+    memset(&a, 0, sizeof a);
+    a.out = out;
+    a.ldo = ldo;
+    a.out_bf16 = out_dtype == ARCHEAD_BF16;
+    return launch_dec(h, x, M, ldx,
+                      reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off), a, false,
+                      s);
+  }
   if (!use_gemv(h, M)) {
     st = launch_mfma_prologue(h, x, M, ldx, w, static_cast<char*>(ws), s);
     if (st != ARCHEAD_OK) return st;
@@ -1862,9 +2472,7 @@ archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
     a.out_bf16 = out_dtype == ARCHEAD_BF16;
     return launch_mfma(h, a, false, s);
   }
-  st = launch_stage1(h, x, M, ldx, t, s);
-  if (st != ARCHEAD_OK) return st;
-  GemvArgs a = gemv_args(h, x, ldx, t);
+  GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off));
   a.out = out;
   a.ldo = ldo;
   a.out_bf16 = out_dtype == ARCHEAD_BF16;
@@ -1886,11 +2494,19 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t
   hipStream_t s = static_cast<hipStream_t>(stream);
   const WsLayout w = ws_layout(h, M, ARCHEAD_OP_LOGITS_CE);
   char* base = static_cast<char*>(ws);
-  float* t = reinterpret_cast<float*>(base + w.t_off);
   float2* part = reinterpret_cast<float2*>(base + w.part_off);
   float* tl = reinterpret_cast<float*>(base + w.tgt_off);
   const int64_t n_part = w.n_part;
-  if (!use_gemv(h, M)) {
+  if (use_dec(h, M)) {
+    DecArgs a;
+    memset(&a, 0, sizeof a);
+    a.tgt = targets;
+    a.tgt64 = tgt_dtype == ARCHEAD_I64;
+    a.part = part;
+    a.n_part = n_part;
+    a.tgt_logit = tl;
+    st = launch_dec(h, x, M, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off), a, true, s);
+  } else if (!use_gemv(h, M)) {
     st = launch_mfma_prologue(h, x, M, ldx, w, base, s);
     if (st != ARCHEAD_OK) return st;
     MfmaArgs a = mfma_args(h, x, M, ldx, w, base);
@@ -1900,9 +2516,7 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t
     a.tgt_logit = tl;
     st = launch_mfma(h, a, true, s);
   } else {
-    st = launch_stage1(h, x, M, ldx, t, s);
-    if (st != ARCHEAD_OK) return st;
-    GemvArgs a = gemv_args(h, x, ldx, t);
+    GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off));
     a.tgt = targets;
     a.tgt64 = tgt_dtype == ARCHEAD_I64;
     a.part = part;

@@ -21,16 +21,54 @@ archead_status fail(archead_status s, const char* fmt, ...) {
 
 void clear_error() { g_err[0] = 0; }
 
-int lanes_per_row(int64_t d) {
-  int64_t chunks = d / 32;
-  int lpr = 64;
+int lanes_per_row(const archead_desc& d) {
+  // a segment of 16 lanes per row reads 256 contiguous bytes per row and 4
+  // rows per load instruction, which streams faster than one row per
+  // instruction; wider segments only where the rank-r codes of a row would
+  // not fit as 2 dwords per lane otherwise
+  const int64_t chunks = d.d / 32;
+  int lpr = 16;
   while (lpr > 1 && chunks % lpr) lpr >>= 1;
+  const int64_t r4 = (d.r_c + d.r_r) / 4;
+  while (lpr < 64 && r4 > 2 * lpr && chunks % (2 * lpr) == 0) lpr *= 2;
   return lpr;
 }
 
 bool use_gemv(const archead_handle* h, int64_t M) {
   // the many-token kernel stages 64 codes of one scale group at a time
   return M <= h->gemv_max_m.load(std::memory_order_relaxed) || h->desc.g % 64 != 0;
+}
+
+DecLds dec_lds(const archead_desc& d, int tok) {
+  DecLds l;
+  l.kcu = int((d.r_c + 31) / 32);
+  l.kca = int((d.r_r + 31) / 32);
+  l.xstr = int(2 * d.d + 16);                   // +16 bytes: rows start on different banks
+  l.tstr = (l.kcu + l.kca) * 32 + 8;            // bf16 elements, +16 bytes likewise
+  l.off_bias = tok * l.xstr;
+  l.off_t = l.off_bias + int(d.d / d.g) * kDecTok * 4;
+  l.off_red = l.off_t + 3 * tok * l.tstr * 2;   // t as three bf16 parts
+  l.total = l.off_red + kDecWaves * kDecTok * 8;
+  return l;
+}
+
+int dec_tokens_per_pass(const archead_desc& d) {
+  // group sizes of 1, 2 or 4 code words per lane, walked 4 groups at a time;
+  // at most 64 groups per row (two scale loads per unit); factor code rows
+  // read as dwords; at most 128 dimensions per factor (4 K-chunks)
+  if (d.g != 32 && d.g != 64 && d.g != 128) return 0;
+  if ((d.d / d.g) % 4 || d.d / d.g > 64) return 0;
+  if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return 0;
+  // byte offsets of the code buffer stay 32-bit
+  if (d.V * (d.d / 2) >= (int64_t(1) << 31)) return 0;
+  for (int tok = kDecTok; tok >= 1; --tok)
+    if (dec_lds(d, tok).total <= kLdsBytes) return tok;
+  return 0;
+}
+
+bool use_dec(const archead_handle* h, int64_t M) {
+  return M >= h->dec_min_m.load(std::memory_order_relaxed) &&
+         M <= h->dec_max_m.load(std::memory_order_relaxed) && dec_tokens_per_pass(h->desc) > 0;
 }
 
 }  // namespace archead
@@ -153,6 +191,21 @@ archead_status archead_set_timing_events(archead_handle* h, void* start, void* s
     return fail(ARCHEAD_E_INVALID_ARG, "start and stop must both be set or both be NULL");
   h->ev_start.store(start);
   h->ev_stop.store(stop);
+  return ARCHEAD_OK;
+}
+
+archead_status archead_set_dec_range(archead_handle* h, int64_t min_m, int64_t max_m) {
+  if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
+  if (min_m < -1 || max_m < -1) return fail(ARCHEAD_E_INVALID_ARG, "dec range bounds must be >= -1");
+  h->dec_min_m.store(min_m == -1 ? kDefaultDecMinM : min_m);
+  h->dec_max_m.store(max_m == -1 ? kDefaultDecMaxM : max_m);
+  return ARCHEAD_OK;
+}
+
+archead_status archead_get_dec_range(const archead_handle* h, int64_t* min_m, int64_t* max_m) {
+  if (!h || !min_m || !max_m) return fail(ARCHEAD_E_INVALID_ARG, "NULL argument");
+  *min_m = h->dec_min_m.load();
+  *max_m = h->dec_max_m.load();
   return ARCHEAD_OK;
 }
 

@@ -14,6 +14,9 @@ struct archead_handle {
   int device;             // HIP device the buffers live on
   int n_cu;               // compute units of that device
   std::atomic<int64_t> gemv_max_m;
+  std::atomic<int64_t> dec_min_m;   // M range of the MFMA decode kernel
+  std::atomic<int64_t> dec_max_m;   // (empty when max < min)
+  int t_spin_limit;       // polls of the in-launch stage-1 exchange before the fallback
   // persistent-grid sizes found with the occupancy API, keyed by kernel
   // variant; 0 = not computed yet
   std::atomic<int> grid_cache[64];
@@ -25,17 +28,22 @@ struct archead_handle {
 namespace archead {
 
 constexpr int64_t kDefaultGemvMaxM = 15;  // largest M on the decode kernel (measured crossover)
+constexpr int64_t kDefaultDecMinM = 2;    // M range of the MFMA decode kernel (a single
+constexpr int64_t kDefaultDecMaxM = 32;   // token streams faster through the GEMV)
 constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
+constexpr int kDecTok = 16;               // tokens per pass of the MFMA decode kernel
+constexpr int kDecWaves = 8;              // waves per workgroup of the MFMA decode kernel
+constexpr int64_t kLdsBytes = 160 * 1024; // LDS per workgroup on gfx950
 
 archead_status fail(archead_status s, const char* fmt, ...);
 void clear_error();
 
 // chunk = 32 consecutive INT4 codes = 16 bytes; lanes per row of the GEMV
-int lanes_per_row(int64_t d);
+int lanes_per_row(const archead_desc& d);
 
 // Workspace carve-up (byte offsets, each 256-aligned).
 struct WsLayout {
-  size_t t_off = 0;      // fp32 [M, r_c + r_r] (decode path)
+  size_t tst_off = 0;    // u64 [M, r_c + r_r] stamped t (both decode kernels)
   // many-token (MFMA) path only:
   size_t ts_off = 0;     // bf16 [M][blocks][4][16] t split into hi, mid, lo (and 0)
   size_t gb_off = 0;     // fp32 [n_mt][slots][256] slot biases
@@ -51,7 +59,26 @@ struct WsLayout {
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op);
 bool use_gemv(const archead_handle* h, int64_t M);
 
+// MFMA decode kernel: its LDS layout for a pass of `tok` tokens, the most
+// tokens per pass the LDS holds (0: the head shape is not supported), and
+// whether a call with M tokens runs on it.
+struct DecLds {
+  int xstr = 0, tstr = 0, off_bias = 0, off_t = 0, off_red = 0, total = 0;
+  int kcu = 0, kca = 0;   // expansion K-chunks of 32 rank dimensions (U_c, A_w)
+};
+DecLds dec_lds(const archead_desc& d, int tok);
+int dec_tokens_per_pass(const archead_desc& d);
+bool use_dec(const archead_handle* h, int64_t M);
+
 // grid of the GEMV kernel: persistent workgroups, at most one per 8 rows
 int64_t gemv_grid(const archead_handle* h, int tok, bool ce);
+
+struct DecGrid {
+  int prod_blocks = 0;          // stage-1 producer workgroups (first in the grid)
+  int64_t consumer_blocks = 0;  // workgroups streaming the head
+  int64_t n_waves = 0;          // consumer waves with work
+  int64_t n_units = 0;          // units of 16 vocabulary rows
+};
+DecGrid dec_grid(const archead_handle* h);
 
 }  // namespace archead

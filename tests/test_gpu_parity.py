@@ -311,37 +311,121 @@ def test_error_paths_on_device():
 
 # ------------------------------------------------------------- forced paths
 
-@pytest.mark.parametrize("cfg,M", [("tiny", 8), ("qwen_decode", 16), ("gemma", 8)])
-def test_gemv_and_mfma_paths_both_match_oracle(cfg, M):
-    """The same tokens through the decode GEMV (forced for any M) and the
-    MFMA kernel (forced for any M): both within tolerance of the oracle."""
-    Mmax = max(CONFIGS[cfg]["Ms"])
+@pytest.mark.parametrize("cfg,M", [("tiny", 8), ("qwen_decode", 16), ("gemma", 8),
+                                   ("qwen_decode", 20)])
+def test_all_paths_match_oracle(cfg, M):
+    """The same tokens through the MFMA decode kernel, the decode GEMV and
+    the tiled MFMA kernel (each forced for any M): all within tolerance of
+    the oracle, logits and CE."""
+    Mmax = max(max(CONFIGS[cfg]["Ms"]), M)
     ref = cached_oracle_logits(cfg, Mmax)[:M]
     ph = packed(cfg)
     x = make_x(cfg, Mmax)[:M]
     y = make_targets(cfg, M)
     ref_ce = ohead.cross_entropy(ref, y)
     try:
-        for name, thr in (("gemv", 10 ** 9), ("mfma", 0)):
-            ph.set_gemv_max_m(thr)
+        for name in ("dec", "gemv", "tiled"):
+            ph.force_path(name)
             say(f"{cfg} M={M} forced {name}")
             assert_logits_close(gpu_logits(ph, x), ref, what=f"{cfg} M={M} {name}")
             ce, mean = gpu_ce(ph, x, y)
             assert_ce_close(ce, ref_ce, what=f"{cfg} M={M} {name} CE")
     finally:
-        ph.set_gemv_max_m(-1)
+        ph.force_path("auto")
 
 
-def test_identity_probe_gemv_forced_bit_exact():
+@pytest.mark.parametrize("path", ["gemv", "dec"])
+def test_identity_probe_decode_kernels_bit_exact(path):
+    """One-hot x, no low-rank parts: every logit is s_res * c, exact in fp32,
+    and both decode kernels reach it exactly (the MFMA decode kernel's chain
+    -136 + (136 + c) is exact too)."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("tiny", rc=0, rr=0)
     ph = PackedHead.from_arrays(h)
-    ph.set_gemv_max_m(10 ** 9)
+    ph.force_path(path)
     eye = np.zeros((h.d, h.d), dtype=np.uint16)
     eye[np.arange(h.d), np.arange(h.d)] = 0x3F80
-    lg = gpu_logits(ph, eye[:96])
-    ref = ohead.logits(h, eye[:96])
-    assert np.array_equal(lg.astype(np.float64), ref)
+    rows = eye[:96] if path == "gemv" else eye
+    say(f"identity probe tiny, {path}: M={rows.shape[0]}")
+    lg = gpu_logits(ph, rows).astype(np.float64)
+    ref = ohead.logits(h, rows)
+    bad = np.argwhere(lg != ref)
+    assert bad.size == 0, (f"{len(bad)} logits differ, first at {bad[:3].tolist()}: "
+                           f"gpu {lg[tuple(bad[0])]!r} oracle {ref[tuple(bad[0])]!r}")
+    ph.close()
+
+
+def test_identity_probe_dec_qwen_sampled_bit_exact():
+    """The same one-hot probe on the Qwen-shaped head through the MFMA decode
+    kernel (several passes of 16 tokens), bit for bit."""
+    h = make_head("qwen_decode", rc=0, rr=0)
+    from paper_2608_02703_amd import PackedHead
+    ph = PackedHead.from_arrays(h)
+    ph.force_path("dec")
+    rng = np.random.default_rng(6)
+    cols = np.unique(np.concatenate([[0, 1, 7, 8, 31, 32, 127, 128, 2047, 4095],
+                                     rng.integers(0, h.d, 22)]))
+    x = np.zeros((cols.size, h.d), dtype=np.uint16)
+    x[np.arange(cols.size), cols] = 0x3F80
+    say(f"identity probe qwen, dec: M={cols.size}")
+    lg = gpu_logits(ph, x)
+    assert np.array_equal(lg.astype(np.float64), ohead.logits(h, x))
+    ph.close()
+
+
+@pytest.mark.parametrize("path", ["dec", "gemv"])
+def test_stage1_fallback_matches(path):
+    """With the in-launch stage-1 exchange's wait bound set to zero polls,
+    every consumer wave computes its t values itself; the logits and CE
+    still match the oracle within tolerance (both decode kernels)."""
+    import os
+    from paper_2608_02703_amd import PackedHead
+    h = cached_head("tiny")
+    x = make_x("tiny", 8)
+    y = make_targets("tiny", 8)
+    ref = cached_oracle_logits("tiny", 8)
+    os.environ["ARCHEAD_T_SPIN_LIMIT"] = "0"
+    try:
+        ph = PackedHead.from_arrays(h)
+    finally:
+        del os.environ["ARCHEAD_T_SPIN_LIMIT"]
+    ph.force_path(path)
+    say(f"{path} stage-1 fallback: tiny M=8")
+    lg = gpu_logits(ph, x)
+    assert_logits_close(lg, ref, what="fallback logits")
+    ce, _ = gpu_ce(ph, x, y)
+    assert_ce_close(ce, ohead.cross_entropy(ref, y), what="fallback CE")
+    ph.close()
+
+
+@pytest.mark.parametrize("V,d,g,M,rc,rr", [(1000, 512, 64, 17, 16, 8), (777, 256, 32, 5, 20, 4),
+                                           (33, 128, 32, 1, 16, 8), (8191, 512, 128, 16, 64, 0),
+                                           (4099, 1024, 128, 3, 0, 36), (130, 256, 64, 40, 12, 28),
+                                           (777, 96, 32, 5, 20, 4), (50, 1536, 128, 2, 6, 8)])
+def test_dec_ragged(V, d, g, M, rc, rr):
+    """The MFMA decode kernel on partial 16-row units, several passes,
+    padded rank dimensions, wide row strides, bf16 output and CE.  The last
+    two shapes are outside its limits (d/g not a multiple of 4, a rank not a
+    multiple of 4): forcing it there must still give correct results through
+    another kernel."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", V=V, d=d, g=g, rc=rc, rr=rr)
+    x = make_x("tiny", M, d=d, basis="identity")
+    ph = PackedHead.from_arrays(h)
+    ph.force_path("dec")
+    ref = ohead.logits(h, x)
+    say(f"dec ragged V={V} d={d} g={g} M={M} rc={rc} rr={rr}")
+    assert_logits_close(gpu_logits(ph, x, ld=d + 8), ref, what="dec ragged")
+    out = torch.full((M, V + 3), 5.0, device="cuda")
+    ph.logits(torch_x(x), out=out[:, :V])
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert (o[:, V:] == 5.0).all(), "wrote past the row"
+    y = (np.arange(M) * 11 % V).astype(np.int32)
+    ce, _ = gpu_ce(ph, x, y)
+    assert_ce_close(ce, ohead.cross_entropy(ref, y), what="dec ragged CE")
+    bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
+    assert_bf16_output(bits, o[:, :V], ref, "dec ragged bf16")
     ph.close()
 
 
@@ -353,7 +437,7 @@ def test_group_size_not_multiple_of_64_uses_decode_kernel():
         h = make_head("tiny", V=V, d=d, g=g, rc=20, rr=4)
         x = make_x("tiny", M, d=d, basis="identity")
         ph = PackedHead.from_arrays(h)
-        ph.set_gemv_max_m(0)
+        ph.force_path("tiled")
         say(f"g={g} fallback V={V} d={d} M={M}")
         assert_logits_close(gpu_logits(ph, x), ohead.logits(h, x), what=f"g={g}")
         ph.close()
@@ -376,7 +460,7 @@ def test_zero_scales_many_token_kernel():
     su[7] = sa[7] = 0
     h = dataclasses.replace(h, res_scales=rs, core_u_scale=su, corr_a_scale=sa)
     ph = PackedHead.from_arrays(h)
-    ph.set_gemv_max_m(0)
+    ph.force_path("tiled")
     x = make_x("tiny", 300)
     say("zero scales: tiny head, M=300 (many-token kernel)")
     lg = gpu_logits(ph, x)
@@ -396,7 +480,7 @@ def test_mfma_ragged_tiles(V, d, g, M):
     h = make_head("tiny", V=V, d=d, g=g, rc=40, rr=12)
     x = make_x("tiny", M, d=d, basis="identity")
     ph = PackedHead.from_arrays(h)
-    ph.set_gemv_max_m(0)
+    ph.force_path("tiled")
     ref = ohead.logits(h, x)
     say(f"mfma ragged V={V} d={d} g={g} M={M}")
     assert_logits_close(gpu_logits(ph, x, ld=d + 16), ref, what="mfma ragged")
