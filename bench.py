@@ -37,6 +37,7 @@ PEAK_BF16_TFLOPS = 2500.0
 N_COPIES = 3
 CALIBRATION_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_qwen_decode_traffic.md")
+SWEEP_PEAK_NOTE = "bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s"
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_02703_amd", "csrc", "archead.hip")
 
 
@@ -56,13 +57,24 @@ def upload_copies(h, n):
     return heads
 
 
-def gemv_algorithmic_bytes(h, M):
-    """Bytes the head-streaming kernel must move once: residual codes and
-    scales, the vocabulary-side factors and their scales, x, t and the fp32
-    logits it writes."""
-    return (h.V * h.d // 2 + h.V * (h.d // h.g) * 2 + h.V * (h.rc + h.rr) +
-            (2 * h.V if h.rc else 0) + (2 * h.V if h.rr else 0) +
-            M * h.d * 2 + M * (h.rc + h.rr) * 4 + M * h.V * 4)
+def decode_algorithmic_bytes(h, M):
+    """Bytes one decode launch must move: the whole packed head once (the
+    residual codes and scales, the factors and their scales, V_c and B_w for
+    the in-launch stage 1), x, and the fp32 logits it writes."""
+    from oracle.bytes import head_bytes
+    return head_bytes(h) + M * h.d * 2 + M * h.V * 4
+
+
+def lanes_per_row(h):
+    """Lanes per vocabulary row of the decode GEMV (the library's rule)."""
+    chunks = h.d // 32
+    lpr = 16
+    while lpr > 1 and chunks % lpr:
+        lpr //= 2
+    r4 = (h.rc + h.rr) // 4
+    while lpr < 64 and r4 > 2 * lpr and chunks % (2 * lpr) == 0:
+        lpr *= 2
+    return lpr
 
 
 def mfma_algorithmic_flops(h, M):
@@ -196,6 +208,39 @@ def profile_run(kind, steps):
     print(f"profile run {kind}: done", flush=True)
 
 
+def sweep(steps):
+    """The 128k-vocabulary head (V=128256, d=8192, r_c=128, r_r=64) at every
+    M of its workload through each kernel: step time, GB/s over the packed
+    bytes and MFMA utilisation (algorithmic flops over the bf16 peak).  One
+    JSON line per (M, kernel); "auto" is the library's own choice."""
+    import torch
+    from oracle.bytes import head_bytes
+    from synth import CONFIGS, make_head, make_x
+    cfg = "sweep128k"
+    h = make_head(cfg)
+    pbytes = head_bytes(h)
+    heads = upload_copies(h, 2)       # 2 x 568 MB > the 256 MB Infinity Cache
+    Ms = CONFIGS[cfg]["Ms"]
+    xb = make_x(cfg, max(Ms))
+    x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+    for M in Ms:
+        for path in ("auto", "dec", "gemv", "tiled"):
+            if path == "gemv" and M > 64:
+                continue          # 4 tokens per pass: far off the crossover
+            for hd in heads:
+                hd.force_path(path)
+            n = steps if M <= 64 else max(3, steps // 8)
+            ms, kern, _ = time_decode(heads, x_all[:M], n, 3)
+            flops = mfma_algorithmic_flops(h, M)
+            print(json.dumps({"sweep": cfg, "M": M, "kernel": path,
+                              "us_per_step": round(ms * 1e3, 2),
+                              "gbs_packed": round(pbytes / ms / 1e6, 1),
+                              "mfma_util": round(flops / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                              "tok_s": round(M / ms * 1e3, 1)}), flush=True)
+    for hd in heads:
+        hd.force_path("auto")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -205,6 +250,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--profile", choices=["decode", "prefill"])
+    ap.add_argument("--sweep", action="store_true",
+                    help="M sweep of the 128k-vocabulary head through each kernel")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; multi-GPU (vocab-parallel) "
@@ -219,6 +266,9 @@ def main():
     torch.cuda.set_device(0)
     if args.profile:
         profile_run(args.profile, args.steps if args.profile == "decode" else args.prefill_steps)
+        return
+    if args.sweep:
+        sweep(min(args.steps, 40))
         return
     cfg = "qwen_decode"
     log("generating the packed head ...")
@@ -260,7 +310,8 @@ def main():
 
     ms1, kern1, _ = res[1]
     value = pbytes / ms1 / 1e6          # GB/s
-    alg = gemv_algorithmic_bytes(h, 1)
+    alg = decode_algorithmic_bytes(h, 1)
+    kname = f"k_gemv<1,{lanes_per_row(h)},false>"
     achieved = alg / kern1 / 1e6
     out = {
         "metric": METRIC,
@@ -282,7 +333,7 @@ def main():
         "pct_peak_hbm": round(100 * value / PEAK_HBM_GBS, 2),
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
-                     "traffic": measured_traffic(), "kernel": "k_gemv<1,64,false>",
+                     "traffic": measured_traffic(), "kernel": kname,
                      "kernel_us": round(kern1 * 1e3, 2), "algorithmic_bytes": alg},
         "decode": {str(M): {"us_per_step": round(v[0] * 1e3, 2),
                             "kernel_us": round(v[1] * 1e3, 2),

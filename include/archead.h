@@ -173,7 +173,7 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *   stream   hipStream_t to launch on (NULL = the default stream)
  * M == 0 returns ARCHEAD_OK without launching.  Three kernels serve the
  * call, chosen by M and the head shape:
- *   - M in the range of archead_set_dec_range (default 2 .. 32) with g in
+ *   - M in the range of archead_set_dec_range (default 3 .. 32) with g in
  *     {32, 64, 128}, (d/g) % 4 == 0, d/g <= 64, r_c and r_r multiples of 4
  *     and at most 128 each, and V * d / 2 < 2^31: the MFMA decode kernel,
  *     which streams the head once per pass of up to 16 tokens (fewer when
@@ -222,7 +222,7 @@ int64_t archead_get_gemv_max_m(const archead_handle* h);
 
 /* Range of M served by the MFMA decode kernel, min_m <= M <= max_m (an
  * empty range, e.g. max_m = 0, never uses it; -1 restores the built-in
- * bound, 2 and 32).  Same threading rule as archead_set_gemv_max_m.  get
+ * bound, 3 and 32).  Same threading rule as archead_set_gemv_max_m.  get
  * returns ARCHEAD_E_INVALID_ARG for a NULL argument. */
 archead_status archead_set_dec_range(archead_handle* h, int64_t min_m, int64_t max_m);
 archead_status archead_get_dec_range(const archead_handle* h, int64_t* min_m, int64_t* max_m);

@@ -268,7 +268,8 @@ struct GemvArgs {
   int64_t V;
   int d, g, rc, rr;
   int gshift;      // log2(g / 32) when g is a power of two, else -1
-  int vec_exp;     // expansion codes loaded as one dword per lane (see ExpOps)
+  int fast;        // the pipelined path applies: expansion codes as dwords (see
+                   // ExpOps), d/g even and at most 2 LPR groups per row
   int64_t cu_stride, ca_stride, su_stride, sa_stride;  // 0 for an absent factor
   int nit;         // iterations along d: (d / 32) / LPR
   int64_t nsteps;  // ceil(V / rows per wave step)
@@ -622,7 +623,7 @@ void k_gemv(GemvArgs a) {
   // buffers, so a wave keeps about kPD iterations of codes in flight while it
   // computes; codes and scales are read through buffer resources whose base
   // and per-row offsets live in scalar registers.
-  const int64_t full_steps = a.vec_exp ? a.V / WR : 0;
+  const int64_t full_steps = a.fast ? a.V / WR : 0;
   {
     constexpr int kPD = ARCHEAD_GEMV_PREFETCH;
     constexpr int NB = kPD + 1;
@@ -645,8 +646,6 @@ void k_gemv(GemvArgs a) {
       const __amdgpu_buffer_rsrc_t rs_ = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<uint16_t*>(a.rs + uint64_t(stp) * WR * ngrp), 0,
           int(sbytes < 0xffffffffull ? sbytes : 0xffffffffull), kBufferWord3);
-      const uint32_t c = uint32_t(itx * LPR + sl);
-      const uint32_t grp = a.gshift >= 0 ? (c >> a.gshift) : (c * 32u) / uint32_t(a.g);
       const int itoff = itx * LPR * 16;
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
@@ -654,10 +653,15 @@ void k_gemv(GemvArgs a) {
             rc_, int(voff), int(uint32_t(rb * SEG) * rowbytes) + itoff, kLoadStream);
         q[rb] = make_uint4(v.x, v.y, v.z, v.w);
       }
+      // a step's group scales come with its first iteration: lane sl of a
+      // segment takes groups 2 sl, 2 sl + 1 of each of its rows (4 bytes);
+      // the lanes that need them fetch them with ds_bpermute
+      if (itx == 0) {
 #pragma unroll
-      for (int rb = 0; rb < RB; ++rb)
-        sc[rb] = __builtin_amdgcn_raw_buffer_load_b16(
-            rs_, int((svoff + grp) * 2u), int(uint32_t(rb * SEG) * ngrp * 2u), 0);
+        for (int rb = 0; rb < RB; ++rb)
+          sc[rb] = __builtin_amdgcn_raw_buffer_load_b32(
+              rs_, int(svoff * 2u + uint32_t(sl) * 4u), int(uint32_t(rb * SEG) * ngrp * 2u), 0);
+      }
     };
     // expansion operands of step stp (one buffer: the next step's operands
     // are requested right after the current step's have been applied)
@@ -682,6 +686,7 @@ void k_gemv(GemvArgs a) {
     };
     uint4 q[NB][RB];
     uint32_t sc[NB][RB];
+    uint32_t ssc[RB];   // the current step's scales (groups 2 sl, 2 sl + 1 of each row)
     ExpOps<RB, KD> e;
     const int64_t last_step = gw + ((full_steps - 1 - gw) / W) * W;
     auto advance = [&](int64_t& st, int& itv) {
@@ -715,7 +720,20 @@ void k_gemv(GemvArgs a) {
       int nit = cit;
       advance(nstep, nit);
       const bool more = nstep < full_steps;
-      gemv_chunk<TOK, RB>(acc, q[j], sc[j], sx, sxb, d, C, cit * LPR + sl, kMask, kMagic);
+      if (cit == 0) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) ssc[rb] = sc[j][rb];
+      }
+      // group of this lane's chunk and the segment lane holding its scale
+      const uint32_t c = uint32_t(cit * LPR + sl);
+      const uint32_t grp = a.gshift >= 0 ? (c >> a.gshift) : (c * 32u) / uint32_t(a.g);
+      const int src = 4 * (seg * LPR + int(grp >> 1));
+      const uint32_t hsh = (grp & 1u) * 16u;
+      uint32_t scv[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        scv[rb] = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(ssc[rb]))) >> hsh;
+      gemv_chunk<TOK, RB>(acc, q[j], scv, sx, sxb, d, C, int(c), kMask, kMagic);
       if (cit == a.nit - 1) {
         // the step's rank-r expansion, then the next step's operands
         if (!t_ready) fetch_t();
@@ -2226,9 +2244,10 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, uint64_t
   a.gshift = (cpg & (cpg - 1)) == 0 ? __builtin_ctzll(uint64_t(cpg)) : -1;
   const int lpr = lanes_per_row(d);
   const int kd = lpr >= 64 ? 1 : 2;   // ExpLanes<LPR>::KD
-  a.vec_exp = d.r_c % 4 == 0 && d.r_r % 4 == 0 && (d.r_c + d.r_r) / 4 <= int64_t(kd) * lpr &&
-              (d.r_c == 0 || aligned(h->ptrs.core_u, 4)) &&
-              (d.r_r == 0 || aligned(h->ptrs.corr_a, 4));
+  const int64_t ngrp = d.d / d.g;
+  a.fast = d.r_c % 4 == 0 && d.r_r % 4 == 0 && (d.r_c + d.r_r) / 4 <= int64_t(kd) * lpr &&
+           (d.r_c == 0 || aligned(h->ptrs.core_u, 4)) &&
+           (d.r_r == 0 || aligned(h->ptrs.corr_a, 4)) && ngrp % 2 == 0 && ngrp <= 2 * lpr;
   // an absent factor reads the (valid, 16-byte aligned) residual buffers with
   // stride 0 instead; its contribution is masked to zero in the kernel
   a.cu_stride = d.r_c; a.su_stride = d.r_c ? 1 : 0;
