@@ -11,6 +11,11 @@ HBM.  The headline value is decode GB/s over the packed bytes.  Secondary
 lines: decode M=4 and M=16, and the M=4096 prefill fused-CE pass (tok/s and
 the many-token kernel's MFMA throughput).
 
+Before any timing, about 0.5 s of untimed decode steps bring the GPU's clocks
+to their sustained-load state (--clock-warmup; a cold GPU runs the first
+~100 ms of steps ~10% slower); then each line does its own --warmup steps
+and times exactly --steps steps.
+
 Prints one JSON line (rank 0, N=1).  --gpus N > 1 is refused: this build
 runs on one GPU.  --profile decode|prefill runs the same work without timing
 or JSON, for rocprofv3 (the decode form first copies 256 MiB once, the
@@ -136,6 +141,26 @@ def _kernel_times(heads, fn, steps):
     return [a.elapsed_time(b) for a, b in ev]
 
 
+def clock_warmup(heads, x, seconds):
+    """Untimed decode steps for about `seconds` of wall time before any
+    measurement.  The GPU's clocks ramp up over the first ~10-100 ms of
+    sustained load (a step measured right after a cold start is ~10% slower
+    than in steady state); a serving loop runs in the steady state."""
+    import torch
+    M = x.shape[0]
+    outs = [torch.empty((M, heads[0].V), device="cuda") for _ in heads]
+    wss = [hd.workspace(M, 0, x.device) for hd in heads]
+    t0 = time.perf_counter()
+    n = 0
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(100):
+            k = n % len(heads)
+            heads[k].logits(x, out=outs[k], ws=wss[k])
+            n += 1
+        torch.cuda.synchronize()
+    return n
+
+
 def time_decode(heads, x, steps, warmup, ws=None):
     """(ms per step, mean head-kernel ms, median head-kernel ms)."""
     import torch
@@ -197,6 +222,7 @@ def profile_run(kind, steps):
         torch.cuda.synchronize()
         del src, dst
         x = torch.from_numpy(make_x("qwen_decode", 1).view(np.int16)).view(torch.bfloat16).cuda()
+        clock_warmup(heads, x, 0.3)
         time_decode(heads, x, steps, 5)
     else:
         Mp = CONFIGS["qwen_prefill"]["Ms"][0]
@@ -223,6 +249,7 @@ def sweep(steps):
     Ms = CONFIGS[cfg]["Ms"]
     xb = make_x(cfg, max(Ms))
     x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
+    clock_warmup(heads, x_all[:1], 0.5)
     for M in Ms:
         for path in ("auto", "dec", "gemv", "tiled"):
             if path == "gemv" and M > 64:
@@ -246,6 +273,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--clock-warmup", type=float, default=0.5,
+                    help="seconds of untimed decode steps before any timing (GPU clock ramp)")
     ap.add_argument("--prefill-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
@@ -278,6 +307,8 @@ def main():
     xb = make_x(cfg, 16)
     x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
 
+    n_clock = clock_warmup(heads, x_all[:1], args.clock_warmup)
+    log(f"clock warm-up: {n_clock} untimed decode steps in {args.clock_warmup} s")
     res = {}
     for M in (1, 4, 16):
         x = x_all[:M]
@@ -331,6 +362,7 @@ def main():
                    "packed_bytes": pbytes, "head_copies_rotated": N_COPIES,
                    "parallelism": "none (1 GPU)"},
         "pct_peak_hbm": round(100 * value / PEAK_HBM_GBS, 2),
+        "clock_warmup_s": args.clock_warmup,
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": measured_traffic(), "kernel": kname,
