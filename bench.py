@@ -194,6 +194,10 @@ def time_prefill(heads, x, y, steps, warmup):
     return ms, float(res["ce"][1].cpu()[0]), float(np.mean(kern))
 
 
+def ms1_for_dense(res):
+    return res[1][0]
+
+
 def cpu_baseline(h, xb):
     """The fp64 oracle on the host cores: full head, one token (M=1)."""
     from oracle import head as ohead
@@ -278,6 +282,8 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-dense", action="store_true",
+                    help="skip the dense bf16 head context line")
     ap.add_argument("--profile", choices=["decode", "prefill"])
     ap.add_argument("--sweep", action="store_true",
                     help="M sweep of the 128k-vocabulary head through each kernel")
@@ -317,6 +323,28 @@ def main():
         res[M] = (ms, kern_ms, kern_med)
         log(f"decode M={M}: {ms * 1e3:.1f} us/step, head kernel {kern_ms * 1e3:.1f} us "
             f"(median {kern_med * 1e3:.1f}), {pbytes / ms / 1e6:.0f} GB/s over packed bytes")
+
+    # context: the same decode step through a dense bf16 head of the same
+    # shape (torch linear, random weights), the bytes the packed head avoids
+    dense = None
+    if not args.no_dense:
+        import torch.nn.functional as F
+        w = [torch.randn((h.V, h.d), device="cuda", dtype=torch.bfloat16) for _ in range(2)]
+        x1 = x_all[:1]
+
+        def dstep(i):
+            F.linear(x1, w[i % 2])
+        for i in range(50):
+            dstep(i)
+        dms = _timed_loop(dstep, args.steps)
+        dbytes = h.V * h.d * 2
+        dense = {"us_per_step": round(dms * 1e3, 2), "gbs": round(dbytes / dms / 1e6, 1),
+                 "bytes": dbytes, "op": "torch.nn.functional.linear, bf16 [V, d] weight, M=1",
+                 "packed_speedup": round(dms / ms1_for_dense(res), 2)}
+        log(f"dense bf16 head M=1: {dms * 1e3:.1f} us/step ({dbytes / dms / 1e6:.0f} GB/s over "
+            f"{dbytes / 1e9:.2f} GB)")
+        del w
+        torch.cuda.empty_cache()
 
     prefill = None
     if not args.no_prefill:
@@ -372,6 +400,7 @@ def main():
                             "gbs_packed": round(pbytes / v[0] / 1e6, 1)}
                    for M, v in res.items()},
         "prefill": prefill,
+        "dense_bf16_head": dense,
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (1 token, full head) ...")
