@@ -238,24 +238,24 @@ def profile_run(kind, steps):
     print(f"profile run {kind}: done", flush=True)
 
 
-def sweep(steps):
-    """The 128k-vocabulary head (V=128256, d=8192, r_c=128, r_r=64) at every
-    M of its workload through each kernel: step time, GB/s over the packed
-    bytes and MFMA utilisation (algorithmic flops over the bf16 peak).  One
-    JSON line per (M, kernel); "auto" is the library's own choice."""
+def sweep(steps, cfg="sweep128k", Ms=None, paths=("auto", "dec", "mid", "gemv", "tiled")):
+    """A head (default the 128k-vocabulary one: V=128256, d=8192, r_c=128,
+    r_r=64) at every M of a list (default its workload's) through each
+    kernel: step time, GB/s over the packed bytes and MFMA utilisation
+    (algorithmic flops over the bf16 peak).  One JSON line per (M, kernel);
+    "auto" is the library's own choice."""
     import torch
     from oracle.bytes import head_bytes
     from synth import CONFIGS, make_head, make_x
-    cfg = "sweep128k"
     h = make_head(cfg)
     pbytes = head_bytes(h)
-    heads = upload_copies(h, 2)       # 2 x 568 MB > the 256 MB Infinity Cache
-    Ms = CONFIGS[cfg]["Ms"]
+    heads = upload_copies(h, 2 if pbytes > 400e6 else 3)   # copies exceed the 256 MB Infinity Cache
+    Ms = Ms or CONFIGS[cfg]["Ms"]
     xb = make_x(cfg, max(Ms))
     x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
     clock_warmup(heads, x_all[:1], 0.5)
     for M in Ms:
-        for path in ("auto", "dec", "gemv", "tiled"):
+        for path in paths:
             if path == "gemv" and M > 64:
                 continue          # 4 tokens per pass: far off the crossover
             for hd in heads:
@@ -286,7 +286,12 @@ def main():
                     help="skip the dense bf16 head context line")
     ap.add_argument("--profile", choices=["decode", "prefill"])
     ap.add_argument("--sweep", action="store_true",
-                    help="M sweep of the 128k-vocabulary head through each kernel")
+                    help="M sweep of a head (default the 128k-vocabulary one) through each kernel")
+    ap.add_argument("--sweep-cfg", default="sweep128k",
+                    help="head of the sweep: sweep128k, qwen_decode or gemma")
+    ap.add_argument("--sweep-ms", default="",
+                    help="comma-separated M values of the sweep (default: the head's workload)")
+    ap.add_argument("--sweep-paths", default="auto,dec,mid,gemv,tiled")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: this build runs on one GPU only; multi-GPU (vocab-parallel) "
@@ -303,7 +308,9 @@ def main():
         profile_run(args.profile, args.steps if args.profile == "decode" else args.prefill_steps)
         return
     if args.sweep:
-        sweep(min(args.steps, 40))
+        sweep(min(args.steps, 40), args.sweep_cfg,
+              [int(v) for v in args.sweep_ms.split(",") if v] or None,
+              tuple(args.sweep_paths.split(",")))
         return
     cfg = "qwen_decode"
     log("generating the packed head ...")

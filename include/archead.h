@@ -153,7 +153,7 @@ void archead_destroy(archead_handle* h);
 
 /* Bytes of workspace the call `op` needs for M tokens (0 for M == 0).  The
  * workspace holds the low-rank projections t (fp32 [M, r_c + r_r]; on the
- * MFMA decode path with a 32-bit call stamp beside each value; on the tiled
+ * decode and several-token paths with a 32-bit call stamp beside each value; on the tiled
  * MFMA path split into three bf16 parts), on the tiled path also per-call
  * tables derived from the head (group-scale ratios, the per-group sums of x,
  * the factor codes as bf16 and the U_c / A_w codes side by side: about
@@ -173,14 +173,21 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *   stream   hipStream_t to launch on (NULL = the default stream)
  * M == 0 returns ARCHEAD_OK without launching.  Three kernels serve the
  * call, chosen by M and the head shape:
- *   - M in the range of archead_set_dec_range (default 3 .. 32) with g in
+ *   - M in the range of archead_set_dec_range (default 3 .. 32, or 3 ..
+ *     the tokens it holds per pass where the several-token kernel applies:
+ *     16 at d = 4096, 8 at d = 8192) with g in
  *     {32, 64, 128}, (d/g) % 4 == 0, d/g <= 64, r_c and r_r multiples of 4
  *     and at most 128 each, and V * d / 2 < 2^31: the MFMA decode kernel,
  *     which streams the head once per pass of up to 16 tokens (fewer when
  *     16 rows of x do not fit in LDS);
+ *   - otherwise M in the range of archead_set_mid_range (default: from one
+ *     past the decode kernel's range to 96) with g in {64, 128},
+ *     d % 512 == 0, d/g <= 64, r_c and r_r multiples of 4 and at most 128
+ *     each: the several-token kernel, which streams the head once per tile
+ *     of up to 32 tokens (x held in LDS in windows of 256 elements of d);
  *   - otherwise M <= archead_get_gemv_max_m (default 15), or g % 64 != 0:
  *     the decode GEMV (VALU dot products), one pass per 4 tokens;
- * Both decode kernels compute t = x V_c^T, x B_w^T inside the same launch
+ * These three kernels compute t = x V_c^T, x B_w^T inside the same launch
  * (a few leading workgroups publish t with a per-call stamp in the
  * workspace; the others wait for it a bounded time and otherwise compute it
  * themselves), so a decode step is a single kernel launch;
@@ -222,10 +229,18 @@ int64_t archead_get_gemv_max_m(const archead_handle* h);
 
 /* Range of M served by the MFMA decode kernel, min_m <= M <= max_m (an
  * empty range, e.g. max_m = 0, never uses it; -1 restores the built-in
- * bound, 3 and 32).  Same threading rule as archead_set_gemv_max_m.  get
+ * bound for the head shape, see archead_logits).  Same threading rule as archead_set_gemv_max_m.  get
  * returns ARCHEAD_E_INVALID_ARG for a NULL argument. */
 archead_status archead_set_dec_range(archead_handle* h, int64_t min_m, int64_t max_m);
 archead_status archead_get_dec_range(const archead_handle* h, int64_t* min_m, int64_t* max_m);
+
+/* Range of M served by the several-token kernel when the MFMA decode kernel
+ * does not take the call (-1 restores the built-in bound for the head
+ * shape, see archead_logits; an empty range never uses it).  Same threading rule as
+ * archead_set_gemv_max_m; get returns ARCHEAD_E_INVALID_ARG for a NULL
+ * argument. */
+archead_status archead_set_mid_range(archead_handle* h, int64_t min_m, int64_t max_m);
+archead_status archead_get_mid_range(const archead_handle* h, int64_t* min_m, int64_t* max_m);
 
 /* Profiling hook: when start and stop are non-NULL hipEvent_t handles
  * (created by the caller on the handle's device), every later compute call

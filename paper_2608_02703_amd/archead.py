@@ -70,6 +70,9 @@ _SIGS = {
     "archead_set_dec_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
     "archead_get_dec_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
                                              ctypes.POINTER(ctypes.c_int64)]),
+    "archead_set_mid_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
+    "archead_get_mid_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_int64),
+                                             ctypes.POINTER(ctypes.c_int64)]),
     "archead_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p,
                                                  ctypes.c_void_p]),
     "archead_packed_bytes": (ctypes.c_uint64, [ctypes.POINTER(Desc)]),
@@ -83,6 +86,7 @@ _SIGS = {
 
 HOST_SYMBOLS = ("archead_validate_desc", "archead_set_gemv_max_m", "archead_set_timing_events",
                 "archead_get_gemv_max_m", "archead_set_dec_range", "archead_get_dec_range",
+                "archead_set_mid_range", "archead_get_mid_range",
                 "archead_packed_bytes", "archead_pack_int4",
                 "archead_unpack_int4", "archead_status_str", "archead_last_error")
 
@@ -220,13 +224,20 @@ class PackedHead:
     def set_dec_range(self, min_m: int, max_m: int):
         _check(self._lib.archead_set_dec_range(self.handle, min_m, max_m), self._lib)
 
+    def set_mid_range(self, min_m: int, max_m: int):
+        _check(self._lib.archead_set_mid_range(self.handle, min_m, max_m), self._lib)
+
     def force_path(self, path: str):
-        """Route every M to one kernel: "dec" (MFMA decode), "gemv" (decode
-        GEMV), "tiled" (many-token MFMA) or "auto" (the built-in choice).
-        Shapes a kernel does not support still take another one."""
-        dec, gemv = {"dec": ((1, 10 ** 9), -1), "gemv": ((1, 0), 10 ** 9),
-                     "tiled": ((1, 0), 0), "auto": ((-1, -1), -1)}[path]
+        """Route every M to one kernel: "dec" (MFMA decode), "mid" (several
+        tokens per pass over the head), "gemv" (decode GEMV), "tiled"
+        (many-token MFMA) or "auto" (the built-in choice).  Shapes a kernel
+        does not support still take another one."""
+        off, every = (1, 0), (1, 10 ** 9)
+        dec, mid, gemv = {"dec": (every, off, -1), "mid": (off, every, -1),
+                          "gemv": (off, off, 10 ** 9), "tiled": (off, off, 0),
+                          "auto": ((-1, -1), (-1, -1), -1)}[path]
         self.set_dec_range(*dec)
+        self.set_mid_range(*mid)
         self.set_gemv_max_m(gemv)
 
     def set_timing_events(self, start, stop):

@@ -71,6 +71,60 @@ bool use_dec(const archead_handle* h, int64_t M) {
          M <= h->dec_max_m.load(std::memory_order_relaxed) && dec_tokens_per_pass(h->desc) > 0;
 }
 
+MidLds mid_lds(const archead_desc& d) {
+  MidLds l;
+  const int tm = kMidTokMax;
+  l.kcu = int((d.r_c + 31) / 32);
+  l.kca = int((d.r_r + 31) / 32);
+  l.tstr = (l.kcu + l.kca) * 32 + 8;            // bf16 elements, +16 bytes: rows on different banks
+  const int xwin = 2 * tm * (2 * kMidWindow + 16);   // two x windows, 16 bytes of padding per row
+  const int tbytes = 3 * tm * l.tstr * 2;       // t as three bf16 parts (over the windows)
+  l.off_bias = xwin > tbytes ? xwin : tbytes;
+  l.off_red = l.off_bias + 2 * int(kMidWindow / d.g) * tm * 4;
+  l.off_y = l.off_red + kMidWaveCount * tm * 8;
+  l.off_sc = l.off_y + tm * 8;                  // per wave: [units][16 rows][d/g + 2] fp16
+  const int nu = d.g == 128 ? 3 : 2;            // units per wave and pass
+  l.total = l.off_sc + kMidWaveCount * nu * 16 * int(2 * (d.d / d.g) + 4);
+  return l;
+}
+
+bool mid_supported(const archead_desc& d) {
+  // groups of 64 or 128 codes, walked two windows of 256 elements at a time,
+  // at most 64 groups per row (a unit's scales staged in LDS), factor code rows
+  // read as dwords, at most 128 dimensions per factor (4 K-chunks)
+  if (d.g != 64 && d.g != 128) return false;
+  if (d.d % (2 * kMidWindow) || d.d / d.g > 64) return false;
+  if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return false;
+  return mid_lds(d).total <= kLdsBytes;
+}
+
+void default_ranges(const archead_desc& d, int64_t (&r)[4]) {
+  const int tpp = dec_tokens_per_pass(d);
+  if (mid_supported(d) && tpp > 0) {
+    r[0] = kDefaultDecMinM;
+    r[1] = tpp;
+    r[2] = tpp + 1;
+    r[3] = kDefaultMidMaxM;
+  } else {
+    r[0] = kDefaultDecMinM;
+    r[1] = kDefaultDecMaxM;
+    r[2] = 1;
+    r[3] = 0;
+  }
+}
+
+bool use_mid(const archead_handle* h, int64_t M) {
+  return M >= h->mid_min_m.load(std::memory_order_relaxed) &&
+         M <= h->mid_max_m.load(std::memory_order_relaxed) && mid_supported(h->desc);
+}
+
+Path choose_path(const archead_handle* h, int64_t M) {
+  if (use_dec(h, M)) return Path::kDec;
+  if (use_mid(h, M)) return Path::kMid;
+  if (use_gemv(h, M)) return Path::kGemv;
+  return Path::kTiled;
+}
+
 }  // namespace archead
 
 using namespace archead;
@@ -197,8 +251,10 @@ archead_status archead_set_timing_events(archead_handle* h, void* start, void* s
 archead_status archead_set_dec_range(archead_handle* h, int64_t min_m, int64_t max_m) {
   if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
   if (min_m < -1 || max_m < -1) return fail(ARCHEAD_E_INVALID_ARG, "dec range bounds must be >= -1");
-  h->dec_min_m.store(min_m == -1 ? kDefaultDecMinM : min_m);
-  h->dec_max_m.store(max_m == -1 ? kDefaultDecMaxM : max_m);
+  int64_t r[4];
+  default_ranges(h->desc, r);
+  h->dec_min_m.store(min_m == -1 ? r[0] : min_m);
+  h->dec_max_m.store(max_m == -1 ? r[1] : max_m);
   return ARCHEAD_OK;
 }
 
@@ -206,6 +262,23 @@ archead_status archead_get_dec_range(const archead_handle* h, int64_t* min_m, in
   if (!h || !min_m || !max_m) return fail(ARCHEAD_E_INVALID_ARG, "NULL argument");
   *min_m = h->dec_min_m.load();
   *max_m = h->dec_max_m.load();
+  return ARCHEAD_OK;
+}
+
+archead_status archead_set_mid_range(archead_handle* h, int64_t min_m, int64_t max_m) {
+  if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
+  if (min_m < -1 || max_m < -1) return fail(ARCHEAD_E_INVALID_ARG, "mid range bounds must be >= -1");
+  int64_t r[4];
+  default_ranges(h->desc, r);
+  h->mid_min_m.store(min_m == -1 ? r[2] : min_m);
+  h->mid_max_m.store(max_m == -1 ? r[3] : max_m);
+  return ARCHEAD_OK;
+}
+
+archead_status archead_get_mid_range(const archead_handle* h, int64_t* min_m, int64_t* max_m) {
+  if (!h || !min_m || !max_m) return fail(ARCHEAD_E_INVALID_ARG, "NULL argument");
+  *min_m = h->mid_min_m.load();
+  *max_m = h->mid_max_m.load();
   return ARCHEAD_OK;
 }
 

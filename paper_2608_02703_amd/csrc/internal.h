@@ -16,6 +16,8 @@ struct archead_handle {
   std::atomic<int64_t> gemv_max_m;
   std::atomic<int64_t> dec_min_m;   // M range of the MFMA decode kernel
   std::atomic<int64_t> dec_max_m;   // (empty when max < min)
+  std::atomic<int64_t> mid_min_m;   // M range of the several-token kernel
+  std::atomic<int64_t> mid_max_m;
   int t_spin_limit;       // polls of the in-launch stage-1 exchange before the fallback
   // persistent-grid sizes found with the occupancy API, keyed by kernel
   // variant; 0 = not computed yet
@@ -30,10 +32,14 @@ namespace archead {
 constexpr int64_t kDefaultGemvMaxM = 15;  // largest M on the decode kernel (measured crossover)
 constexpr int64_t kDefaultDecMinM = 3;    // M range of the MFMA decode kernel (one or
 constexpr int64_t kDefaultDecMaxM = 32;   // two tokens stream faster through the GEMV)
+constexpr int64_t kDefaultMidMaxM = 96;   // largest M of the several-token kernel
 constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
 constexpr int kDecTok = 16;               // tokens per pass of the MFMA decode kernel
 constexpr int kDecWaves = 8;              // waves per workgroup of the MFMA decode kernel
 constexpr int64_t kLdsBytes = 160 * 1024; // LDS per workgroup on gfx950
+constexpr int kMidTokMax = 32;            // tokens per tile of the several-token kernel
+constexpr int kMidWindow = 256;           // elements of d per x window of that kernel
+constexpr int kMidWaveCount = 8;          // its waves per workgroup
 
 archead_status fail(archead_status s, const char* fmt, ...);
 void clear_error();
@@ -70,6 +76,29 @@ DecLds dec_lds(const archead_desc& d, int tok);
 int dec_tokens_per_pass(const archead_desc& d);
 bool use_dec(const archead_handle* h, int64_t M);
 
+// Several-token kernel: LDS layout for its tiles of kMidTokMax tokens, whether the
+// head shape is supported, and whether a call with M tokens runs on it.
+struct MidLds {
+  int tstr = 0, off_bias = 0, off_red = 0, off_y = 0, off_sc = 0, total = 0;
+  int kcu = 0, kca = 0;
+};
+MidLds mid_lds(const archead_desc& d);
+bool mid_supported(const archead_desc& d);
+bool use_mid(const archead_handle* h, int64_t M);
+
+// Built-in M ranges for a head shape: {dec_min, dec_max, mid_min, mid_max}.
+// Where the several-token kernel applies, the MFMA decode kernel keeps the M
+// it serves in one pass and the several-token kernel takes over from there
+// up to kDefaultMidMaxM (measured crossovers); otherwise the decode kernel
+// keeps 3 .. kDefaultDecMaxM.
+void default_ranges(const archead_desc& d, int64_t (&r)[4]);
+
+// The kernel a call with M tokens runs on: the MFMA decode kernel, the
+// several-token kernel, the decode GEMV or the tiled MFMA kernel, in that
+// order of preference where the M ranges and the head shape allow.
+enum class Path { kDec, kMid, kGemv, kTiled };
+Path choose_path(const archead_handle* h, int64_t M);
+
 // grid of the GEMV kernel: persistent workgroups, at most one per 8 rows
 int64_t gemv_grid(const archead_handle* h, int tok, bool ce);
 
@@ -80,5 +109,12 @@ struct DecGrid {
   int64_t n_units = 0;          // units of 16 vocabulary rows
 };
 DecGrid dec_grid(const archead_handle* h);
+
+struct MidGrid {
+  int prod_blocks = 0;          // stage-1 producer workgroups (first in the grid)
+  int64_t cblocks = 0;          // consumer workgroups (balanced ranges of units)
+  int64_t n_units = 0;
+};
+MidGrid mid_grid(const archead_handle* h);
 
 }  // namespace archead

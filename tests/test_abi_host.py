@@ -167,6 +167,9 @@ def test_null_handle_calls(L):
                                None) == ab.E_INVALID_ARG
     assert L.archead_set_gemv_max_m(None, 3) == ab.E_INVALID_ARG
     assert L.archead_get_gemv_max_m(None) == -1
+    assert L.archead_set_mid_range(None, 2, 3) == ab.E_INVALID_ARG
+    assert L.archead_get_mid_range(None, ctypes.byref(ctypes.c_int64()),
+                                   ctypes.byref(ctypes.c_int64())) == ab.E_INVALID_ARG
     assert L.archead_set_dec_range(None, 2, 3) == ab.E_INVALID_ARG
     lo, hi = ctypes.c_int64(), ctypes.c_int64()
     assert L.archead_get_dec_range(None, ctypes.byref(lo), ctypes.byref(hi)) == ab.E_INVALID_ARG

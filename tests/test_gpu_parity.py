@@ -324,7 +324,7 @@ def test_all_paths_match_oracle(cfg, M):
     y = make_targets(cfg, M)
     ref_ce = ohead.cross_entropy(ref, y)
     try:
-        for name in ("dec", "gemv", "tiled"):
+        for name in ("dec", "mid", "gemv", "tiled"):
             ph.force_path(name)
             say(f"{cfg} M={M} forced {name}")
             assert_logits_close(gpu_logits(ph, x), ref, what=f"{cfg} M={M} {name}")
@@ -334,11 +334,11 @@ def test_all_paths_match_oracle(cfg, M):
         ph.force_path("auto")
 
 
-@pytest.mark.parametrize("path", ["gemv", "dec"])
+@pytest.mark.parametrize("path", ["gemv", "dec", "mid"])
 def test_identity_probe_decode_kernels_bit_exact(path):
     """One-hot x, no low-rank parts: every logit is s_res * c, exact in fp32,
-    and both decode kernels reach it exactly (the MFMA decode kernel's chain
-    -136 + (136 + c) is exact too)."""
+    and the decode kernels and the several-token kernel reach it exactly (the
+    MFMA kernels' chain -136 + (136 + c) is exact too)."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("tiny", rc=0, rr=0)
     ph = PackedHead.from_arrays(h)
@@ -373,7 +373,7 @@ def test_identity_probe_dec_qwen_sampled_bit_exact():
     ph.close()
 
 
-@pytest.mark.parametrize("path", ["dec", "gemv"])
+@pytest.mark.parametrize("path", ["dec", "gemv", "mid"])
 def test_stage1_fallback_matches(path):
     """With the in-launch stage-1 exchange's wait bound set to zero polls,
     every consumer wave computes its t values itself; the logits and CE
@@ -426,6 +426,57 @@ def test_dec_ragged(V, d, g, M, rc, rr):
     assert_ce_close(ce, ohead.cross_entropy(ref, y), what="dec ragged CE")
     bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
     assert_bf16_output(bits, o[:, :V], ref, "dec ragged bf16")
+    ph.close()
+
+
+@pytest.mark.parametrize("V,d,g,M,rc,rr", [(1000, 512, 64, 17, 16, 8), (777, 1024, 128, 40, 20, 4),
+                                           (33, 512, 64, 5, 16, 8), (8191, 512, 128, 64, 64, 0),
+                                           (4099, 1024, 64, 100, 0, 36), (130, 2560, 128, 33, 12, 28),
+                                           (500, 4096, 64, 20, 128, 128), (777, 96, 32, 5, 20, 4),
+                                           (300, 768, 128, 20, 8, 8)])
+def test_mid_ragged(V, d, g, M, rc, rr):
+    """The several-token kernel on partial 16-row units, tiles of 32 and 64
+    tokens with partial row blocks, several tiles, 4 to 64 scale groups,
+    padded rank dimensions (up to 128 + 128), wide row strides, bf16 output
+    and CE.  The last two shapes are outside its limits (g = 32; d not a
+    multiple of two 256-element windows): forcing it there must still give
+    correct results through another kernel."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", V=V, d=d, g=g, rc=rc, rr=rr)
+    x = make_x("tiny", M, d=d, basis="identity")
+    ph = PackedHead.from_arrays(h)
+    ph.force_path("mid")
+    ref = ohead.logits(h, x)
+    say(f"mid ragged V={V} d={d} g={g} M={M} rc={rc} rr={rr}")
+    assert_logits_close(gpu_logits(ph, x, ld=d + 8), ref, what="mid ragged")
+    out = torch.full((M, V + 3), 5.0, device="cuda")
+    ph.logits(torch_x(x), out=out[:, :V])
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    assert (o[:, V:] == 5.0).all(), "wrote past the row"
+    y = (np.arange(M) * 11 % V).astype(np.int32)
+    ce, _ = gpu_ce(ph, x, y)
+    assert_ce_close(ce, ohead.cross_entropy(ref, y), what="mid ragged CE")
+    bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
+    assert_bf16_output(bits, o[:, :V], ref, "mid ragged bf16")
+    ph.close()
+
+
+def test_identity_probe_mid_qwen_sampled_bit_exact():
+    """The one-hot probe on the Qwen-shaped head through the several-token
+    kernel (a tile of 64 tokens and a partial one), bit for bit."""
+    h = make_head("qwen_decode", rc=0, rr=0)
+    from paper_2608_02703_amd import PackedHead
+    ph = PackedHead.from_arrays(h)
+    ph.force_path("mid")
+    rng = np.random.default_rng(7)
+    cols = np.unique(np.concatenate([[0, 1, 7, 8, 31, 32, 127, 128, 255, 256, 2047, 4095],
+                                     rng.integers(0, h.d, 90)]))
+    x = np.zeros((cols.size, h.d), dtype=np.uint16)
+    x[np.arange(cols.size), cols] = 0x3F80
+    say(f"identity probe qwen, mid: M={cols.size}")
+    lg = gpu_logits(ph, x)
+    assert np.array_equal(lg.astype(np.float64), ohead.logits(h, x))
     ph.close()
 
 
