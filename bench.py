@@ -8,8 +8,9 @@ expansion, logit store) for one decode token (M=1), with every input already
 resident in HBM.  The step rotates over three copies of the packed head
 (3 x 336 MB > the 256 MB Infinity Cache), so each step streams its head from
 HBM.  The headline value is decode GB/s over the packed bytes.  Secondary
-lines: decode M=4 and M=16, and the M=4096 prefill fused-CE pass (tok/s and
-the many-token kernel's MFMA throughput).
+lines: decode M=4, 16, 32 and 64, greedy decoding (the fused argmax, no
+logits written) at M=1 and 16, and the M=4096 prefill fused-CE pass (tok/s
+and the many-token kernel's MFMA throughput).
 
 Before any timing, about 0.5 s of untimed decode steps bring the GPU's clocks
 to their sustained-load state (--clock-warmup; a cold GPU runs the first
@@ -178,6 +179,19 @@ def time_decode(heads, x, steps, warmup, ws=None):
     return ms, float(np.mean(kern)), float(np.median(kern))
 
 
+def time_argmax(heads, x, steps, warmup):
+    """ms per greedy step (fused argmax, no logits written)."""
+    M = x.shape[0]
+    wss = [hd.workspace(M, 2, x.device) for hd in heads]
+
+    def step(i):
+        k = i % len(heads)
+        heads[k].logits_argmax(x, ws=wss[k])
+    for i in range(warmup):
+        step(i)
+    return _timed_loop(step, steps)
+
+
 def time_prefill(heads, x, y, steps, warmup):
     """(ms per step, mean CE, mean many-token kernel ms)."""
     import torch
@@ -317,19 +331,27 @@ def main():
     h = make_head(cfg)
     pbytes = head_bytes(h)
     heads = upload_copies(h, N_COPIES)
-    xb = make_x(cfg, 16)
+    xb = make_x(cfg, 64)
     x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
 
     n_clock = clock_warmup(heads, x_all[:1], args.clock_warmup)
     log(f"clock warm-up: {n_clock} untimed decode steps in {args.clock_warmup} s")
     res = {}
-    for M in (1, 4, 16):
+    for M in (1, 4, 16, 32, 64):
         x = x_all[:M]
         ms, kern_ms, kern_med = time_decode(heads, x, args.steps if M == 1 else
                                             max(20, args.steps // 4), args.warmup)
         res[M] = (ms, kern_ms, kern_med)
         log(f"decode M={M}: {ms * 1e3:.1f} us/step, head kernel {kern_ms * 1e3:.1f} us "
             f"(median {kern_med * 1e3:.1f}), {pbytes / ms / 1e6:.0f} GB/s over packed bytes")
+
+    # greedy decoding: the fused argmax step (no [M, V] logits written)
+    greedy = {}
+    for M in (1, 16):
+        gms = time_argmax(heads, x_all[:M], max(20, args.steps // 2), args.warmup)
+        greedy[str(M)] = {"us_per_step": round(gms * 1e3, 2),
+                          "gbs_packed": round(pbytes / gms / 1e6, 1)}
+        log(f"greedy (fused argmax) M={M}: {gms * 1e3:.1f} us/step")
 
     # context: the same decode step through a dense bf16 head of the same
     # shape (torch linear, random weights), the bytes the packed head avoids
@@ -406,6 +428,7 @@ def main():
                             "kernel_us": round(v[1] * 1e3, 2),
                             "gbs_packed": round(pbytes / v[0] / 1e6, 1)}
                    for M, v in res.items()},
+        "greedy_argmax": greedy,
         "prefill": prefill,
         "dense_bf16_head": dense,
     }

@@ -93,7 +93,8 @@ typedef enum archead_int4_encoding { ARCHEAD_INT4_V1 = 1 } archead_int4_encoding
 
 typedef enum archead_op {
   ARCHEAD_OP_LOGITS = 0,    /* archead_logits    */
-  ARCHEAD_OP_LOGITS_CE = 1  /* archead_logits_ce */
+  ARCHEAD_OP_LOGITS_CE = 1, /* archead_logits_ce */
+  ARCHEAD_OP_ARGMAX = 2     /* archead_logits_argmax */
 } archead_op;
 
 /* Shape and encoding of a packed head (the "integer shapes/groups" metadata
@@ -218,6 +219,25 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x,
                                  archead_dtype tgt_dtype, float* ce,
                                  float* mean_ce, void* ws, size_t ws_bytes,
                                  void* stream);
+
+/* Greedy decoding over the packed head: idx[m] = the smallest v attaining
+ * max_v logit[m, v] and, when max_logit is not NULL, max_logit[m] = that
+ * logit, for m < M.  The logits are the fp32 ones archead_logits computes
+ * (the same kernel for the same M), so idx equals the first-index argmax of
+ * its output, ties included.  This is the next-token choice of the
+ * generation runs the paper times with the packed head in place ("Efficiency
+ * and Calibration" and its throughput appendix), fused into the head pass,
+ * and its top-1 agreement metric ("Logit Fidelity"): the [M, V]
+ * logits are never written; each kernel leaves per-partial (max, smallest
+ * index at the max) pairs in the workspace and a merge kernel combines them.
+ *   idx        device int64 [M], 8-byte aligned
+ *   max_logit  device fp32 [M] or NULL
+ *   ws         archead_workspace_bytes(h, M, ARCHEAD_OP_ARGMAX) bytes
+ * Other arguments and errors as archead_logits.  A token whose logits are
+ * all NaN gets idx -1. */
+archead_status archead_logits_argmax(const archead_handle* h, const void* x, int64_t M,
+                                     int64_t ldx, int64_t* idx, float* max_logit, void* ws,
+                                     size_t ws_bytes, void* stream);
 
 /* Largest M served by the decode GEMV kernel when the MFMA decode kernel
  * does not take the call; larger M use the tiled MFMA kernel (unless

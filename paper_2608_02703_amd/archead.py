@@ -20,7 +20,7 @@ ABI_VERSION = 1
 OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
 F32, BF16, F16, I32, I64, I8 = range(6)
 INT4_V1 = 1
-OP_LOGITS, OP_LOGITS_CE = 0, 1
+OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX = 0, 1, 2
 
 
 class ArcheadError(RuntimeError):
@@ -65,6 +65,9 @@ _SIGS = {
                                          ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                          ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_logits_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                             ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
     "archead_set_gemv_max_m": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64]),
     "archead_get_gemv_max_m": (ctypes.c_int64, [ctypes.c_void_p]),
     "archead_set_dec_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
@@ -280,6 +283,22 @@ class PackedHead:
             self.handle, _ptr(x), M, x.stride(0), _ptr(out), code, out.stride(0),
             _ptr(ws), ws.numel(), self._stream(x.device)), self._lib)
         return out
+
+    def logits_argmax(self, x, idx=None, max_logit=None, ws=None):
+        """Greedy next token: returns (idx int64 [M], max_logit fp32 [M]), the
+        smallest vocabulary index of each token's largest logit."""
+        import torch
+        if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+            raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+        M = x.shape[0]
+        idx = torch.empty(M, dtype=torch.int64, device=x.device) if idx is None else idx
+        if max_logit is None:
+            max_logit = torch.empty(M, dtype=torch.float32, device=x.device)
+        ws = self.workspace(M, OP_ARGMAX, x.device) if ws is None else ws
+        _check(self._lib.archead_logits_argmax(
+            self.handle, _ptr(x), M, x.stride(0), _ptr(idx), _ptr(max_logit), _ptr(ws),
+            ws.numel(), self._stream(x.device)), self._lib)
+        return idx, max_logit
 
     def logits_ce(self, x, targets, ce=None, mean=None, ws=None):
         """Fused log-softmax + cross-entropy; returns (ce [M], mean [1])."""

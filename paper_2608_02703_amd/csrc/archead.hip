@@ -289,6 +289,7 @@ struct GemvArgs {
   const void* tgt;
   int tgt64;
   float2* part;    // [M, n_part]
+  int* part_idx;   // [M, n_part] argmax partials, or null
   int64_t n_part;
   float* tgt_logit;  // [M]
 };
@@ -452,8 +453,12 @@ __device__ __forceinline__ void gemv_chunk(float (&acc)[RB][TOK], const uint4 (&
 template <int TOK>
 struct CeState {
   float mx[TOK], se[TOK];
+  int am[TOK];      // smallest vocabulary index attaining mx so far
   int64_t y[TOK];
 };
+
+// "no index yet" for the argmax partials: larger than any vocabulary index
+constexpr int kNoIdx = 0x7fffffff;
 
 // End of a step: add the rank-r expansions of the lane's rows, reduce over
 // the segment and store the logits (or fold them into the softmax state).
@@ -504,9 +509,12 @@ __device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvA
         else
           reinterpret_cast<float*>(a.out)[o] = l;
       } else {
+        // a lane's rows come in increasing order: the first of equal
+        // maxima is the smallest index
         if (l > ce.mx[tt]) {
           ce.se[tt] = ce.se[tt] * fast_exp(ce.mx[tt] - l) + 1.f;
           ce.mx[tt] = l;
+          ce.am[tt] = int(v);
         } else {
           ce.se[tt] += fast_exp(l - ce.mx[tt]);
         }
@@ -537,6 +545,7 @@ void k_gemv(GemvArgs a) {
   constexpr int WR = RB * SEG;               // rows per wave step
   extern __shared__ __align__(16) unsigned char smem[];
   __shared__ float2 red[kWaves][TOK];
+  __shared__ int redi[kWaves][TOK];
 
   const int d = a.d;
   const int C = d / 32;                      // 16-byte chunks per row
@@ -617,9 +626,12 @@ void k_gemv(GemvArgs a) {
   for (int tt = 0; tt < TOK; ++tt) {
     ce.mx[tt] = -INFINITY;
     ce.se[tt] = 0.f;
+    ce.am[tt] = kNoIdx;
+    ce.y[tt] = -1;
     if constexpr (CE)
-      ce.y[tt] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + tt]
-                         : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + tt]);
+      if (a.tgt)
+        ce.y[tt] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + tt]
+                           : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + tt]);
   }
   float acc[RB][TOK];
 #pragma unroll
@@ -805,22 +817,38 @@ void k_gemv(GemvArgs a) {
   }
 
   if constexpr (CE) {
+    // (max, sum exp) over the workgroup, and the argmax: the smallest index
+    // among the lanes (then waves) whose maximum is the overall one
 #pragma unroll
     for (int tt = 0; tt < TOK; ++tt) {
+      const float own = ce.mx[tt];
 #pragma unroll
       for (int off = 32; off > 0; off >>= 1) {
         const float om = __shfl_xor(ce.mx[tt], off, 64);
         const float os = __shfl_xor(ce.se[tt], off, 64);
         lse_merge(ce.mx[tt], ce.se[tt], om, os);
       }
-      if (lane == 0) red[wid][tt] = make_float2(ce.mx[tt], ce.se[tt]);
+      int ai = own == ce.mx[tt] ? ce.am[tt] : kNoIdx;
+#pragma unroll
+      for (int off = 32; off > 0; off >>= 1) ai = min(ai, __shfl_xor(ai, off, 64));
+      if (lane == 0) {
+        red[wid][tt] = make_float2(ce.mx[tt], ce.se[tt]);
+        redi[wid][tt] = ai;
+      }
     }
     __syncthreads();
     if (threadIdx.x < TOK) {
       const int tt = threadIdx.x;
       float m = red[0][tt].x, s = red[0][tt].y;
       for (int w = 1; w < kWaves; ++w) lse_merge(m, s, red[w][tt].x, red[w][tt].y);
-      a.part[(a.tok0 + tt) * a.n_part + (blockIdx.x - a.n_prod_blocks)] = make_float2(m, s);
+      const int64_t o = (a.tok0 + tt) * a.n_part + (blockIdx.x - a.n_prod_blocks);
+      a.part[o] = make_float2(m, s);
+      if (a.part_idx) {
+        int ai = kNoIdx;
+        for (int w = 0; w < kWaves; ++w)
+          if (red[w][tt].x == m) ai = min(ai, redi[w][tt]);
+        a.part_idx[o] = ai;
+      }
     }
   }
 }
@@ -927,6 +955,12 @@ __device__ __forceinline__ float row16_max(float v) {
   v = fmaxf(v, dpp_swap<0x141>(v));
   return fmaxf(v, dpp_swap<0x140>(v));
 }
+__device__ __forceinline__ int row16_min_i(int v) {
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0xB1, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x4E, 0xF, 0xF, false));
+  v = min(v, __builtin_amdgcn_update_dpp(0, v, 0x141, 0xF, 0xF, false));
+  return min(v, __builtin_amdgcn_update_dpp(0, v, 0x140, 0xF, 0xF, false));
+}
 __device__ __forceinline__ float row16_sum(float v) {
   v += dpp_swap<0xB1>(v);
   v += dpp_swap<0x4E>(v);
@@ -965,6 +999,7 @@ struct MfmaArgs {
   const void* tgt;
   int tgt64;
   float2* part;            // [M, n_vt]
+  int* part_idx;           // [M, n_vt] argmax partials, or null
   float* tgt_logit;        // [M]
 };
 
@@ -1111,7 +1146,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 #pragma unroll
   for (int ni = 0; ni < 4; ++ni) fin[ni] = a.fin[vt * kTN + 64 * wn + 16 * ni + lr];
   int64_t y_row = -1;
-  if (CE && tid < rows)
+  if (CE && tid < rows && a.tgt)
     y_row = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[m0 + tid]
                     : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[m0 + tid]);
   issue(0, 0);
@@ -1247,38 +1282,61 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
     // staged in LDS as tile-local columns (-1: not in this tile).
     float2* sred = reinterpret_cast<float2*>(mfma_lds);               // [4][kTM]
     int* sy = reinterpret_cast<int*>(mfma_lds + 4 * kTM * sizeof(float2));   // [kTM]
+    int* sidx = sy + kTM;                                                // [4][kTM] argmax
     __syncthreads();
     if (tid < kTM) sy[tid] = y_row >= v0 && y_row < v0 + cols ? int(y_row - v0) : -1;
     __syncthreads();
+    // IDX: also the smallest tile column at each row's maximum (argmax
+    // partials); compiled apart so the CE-only pass pays nothing for it
+    auto rows_pass = [&](auto IDX) {
+      constexpr bool kIdx = decltype(IDX)::value;
 #pragma unroll
-    for (int mi = 0; mi < 8; ++mi)
+      for (int mi = 0; mi < 8; ++mi)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int row = 128 * wm + 16 * mi + 4 * q + i;
-        const int yl = sy[row];
-        float mx = -INFINITY;
+        for (int i = 0; i < 4; ++i) {
+          const int row = 128 * wm + 16 * mi + 4 * q + i;
+          const int yl = sy[row];
+          float mx = -INFINITY;
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni)
-          if (64 * wn + 16 * ni + lr < cols) mx = fmaxf(mx, acc[mi][ni][i]);
-        mx = row16_max(mx);
-        float se = 0.f;
+          for (int ni = 0; ni < 4; ++ni)
+            if (64 * wn + 16 * ni + lr < cols) mx = fmaxf(mx, acc[mi][ni][i]);
+          mx = row16_max(mx);
+          float se = 0.f;
+          int ai = kNoIdx;
 #pragma unroll
-        for (int ni = 0; ni < 4; ++ni) {
-          const int col = 64 * wn + 16 * ni + lr;
-          if (col < cols) {
-            se += fast_exp(acc[mi][ni][i] - mx);
-            if (col == yl) a.tgt_logit[m0 + row] = acc[mi][ni][i];
+          for (int ni = 0; ni < 4; ++ni) {
+            const int col = 64 * wn + 16 * ni + lr;
+            if (col < cols) {
+              se += fast_exp(acc[mi][ni][i] - mx);
+              if (col == yl) a.tgt_logit[m0 + row] = acc[mi][ni][i];
+              if (kIdx && acc[mi][ni][i] == mx) ai = min(ai, col);
+            }
+          }
+          se = row16_sum(se);
+          if constexpr (kIdx) ai = row16_min_i(ai);
+          if (lr == 0) {
+            sred[wn * kTM + row] = make_float2(mx, se);
+            if constexpr (kIdx) sidx[wn * kTM + row] = ai;
           }
         }
-        se = row16_sum(se);
-        if (lr == 0) sred[wn * kTM + row] = make_float2(mx, se);
-      }
+    };
+    if (a.part_idx)
+      rows_pass(std::true_type{});
+    else
+      rows_pass(std::false_type{});
     __syncthreads();
     if (tid < rows) {
       float m_ = sred[tid].x, s_ = sred[tid].y;
 #pragma unroll
       for (int w = 1; w < 4; ++w) lse_merge(m_, s_, sred[w * kTM + tid].x, sred[w * kTM + tid].y);
       a.part[(m0 + tid) * a.n_vt + vt] = make_float2(m_, s_);
+      if (a.part_idx) {
+        int ai = kNoIdx;
+#pragma unroll
+        for (int w = 0; w < 4; ++w)
+          if (sred[w * kTM + tid].x == m_) ai = min(ai, sidx[w * kTM + tid]);
+        a.part_idx[(m0 + tid) * a.n_vt + vt] = ai == kNoIdx ? kNoIdx : int(v0) + ai;
+      }
     }
   }
 }
@@ -1565,6 +1623,48 @@ __global__ __launch_bounds__(kBlock) void k_ce_merge(const float2* part, int64_t
   }
 }
 
+// Per token: the largest of the partial maxima and the smallest index among
+// the partials that hold it (the smallest vocabulary index of the maximum).
+__global__ __launch_bounds__(kBlock) void k_argmax_merge(const float2* part, const int* pidx,
+                                                         int64_t n_part, int64_t* idx,
+                                                         float* max_logit) {
+  __shared__ float smx[kBlock];
+  __shared__ int sai[kBlock];
+  const int64_t m = blockIdx.x;
+  float mx = -INFINITY;
+  int ai = kNoIdx;
+  for (int64_t p = threadIdx.x; p < n_part; p += kBlock) {
+    const float v = part[m * n_part + p].x;
+    const int i = pidx[m * n_part + p];
+    if (v > mx) {
+      mx = v;
+      ai = i;
+    } else if (v == mx) {
+      ai = min(ai, i);
+    }
+  }
+  smx[threadIdx.x] = mx;
+  sai[threadIdx.x] = ai;
+  __syncthreads();
+  for (int s = kBlock / 2; s > 0; s >>= 1) {
+    if (threadIdx.x < s) {
+      const float b = smx[threadIdx.x + s];
+      const int bi = sai[threadIdx.x + s];
+      if (b > smx[threadIdx.x]) {
+        smx[threadIdx.x] = b;
+        sai[threadIdx.x] = bi;
+      } else if (b == smx[threadIdx.x]) {
+        sai[threadIdx.x] = min(sai[threadIdx.x], bi);
+      }
+    }
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    idx[m] = sai[0] == kNoIdx ? int64_t(-1) : int64_t(sai[0]);
+    if (max_logit) max_logit[m] = smx[0];
+  }
+}
+
 __global__ __launch_bounds__(kBlock) void k_mean(const float* v, int64_t n, float* out) {
   __shared__ float s[kBlock];
   float acc = 0.f;
@@ -1649,6 +1749,7 @@ struct DecArgs {
   const void* tgt;
   int tgt64;
   float2* part;          // [tokens, n_part]
+  int* part_idx;         // [tokens, n_part] argmax partials, or null
   int64_t n_part;
   float* tgt_logit;
 };
@@ -1740,8 +1841,9 @@ void k_dec(DecArgs a) {
   for (int r = 0; r < 4; ++r) {
     ce.mx[r] = -INFINITY;
     ce.se[r] = 0.f;
+    ce.am[r] = kNoIdx;
     ce.y[r] = -1;
-    if (CE && 4 * q + r < M)
+    if (CE && 4 * q + r < M && a.tgt)
       ce.y[r] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + 4 * q + r]
                         : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + 4 * q + r]);
   }
@@ -1899,9 +2001,10 @@ void k_dec(DecArgs a) {
             else
               reinterpret_cast<float*>(a.out)[o] = l;
           } else {
-            if (l > ce.mx[r]) {
+            if (l > ce.mx[r]) {   // rows come in increasing order per lane
               ce.se[r] = ce.se[r] * fast_exp(ce.mx[r] - l) + 1.f;
               ce.mx[r] = l;
+              ce.am[r] = int(v);
             } else {
               ce.se[r] += fast_exp(l - ce.mx[r]);
             }
@@ -1961,18 +2064,30 @@ void k_dec(DecArgs a) {
   if constexpr (CE) {
     // per token: merge the 16 rows' states of each quarter, then the waves
     float2* red = reinterpret_cast<float2*>(dec_lds + a.off_red);   // [kDWaves][kDTok]
+    int* redi = reinterpret_cast<int*>(red + kDWaves * kDTok);       // [kDWaves][kDTok]
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const float m = row16_max(ce.mx[r]);
       float se = m == -INFINITY ? 0.f : ce.se[r] * fast_exp(ce.mx[r] - m);
       se = row16_sum(se);
-      if (lr == 0) red[wid * kDTok + 4 * q + r] = make_float2(m, se);
+      const int ai = row16_min_i(ce.mx[r] == m ? ce.am[r] : kNoIdx);
+      if (lr == 0) {
+        red[wid * kDTok + 4 * q + r] = make_float2(m, se);
+        redi[wid * kDTok + 4 * q + r] = ai;
+      }
     }
     __syncthreads();
     if (tid < M) {
       float m = red[tid].x, s = red[tid].y;
       for (int w = 1; w < kDWaves; ++w) lse_merge(m, s, red[w * kDTok + tid].x, red[w * kDTok + tid].y);
-      a.part[(a.tok0 + tid) * a.n_part + (blockIdx.x - a.n_prod_blocks)] = make_float2(m, s);
+      const int64_t o = (a.tok0 + tid) * a.n_part + (blockIdx.x - a.n_prod_blocks);
+      a.part[o] = make_float2(m, s);
+      if (a.part_idx) {
+        int ai = kNoIdx;
+        for (int w = 0; w < kDWaves; ++w)
+          if (red[w * kDTok + tid].x == m) ai = min(ai, redi[w * kDTok + tid]);
+        a.part_idx[o] = ai;
+      }
     }
   }
 }
@@ -2018,13 +2133,14 @@ struct MidArgs {
   int n_cblocks;         // consumer workgroups
   int n_prod_blocks;     // leading workgroups that compute t
   int tstr;              // LDS: bf16 elements per token row of each part of t
-  int off_bias, off_red, off_y, off_sc;   // LDS byte offsets
+  int off_bias, off_red, off_y, off_idx, off_sc;   // LDS byte offsets
   void* out;
   int64_t ldo;
   int out_bf16;
   const void* tgt;
   int tgt64;
   float2* part;          // [tokens, n_part]
+  int* part_idx;         // [tokens, n_part] argmax partials, or null
   int64_t n_part;
   float* tgt_logit;
 };
@@ -2099,16 +2215,21 @@ void k_mid(MidArgs a) {
   auto* const sbias = reinterpret_cast<__attribute__((address_space(3))) float*>(L + a.off_bias);
   float2* const sred = reinterpret_cast<float2*>(mid_lds + a.off_red);
   int64_t* const sy = reinterpret_cast<int64_t*>(mid_lds + a.off_y);
+  int* const sidx = reinterpret_cast<int*>(mid_lds + a.off_idx);   // [waves][TM] argmax
   // residual scales of this wave's units: [unit][row][group] fp16, rows
   // padded by 4 bytes so the 16 rows read at one step fall on distinct banks
   const int sstr = 2 * ngrp + 4;
   lds_u8* const ssc = L + a.off_sc + wid * (NU * 16 * sstr);
   if constexpr (CE) {
-    for (int e = tid; e < kMidWaves * TM; e += kMidBlock) sred[e] = make_float2(-INFINITY, 0.f);
+    for (int e = tid; e < kMidWaves * TM; e += kMidBlock) {
+      sred[e] = make_float2(-INFINITY, 0.f);
+      sidx[e] = kNoIdx;
+    }
     for (int e = tid; e < TM; e += kMidBlock)
-      sy[e] = e >= M ? int64_t(-1)
-                     : (a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + e]
-                                : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + e]));
+      sy[e] = e >= M || !a.tgt
+                  ? int64_t(-1)
+                  : (a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + e]
+                             : int64_t(reinterpret_cast<const int32_t*>(a.tgt)[a.tok0 + e]));
   }
 
   // buffer resource over the rows of unit u of an array with `stride` bytes
@@ -2437,9 +2558,12 @@ void k_mid(MidArgs a) {
           } else {
             const float m = row16_max(vok ? l : -INFINITY);
             const float e = row16_sum(vok ? fast_exp(l - m) : 0.f);
+            const int ai = row16_min_i(vok && l == m ? int(v) : kNoIdx);
             if (vok && tt < M && v == sy[tt]) a.tgt_logit[a.tok0 + tt] = l;
             if (lr == 0) {
               float2 cur = sred[wid * TM + tt];
+              const int ci = sidx[wid * TM + tt];
+              sidx[wid * TM + tt] = m > cur.x ? ai : (m == cur.x ? min(ci, ai) : ci);
               lse_merge(cur.x, cur.y, m, e);
               sred[wid * TM + tt] = cur;
             }
@@ -2456,6 +2580,12 @@ void k_mid(MidArgs a) {
       float m = sred[tid].x, s = sred[tid].y;
       for (int w = 1; w < kMidWaves; ++w) lse_merge(m, s, sred[w * TM + tid].x, sred[w * TM + tid].y);
       a.part[(a.tok0 + tid) * a.n_part + cb] = make_float2(m, s);
+      if (a.part_idx) {
+        int ai = kNoIdx;
+        for (int w = 0; w < kMidWaves; ++w)
+          if (sred[w * TM + tid].x == m) ai = min(ai, sidx[w * TM + tid]);
+        a.part_idx[(a.tok0 + tid) * a.n_part + cb] = ai;
+      }
     }
   }
 }
@@ -2607,7 +2737,7 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
     w.uc_off = off;
     off = align256(off + size_t(d.V) * nch * 32);                    // [c|c] x 16
   }
-  if (op == ARCHEAD_OP_LOGITS_CE) {
+  if (op == ARCHEAD_OP_LOGITS_CE || op == ARCHEAD_OP_ARGMAX) {
     // GEMV: all CE passes share one grid (the smallest of the variants
     // used) so every token row of the partials has the same number of
     // slots.  MFMA: one slot per vocabulary tile.
@@ -2628,6 +2758,10 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
     off = align256(off + 2 * sizeof(float) * size_t(M) * size_t(np));
     w.tgt_off = off;
     off = align256(off + sizeof(float) * size_t(M));
+    if (op == ARCHEAD_OP_ARGMAX) {
+      w.pidx_off = off;
+      off = align256(off + sizeof(int32_t) * size_t(M) * size_t(np));
+    }
   }
   w.total = off;
   return w;
@@ -2909,7 +3043,8 @@ archead_status launch_mid(const archead_handle* h, const void* x, int64_t M, int
     a.M = tok;
     a.kcu = l.kcu; a.kca = l.kca;
     a.tstr = l.tstr;
-    a.off_bias = l.off_bias; a.off_red = l.off_red; a.off_y = l.off_y; a.off_sc = l.off_sc;
+    a.off_bias = l.off_bias; a.off_red = l.off_red; a.off_y = l.off_y; a.off_idx = l.off_idx;
+    a.off_sc = l.off_sc;
     if (l.total > 65536) {
       hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(fn),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, l.total);
@@ -2966,6 +3101,60 @@ archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStr
   if (grid > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "too many MFMA tiles");
   e = hipExtLaunchKernel(fn, dim3(unsigned(grid)), dim3(kMBlock), args, size_t(lds), s, ev0, ev1, 0);
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "MFMA launch");
+}
+
+// The fused-softmax pass of every kernel: per token and partial (a
+// workgroup, or a vocabulary tile) the (max, sum exp) pair, the target's
+// logit when targets is not null, and the argmax partials when pidx is not
+// null.
+archead_status launch_softmax_partials(const archead_handle* h, const void* x, int64_t M,
+                                       int64_t ldx, const void* targets, bool tgt64,
+                                       const WsLayout& w, char* base, int* pidx, hipStream_t s) {
+  float2* part = reinterpret_cast<float2*>(base + w.part_off);
+  float* tl = reinterpret_cast<float*>(base + w.tgt_off);
+  const int64_t n_part = w.n_part;
+  const Path path = choose_path(h, M);
+  if (path == Path::kDec) {
+    DecArgs a;
+    memset(&a, 0, sizeof a);
+    a.tgt = targets;
+    a.tgt64 = tgt64;
+    a.part = part;
+    a.part_idx = pidx;
+    a.n_part = n_part;
+    a.tgt_logit = tl;
+    return launch_dec(h, x, M, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off), a, true, s);
+  }
+  if (path == Path::kMid) {
+    MidArgs a;
+    memset(&a, 0, sizeof a);
+    a.tgt = targets;
+    a.tgt64 = tgt64;
+    a.part = part;
+    a.part_idx = pidx;
+    a.n_part = n_part;
+    a.tgt_logit = tl;
+    return launch_mid(h, x, M, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off), a, true, s);
+  }
+  if (path == Path::kTiled) {
+    archead_status st = launch_mfma_prologue(h, x, M, ldx, w, base, s);
+    if (st != ARCHEAD_OK) return st;
+    MfmaArgs a = mfma_args(h, x, M, ldx, w, base);
+    a.tgt = targets;
+    a.tgt64 = tgt64;
+    a.part = part;
+    a.part_idx = pidx;
+    a.tgt_logit = tl;
+    return launch_mfma(h, a, true, s);
+  }
+  GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off));
+  a.tgt = targets;
+  a.tgt64 = tgt64;
+  a.part = part;
+  a.part_idx = pidx;
+  a.n_part = n_part;
+  a.tgt_logit = tl;
+  return launch_gemv_passes(h, a, M, true, n_part, s);
 }
 
 }  // namespace
@@ -3103,49 +3292,13 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t
     return fail(ARCHEAD_E_MISALIGNED, "targets / ce / mean_ce misaligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const WsLayout w = ws_layout(h, M, ARCHEAD_OP_LOGITS_CE);
-  char* base = static_cast<char*>(ws);
-  float2* part = reinterpret_cast<float2*>(base + w.part_off);
-  float* tl = reinterpret_cast<float*>(base + w.tgt_off);
-  const int64_t n_part = w.n_part;
-  const Path path = choose_path(h, M);
-  if (path == Path::kDec) {
-    DecArgs a;
-    memset(&a, 0, sizeof a);
-    a.tgt = targets;
-    a.tgt64 = tgt_dtype == ARCHEAD_I64;
-    a.part = part;
-    a.n_part = n_part;
-    a.tgt_logit = tl;
-    st = launch_dec(h, x, M, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off), a, true, s);
-  } else if (path == Path::kMid) {
-    MidArgs a;
-    memset(&a, 0, sizeof a);
-    a.tgt = targets;
-    a.tgt64 = tgt_dtype == ARCHEAD_I64;
-    a.part = part;
-    a.n_part = n_part;
-    a.tgt_logit = tl;
-    st = launch_mid(h, x, M, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off), a, true, s);
-  } else if (path == Path::kTiled) {
-    st = launch_mfma_prologue(h, x, M, ldx, w, base, s);
-    if (st != ARCHEAD_OK) return st;
-    MfmaArgs a = mfma_args(h, x, M, ldx, w, base);
-    a.tgt = targets;
-    a.tgt64 = tgt_dtype == ARCHEAD_I64;
-    a.part = part;
-    a.tgt_logit = tl;
-    st = launch_mfma(h, a, true, s);
-  } else {
-    GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off));
-    a.tgt = targets;
-    a.tgt64 = tgt_dtype == ARCHEAD_I64;
-    a.part = part;
-    a.n_part = n_part;
-    a.tgt_logit = tl;
-    st = launch_gemv_passes(h, a, M, true, n_part, s);
-  }
+  st = launch_softmax_partials(h, x, M, ldx, targets, tgt_dtype == ARCHEAD_I64, w,
+                               static_cast<char*>(ws), nullptr, s);
   if (st != ARCHEAD_OK) return st;
-  hipLaunchKernelGGL(k_ce_merge, dim3(unsigned(M)), dim3(kBlock), 0, s, part, n_part, targets,
+  char* base = static_cast<char*>(ws);
+  const float2* part = reinterpret_cast<const float2*>(base + w.part_off);
+  const float* tl = reinterpret_cast<const float*>(base + w.tgt_off);
+  hipLaunchKernelGGL(k_ce_merge, dim3(unsigned(M)), dim3(kBlock), 0, s, part, w.n_part, targets,
                      int(tgt_dtype == ARCHEAD_I64), tl, h->desc.V, ce);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "CE merge launch");
@@ -3155,6 +3308,28 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t
     if (e != hipSuccess) return hip_fail(e, "mean launch");
   }
   return ARCHEAD_OK;
+}
+
+archead_status archead_logits_argmax(const archead_handle* h, const void* x, int64_t M,
+                                     int64_t ldx, int64_t* idx, float* max_logit, void* ws,
+                                     size_t ws_bytes, void* stream) {
+  clear_error();
+  archead_status st = check_call(h, x, M, ldx, ws, ws_bytes, ARCHEAD_OP_ARGMAX);
+  if (st != ARCHEAD_OK || M == 0) return st;
+  if (!idx) return fail(ARCHEAD_E_INVALID_ARG, "idx is required");
+  if (!aligned(idx, 8) || (max_logit && !aligned(max_logit, 4)))
+    return fail(ARCHEAD_E_MISALIGNED, "idx / max_logit misaligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const WsLayout w = ws_layout(h, M, ARCHEAD_OP_ARGMAX);
+  char* base = static_cast<char*>(ws);
+  int* pidx = reinterpret_cast<int*>(base + w.pidx_off);
+  st = launch_softmax_partials(h, x, M, ldx, nullptr, false, w, base, pidx, s);
+  if (st != ARCHEAD_OK) return st;
+  const float2* part = reinterpret_cast<const float2*>(base + w.part_off);
+  hipLaunchKernelGGL(k_argmax_merge, dim3(unsigned(M)), dim3(kBlock), 0, s, part, pidx,
+                     w.n_part, idx, max_logit);
+  hipError_t e = hipGetLastError();
+  return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "argmax merge launch");
 }
 
 }  // extern "C"

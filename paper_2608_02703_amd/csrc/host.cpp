@@ -48,7 +48,7 @@ DecLds dec_lds(const archead_desc& d, int tok) {
   l.off_bias = tok * l.xstr;
   l.off_t = l.off_bias + int(d.d / d.g) * kDecTok * 4;
   l.off_red = l.off_t + 3 * tok * l.tstr * 2;   // t as three bf16 parts
-  l.total = l.off_red + kDecWaves * kDecTok * 8;
+  l.total = l.off_red + kDecWaves * kDecTok * (8 + 4);   // softmax and argmax partials
   return l;
 }
 
@@ -82,7 +82,8 @@ MidLds mid_lds(const archead_desc& d) {
   l.off_bias = xwin > tbytes ? xwin : tbytes;
   l.off_red = l.off_bias + 2 * int(kMidWindow / d.g) * tm * 4;
   l.off_y = l.off_red + kMidWaveCount * tm * 8;
-  l.off_sc = l.off_y + tm * 8;                  // per wave: [units][16 rows][d/g + 2] fp16
+  l.off_idx = l.off_y + tm * 8;                 // argmax partials [waves][tm]
+  l.off_sc = l.off_idx + kMidWaveCount * tm * 4; // per wave: [units][16 rows][d/g + 2] fp16
   const int nu = d.g == 128 ? 3 : 2;            // units per wave and pass
   l.total = l.off_sc + kMidWaveCount * nu * 16 * int(2 * (d.d / d.g) + 4);
   return l;

@@ -59,6 +59,7 @@ struct WsLayout {
   size_t uc_off = 0;     // int8 [V][blocks][2][16] codes of U_c and A_w, padded, twice
   size_t part_off = 0;   // float2 [M, n_part] (CE)
   size_t tgt_off = 0;    // fp32 [M] (CE)
+  size_t pidx_off = 0;   // int32 [M, n_part] (argmax)
   size_t total = 0;
   int64_t n_part = 0;
 };
@@ -79,7 +80,7 @@ bool use_dec(const archead_handle* h, int64_t M);
 // Several-token kernel: LDS layout for its tiles of kMidTokMax tokens, whether the
 // head shape is supported, and whether a call with M tokens runs on it.
 struct MidLds {
-  int tstr = 0, off_bias = 0, off_red = 0, off_y = 0, off_sc = 0, total = 0;
+  int tstr = 0, off_bias = 0, off_red = 0, off_y = 0, off_idx = 0, off_sc = 0, total = 0;
   int kcu = 0, kca = 0;
 };
 MidLds mid_lds(const archead_desc& d);

@@ -546,3 +546,95 @@ def test_mfma_ragged_tiles(V, d, g, M):
     bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
     assert_bf16_output(bits, o[:, :V], ref, "mfma ragged bf16")
     ph.close()
+
+
+# ------------------------------------------------------------- fused argmax
+
+def gpu_argmax(ph, x_bits):
+    idx, mx = ph.logits_argmax(torch_x(x_bits))
+    torch.cuda.synchronize()
+    return idx.cpu().numpy(), mx.cpu().numpy()
+
+
+def assert_argmax_matches_oracle(idx, ref, what):
+    """idx equals the oracle's argmax on every token whose oracle top-2 gap
+    exceeds twice the logit tolerance; returns the number of such tokens."""
+    from tests.gpu_util import LOGIT_TOL
+    top = ref.max(axis=1)
+    keep = ohead.top2_gap(ref) > 2 * LOGIT_TOL * (1 + np.abs(top))
+    bad = np.nonzero(keep & (np.asarray(idx) != ohead.argmax(ref)))[0]
+    assert bad.size == 0, f"{what}: argmax differs from the oracle on tokens {bad[:10]}"
+    return int(keep.sum())
+
+
+@pytest.mark.parametrize("cfg,M", [("tiny", 8), ("qwen_decode", 16), ("gemma", 8),
+                                   ("qwen_decode", 40)])
+def test_argmax_equals_first_argmax_of_own_logits(cfg, M):
+    """The fused argmax through each kernel (forced) is the first-index
+    argmax of the same kernel's fp32 logits, bit for bit (ties included), and
+    its max is their maximum; both agree with the oracle's argmax on every
+    token whose top-2 gap is clear of the logit tolerance."""
+    Mmax = max(max(CONFIGS[cfg]["Ms"]), M)
+    ref = cached_oracle_logits(cfg, Mmax)[:M]
+    ph = packed(cfg)
+    x = make_x(cfg, Mmax)[:M]
+    try:
+        for name in ("dec", "mid", "gemv", "tiled"):
+            ph.force_path(name)
+            say(f"argmax {cfg} M={M} forced {name}")
+            lg = gpu_logits(ph, x)
+            idx, mx = gpu_argmax(ph, x)
+            assert np.array_equal(idx, np.argmax(lg, axis=1)), f"{name}: argmax differs"
+            assert np.array_equal(mx, lg.max(axis=1)), f"{name}: max differs"
+            assert_argmax_matches_oracle(idx, ref, name)
+    finally:
+        ph.force_path("auto")
+
+
+@pytest.mark.parametrize("path", ["dec", "mid", "gemv", "tiled"])
+def test_argmax_ties_take_the_smallest_index(path):
+    """x = 0 makes every logit exactly 0: the argmax is index 0.  With a
+    one-hot x and no low-rank parts, two far-apart rows (in different
+    workgroups and tiles, identical scales and the same code 7 at the hot
+    column) share the largest logit 7 * 1.0: the argmax is the smaller of
+    the two."""
+    from oracle.layout import pack_int4, unpack_int4
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", rc=0, rr=0)
+    i0, a, b = 5, 100, h.V - 5
+    codes = unpack_int4(h.res_codes, h.d)
+    codes[[a, b], i0] = 7
+    h.res_codes = pack_int4(codes)
+    h.res_scales = h.res_scales.copy()
+    h.res_scales[a, i0 // h.g] = np.float16(1.0)
+    h.res_scales[b] = h.res_scales[a]   # identical rows of scales: identical arithmetic
+    ph = PackedHead.from_arrays(h)
+    ph.force_path(path)
+    say(f"argmax ties, {path}")
+    zeros = np.zeros((3, h.d), dtype=np.uint16)
+    idx, mx = gpu_argmax(ph, zeros)
+    assert idx.tolist() == [0, 0, 0] and mx.tolist() == [0.0, 0.0, 0.0]
+    x = np.zeros((2, h.d), dtype=np.uint16)
+    x[:, i0] = 0x3F80
+    ref = ohead.logits(h, x)
+    assert ref[0, a] == ref[0, b] == ref[0].max() == 7.0
+    idx, mx = gpu_argmax(ph, x)
+    assert idx.tolist() == [a, a]
+    if path == "tiled":   # its scale-ratio chain rounds in the last bits
+        assert np.allclose(mx, 7.0, rtol=1e-6, atol=0)
+    else:
+        assert mx.tolist() == [7.0, 7.0]
+    ph.close()
+
+
+def test_argmax_gemma_m64_against_oracle():
+    """The Gemma-shaped workload with 64 tokens (logits + argmax), through the
+    library's own kernel choice: the fused argmax equals the oracle's on
+    every token whose top-2 gap is clear of the logit tolerance."""
+    ref = cached_oracle_logits("gemma", 64)
+    ph = packed("gemma")
+    idx, mx = gpu_argmax(ph, make_x("gemma", 64))
+    n = assert_argmax_matches_oracle(idx, ref, "gemma M=64")
+    say(f"gemma M=64 argmax: {n} clear tokens agree")
+    assert n > 0
+    assert_logits_close(mx[:, None], ref.max(axis=1)[:, None], what="gemma max logit")
