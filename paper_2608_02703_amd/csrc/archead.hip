@@ -133,8 +133,8 @@ __device__ __forceinline__ float seg_sum(float v) {
 }
 
 // ------------------------------------------------ stage 1 inside the launch
-// Both decode kernels compute t = x V_c^T, x B_w^T in the same launch as the
-// head stream: the first workgroups of the grid ("producers") take one rank
+// The decode GEMV, the MFMA decode kernel and the several-token kernel
+// compute t = x V_c^T, x B_w^T in the same launch as the head stream: the first workgroups of the grid ("producers") take one rank
 // row per wave and publish each value t[m][k] together with the call's
 // epoch in one 64-bit store (agent scope, so the value and its stamp become
 // visible together on every XCD).  The other waves need t only at the end of

@@ -49,7 +49,7 @@ int lanes_per_row(const archead_desc& d);
 
 // Workspace carve-up (byte offsets, each 256-aligned).
 struct WsLayout {
-  size_t tst_off = 0;    // u64 [M, r_c + r_r] stamped t (both decode kernels)
+  size_t tst_off = 0;    // u64 [M, r_c + r_r] stamped t (decode and several-token kernels)
   // many-token (MFMA) path only:
   size_t ts_off = 0;     // bf16 [M][blocks][4][16] t split into hi, mid, lo (and 0)
   size_t gb_off = 0;     // fp32 [n_mt][slots][256] slot biases
