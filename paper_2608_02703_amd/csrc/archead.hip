@@ -1764,7 +1764,7 @@ __device__ __forceinline__ bool unroll_until(F& f) {
   return false;
 }
 
-template <int GW, bool CE>
+template <int GW, bool CE, int EK>
 __global__ __launch_bounds__(kDBlock) __attribute__((amdgpu_waves_per_eu(2)))
 void k_dec(DecArgs a) {
   static_assert(GW == 1 || GW == 2 || GW == 4, "code words per lane and group");
@@ -1950,27 +1950,33 @@ void k_dec(DecArgs a) {
     // expansion operands of the unit being computed (codes of dims
     // q 8 kc .. +8 kc - 1 of the lane's row, kc K-chunks per part) and its
     // row scales, loaded s_issue steps into the unit
-    u32x2_t eu[4], ea[4];
-    uint32_t esu = 0, esa = 0;
+    // EK (2 or 4): the most K-chunks either factor has.  With EK = 2 every
+    // load is unconditional (an absent factor's resource has no bytes, and
+    // chunks past a factor's rank are read but not used), so no load sits
+    // under a branch, which would make the wait-count pass drain the code
+    // loads in flight when the unit's operands are requested
+    u32x2_t eu[EK], ea[EK];
+    uint16_t esu = 0, esa = 0;
     auto load_exp = [&]() {
       const __amdgpu_buffer_rsrc_t ru = unit_rsrc(a.cu, cu_, uint32_t(a.rc));
       const __amdgpu_buffer_rsrc_t ra = unit_rsrc(a.ca, cu_, uint32_t(a.rr));
 #pragma unroll
-      for (int kc = 0; kc < 4; ++kc) {
-        if (kc < kcu) eu[kc] = __builtin_amdgcn_raw_buffer_load_b64(ru, voff_u, 8 * kc, 0);
-        if (kc < kca) ea[kc] = __builtin_amdgcn_raw_buffer_load_b64(ra, voff_a, 8 * kc, 0);
+      for (int kc = 0; kc < EK; ++kc) {
+        if (EK == 2 || kc < kcu) eu[kc] = __builtin_amdgcn_raw_buffer_load_b64(ru, voff_u, 8 * kc, 0);
+        if (EK == 2 || kc < kca) ea[kc] = __builtin_amdgcn_raw_buffer_load_b64(ra, voff_a, 8 * kc, 0);
       }
-      if (kcu) esu = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.su, cu_, 2u), 2 * lr, 0, 0);
-      if (kca) esa = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.sa, cu_, 2u), 2 * lr, 0, 0);
+      if (EK == 2 || kcu) esu = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.su, cu_, a.rc ? 2u : 0u), 2 * lr, 0, 0);
+      if (EK == 2 || kca) esa = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.sa, cu_, a.rr ? 2u : 0u), 2 * lr, 0, 0);
     };
     auto finish_unit = [&]() {
       if (!t_ready) fetch_t();
       if (kcu + kca > 0) {
         f32x4_t au = {0.f, 0.f, 0.f, 0.f}, aa = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kc = 0; kc < 4; ++kc) {
+        for (int kc = 0; kc < EK; ++kc) {
           if (kc < kcu) {
-            const bf16x8_t B = int8x8_to_bf16(eu[kc].x, eu[kc].y);
+            const bf16x8_t B = EK == 2 ? int8x8_to_bf16(opaque_vgpr(eu[kc].x), opaque_vgpr(eu[kc].y))
+                                       : int8x8_to_bf16(eu[kc].x, eu[kc].y);
             const lds_u8* tp = trow + 2 * (q * 8 * kcu + 8 * kc);
 #pragma unroll
             for (int p = 0; p < 3; ++p)
@@ -1978,7 +1984,8 @@ void k_dec(DecArgs a) {
                                                            B, au, 0, 0, 0);
           }
           if (kc < kca) {
-            const bf16x8_t B = int8x8_to_bf16(ea[kc].x, ea[kc].y);
+            const bf16x8_t B = EK == 2 ? int8x8_to_bf16(opaque_vgpr(ea[kc].x), opaque_vgpr(ea[kc].y))
+                                       : int8x8_to_bf16(ea[kc].x, ea[kc].y);
             const lds_u8* tp = trow + 2 * (32 * kcu + q * 8 * kca + 8 * kc);
 #pragma unroll
             for (int p = 0; p < 3; ++p)
@@ -2940,13 +2947,18 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
 
 using DecFn = void (*)(DecArgs);
 
-template <bool CE>
-DecFn dec_fn(int gw) {
+template <bool CE, int EK>
+DecFn dec_fn_ek(int gw) {
   switch (gw) {
-    case 1: return k_dec<1, CE>;
-    case 2: return k_dec<2, CE>;
-    default: return k_dec<4, CE>;
+    case 1: return k_dec<1, CE, EK>;
+    case 2: return k_dec<2, CE, EK>;
+    default: return k_dec<4, CE, EK>;
   }
+}
+
+template <bool CE>
+DecFn dec_fn(int gw, int kcu, int kca) {
+  return kcu <= 2 && kca <= 2 ? dec_fn_ek<CE, 2>(gw) : dec_fn_ek<CE, 4>(gw);
 }
 
 // One launch per pass of up to dec_tokens_per_pass tokens.  The CE form
@@ -2972,7 +2984,8 @@ archead_status launch_dec(const archead_handle* h, const void* x, int64_t M, int
   a.n_waves = gr.n_waves;
   a.n_prod_blocks = gr.prod_blocks;
   const int gw = int(d.g / 32);
-  DecFn fn = ce ? dec_fn<true>(gw) : dec_fn<false>(gw);
+  const DecLds l0 = dec_lds(d, 1);
+  DecFn fn = ce ? dec_fn<true>(gw, l0.kcu, l0.kca) : dec_fn<false>(gw, l0.kcu, l0.kca);
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
   hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
   const int64_t grid = gr.prod_blocks + gr.consumer_blocks;
