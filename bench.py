@@ -8,9 +8,10 @@ expansion, logit store) for one decode token (M=1), with every input already
 resident in HBM.  The step rotates over three copies of the packed head
 (3 x 336 MB > the 256 MB Infinity Cache), so each step streams its head from
 HBM.  The headline value is decode GB/s over the packed bytes.  Secondary
-lines: decode M=4, 16, 32 and 64, greedy decoding (the fused argmax, no
-logits written) at M=1 and 16, and the M=4096 prefill fused-CE pass (tok/s
-and the many-token kernel's MFMA throughput).
+lines: decode M=4, 16, 32 and 64, decode M=1 of the same head with 8-bit
+residual scale codes, greedy decoding (the fused argmax, no logits written)
+at M=1 and 16, and the M=4096 prefill fused-CE pass (tok/s and the
+many-token kernel's MFMA throughput).
 
 Before any timing, about 0.5 s of untimed decode steps bring the GPU's clocks
 to their sustained-load state (--clock-warmup; a cold GPU runs the first
@@ -296,6 +297,8 @@ def main():
     ap.add_argument("--prefill-steps", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
+    ap.add_argument("--no-u8", action="store_true",
+                    help="skip the decode line of the head with 8-bit residual scale codes")
     ap.add_argument("--no-dense", action="store_true",
                     help="skip the dense bf16 head context line")
     ap.add_argument("--profile", choices=["decode", "prefill"])
@@ -344,6 +347,25 @@ def main():
         res[M] = (ms, kern_ms, kern_med)
         log(f"decode M={M}: {ms * 1e3:.1f} us/step, head kernel {kern_ms * 1e3:.1f} us "
             f"(median {kern_med * 1e3:.1f}), {pbytes / ms / 1e6:.0f} GB/s over packed bytes")
+
+    # the same head with 8-bit residual scale codes (fp16 row scale): fewer
+    # packed bytes per decode step
+    u8 = None
+    if not args.no_u8:
+        h8 = make_head(cfg, scales="u8")
+        b8 = head_bytes(h8)
+        heads8 = upload_copies(h8, N_COPIES)
+        torch.cuda.synchronize()
+        clock_warmup(heads8, x_all[:1], 0.2)
+        ms8, k8, _ = time_decode(heads8, x_all[:1], args.steps, args.warmup)
+        u8 = {"us_per_step": round(ms8 * 1e3, 2), "kernel_us": round(k8 * 1e3, 2),
+              "packed_bytes": b8, "gbs_packed": round(b8 / ms8 / 1e6, 1)}
+        log(f"decode M=1, 8-bit scale codes: {ms8 * 1e3:.1f} us/step, {b8 / 1e6:.1f} MB packed, "
+            f"{b8 / ms8 / 1e6:.0f} GB/s")
+        for hd in heads8:
+            hd.close()
+        del heads8
+        torch.cuda.empty_cache()
 
     # greedy decoding: the fused argmax step (no [M, V] logits written)
     greedy = {}
@@ -429,6 +451,7 @@ def main():
                             "gbs_packed": round(pbytes / v[0] / 1e6, 1)}
                    for M, v in res.items()},
         "greedy_argmax": greedy,
+        "decode_u8_scales": u8,
         "prefill": prefill,
         "dense_bf16_head": dense,
     }

@@ -69,7 +69,7 @@
 extern "C" {
 #endif
 
-#define ARCHEAD_ABI_VERSION 1u
+#define ARCHEAD_ABI_VERSION 2u
 
 typedef enum archead_status {
   ARCHEAD_OK = 0,
@@ -86,7 +86,8 @@ typedef enum archead_dtype {
   ARCHEAD_F16 = 2,
   ARCHEAD_I32 = 3,
   ARCHEAD_I64 = 4,
-  ARCHEAD_I8 = 5
+  ARCHEAD_I8 = 5,
+  ARCHEAD_U8 = 6
 } archead_dtype;
 
 typedef enum archead_int4_encoding { ARCHEAD_INT4_V1 = 1 } archead_int4_encoding;
@@ -104,8 +105,17 @@ typedef enum archead_op {
  *   INT4, r_r = 0 is the "core only" ablation);
  *   g_v, g_b: group length along d of the core_v / corr_b scales, dividing d
  *   and a multiple of 32 (d = one scale per row);
- *   int4_encoding = ARCHEAD_INT4_V1, scale_dtype = ARCHEAD_F16,
- *   factor_dtype = ARCHEAD_I8. */
+ *   int4_encoding = ARCHEAD_INT4_V1, factor_dtype = ARCHEAD_I8;
+ *   scale_dtype: the residual group scales s[v, j] (the "quantized group
+ *   scales" of the paper's packed state dictionary, Section 3.3 and its
+ *   packed-buffer appendix, which leave their format open):
+ *     ARCHEAD_F16: res_scales holds s as fp16 [V, d/g];
+ *     ARCHEAD_U8:  res_scales holds 8-bit codes q [V, d/g] (uint8) and
+ *                  res_row_scales one fp16 scale rs per vocabulary row [V],
+ *                  s[v, j] = rs[v] * q[v, j] (exact in fp32).  One byte of
+ *                  scale per group is the storage the paper's reported head
+ *                  sizes imply.  Served by the decode GEMV and the tiled
+ *                  MFMA kernel (archead_logits). */
 typedef struct archead_desc {
   uint32_t abi_version; /* ARCHEAD_ABI_VERSION */
   int64_t V, d, g;
@@ -116,9 +126,10 @@ typedef struct archead_desc {
   int32_t factor_dtype;
 } archead_desc;
 
-/* Device pointers to the ten packed buffers (layouts above).  res_codes must
+/* Device pointers to the packed buffers (layouts above).  res_codes must
  * be 16-byte aligned, fp16 buffers 2-byte aligned.  Pointers of an absent
- * component (rank 0) may be NULL. */
+ * component (rank 0) may be NULL; res_row_scales is required with
+ * ARCHEAD_U8 scales and ignored otherwise. */
 typedef struct archead_ptrs {
   const void* res_codes;
   const void* res_scales;
@@ -130,6 +141,7 @@ typedef struct archead_ptrs {
   const void* corr_a_scale;
   const void* corr_b;
   const void* corr_b_scale;
+  const void* res_row_scales;
 } archead_ptrs;
 
 typedef struct archead_handle archead_handle;

@@ -24,13 +24,15 @@ def packed_bytes(V: int, d: int, g: int, rc: int, rr: int, gV: int = None,
                  gB: int = None, *, res_bits: int = 4,
                  res_scale_bits: int = 16, core_u_bits: int = 8,
                  core_v_bits: int = 8, corr_bits: int = 8,
-                 factor_scale_bytes: int = 2) -> int:
-    """Sum of numel x element size over the registered buffers."""
+                 factor_scale_bytes: int = 2, res_row_scale_bytes: int = 0) -> int:
+    """Sum of numel x element size over the registered buffers
+    (res_row_scale_bytes: per-row scale of 8-bit residual scale codes)."""
     gV = d if gV is None else gV
     gB = d if gB is None else gB
     buffers = [
         _bits_to_bytes(V * d, res_bits),            # residual codes
         _bits_to_bytes(V * (d // g), res_scale_bits),  # residual scales
+        V * res_row_scale_bytes,                    # their row scales (8-bit codes)
     ]
     if rc:
         buffers += [
@@ -55,4 +57,7 @@ def dense_bf16_bytes(V: int, d: int) -> int:
 
 def head_bytes(h) -> int:
     """packed_bytes of a head object carrying the shape attributes."""
+    if getattr(h, "res_scales", None) is not None and h.res_scales.dtype == "uint8":
+        return packed_bytes(h.V, h.d, h.g, h.rc, h.rr, h.gV, h.gB, res_scale_bits=8,
+                            res_row_scale_bytes=2)
     return packed_bytes(h.V, h.d, h.g, h.rc, h.rr, h.gV, h.gB)

@@ -15,6 +15,12 @@ In buffer terms (names of the packed buffers, shapes as in the layout notes):
   W_corr[v, i] = sum_k (s_A[v] cA[v, k]) (s_B[k, i // gB] cB[k, i])
   W_hat = W_res + W_core + W_corr,    logits[m, v] = sum_i x[m, i] W_hat[v, i]
 
+The residual group scales s_res are stored either as fp16 or, the paper's
+"quantized group scales" (packed-buffer table), as 8-bit codes q with one
+fp16 scale rs per vocabulary row: s_res[v, j] = rs[v] * q[v, j] (a uint8
+res_scales array plus res_row_scales [V]; the format is this library's
+reading, the paper leaves it open).
+
 A rank of zero means the component is absent (the paper's "core only" and
 "Group INT4" ablations).  The head object is any object with the attributes
 V, d, g, rc, rr, gV, gB and the ten buffers (res_codes, res_scales, core_u,
@@ -36,8 +42,17 @@ ROW_CHUNK = 4096
 def residual_rows(h, v0: int, v1: int) -> np.ndarray:
     """W_res for vocabulary rows [v0, v1): s_res[v, i // g] * c[v, i]."""
     c = unpack_int4(h.res_codes[v0:v1], h.d).astype(np.float64)
-    s = fp16_to_f64(h.res_scales[v0:v1])                 # [n, d/g]
-    return c * np.repeat(s, h.g, axis=1)
+    return c * np.repeat(residual_scales(h, v0, v1), h.g, axis=1)
+
+
+def residual_scales(h, v0: int, v1: int) -> np.ndarray:
+    """s_res for rows [v0, v1) as float64 [n, d/g]: the fp16 values, or
+    rs[v] * q[v, j] for 8-bit codes."""
+    sc = np.asarray(h.res_scales[v0:v1])
+    if sc.dtype == np.uint8:
+        rs = fp16_to_f64(np.asarray(h.res_row_scales)[v0:v1])
+        return rs[:, None] * sc.astype(np.float64)
+    return fp16_to_f64(sc)
 
 
 def left_factor(codes, scales) -> np.ndarray:
@@ -112,6 +127,8 @@ def _gather_rows(h, ids) -> np.ndarray:
     for k in ("res_codes", "res_scales", "core_u", "core_u_scale", "corr_a",
               "corr_a_scale"):
         setattr(s, k, np.asarray(getattr(h, k))[ids])
+    if getattr(h, "res_row_scales", None) is not None:
+        s.res_row_scales = np.asarray(h.res_row_scales)[ids]
     return dense_rows(s, 0, ids.size)
 
 

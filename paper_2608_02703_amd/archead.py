@@ -16,9 +16,9 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libarchead.so")
 HOST_LIB_PATH = os.path.join(_PKG, "libarchead_host.so")
 
-ABI_VERSION = 1
+ABI_VERSION = 2
 OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
-F32, BF16, F16, I32, I64, I8 = range(6)
+F32, BF16, F16, I32, I64, I8, U8 = range(7)
 INT4_V1 = 1
 OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX = 0, 1, 2
 
@@ -47,7 +47,8 @@ class Desc(ctypes.Structure):
 class Ptrs(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
-        "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale")]
+        "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale",
+        "res_row_scales")]
 
 
 _SIGS = {
@@ -167,11 +168,14 @@ def _ptr(t) -> int:
 class PackedHead:
     """A packed head resident on the current GPU plus its library handle.
 
-    ``buffers`` maps the ten buffer names to torch tensors on the device (the
-    caller keeps ownership; the handle only borrows them)."""
+    ``buffers`` maps the buffer names to torch tensors on the device (the
+    caller keeps ownership; the handle only borrows them).  A uint8
+    ``res_scales`` selects 8-bit group scale codes, with ``res_row_scales``
+    (fp16 [V]) the per-row scale."""
 
     BUFFERS = ("res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
-               "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale")
+               "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale",
+               "res_row_scales")
 
     def __init__(self, V, d, g, rc, rr, buffers: dict, gV=None, gB=None):
         import torch  # noqa: F401  (device memory only)
@@ -179,7 +183,9 @@ class PackedHead:
         self.gV = d if gV is None else gV
         self.gB = d if gB is None else gB
         self.buffers = buffers
-        self.desc = Desc.make(V, d, g, rc, rr, self.gV, self.gB)
+        sc = buffers.get("res_scales")
+        u8 = sc is not None and str(sc.dtype) == "torch.uint8"
+        self.desc = Desc.make(V, d, g, rc, rr, self.gV, self.gB, scale_dtype=U8 if u8 else F16)
         self.ptrs = Ptrs(*[_ptr(buffers.get(n)) for n in self.BUFFERS])
         self._lib = lib()
         h = ctypes.c_void_p()
@@ -195,7 +201,11 @@ class PackedHead:
         import torch
         bufs = {}
         for n in cls.BUFFERS:
-            a = np.ascontiguousarray(getattr(h, n))
+            a = getattr(h, n, None)
+            if a is None:
+                bufs[n] = None
+                continue
+            a = np.ascontiguousarray(a)
             if a.size == 0:
                 bufs[n] = None
                 continue

@@ -271,6 +271,7 @@ struct GemvArgs {
   const uint16_t* sa;
   const uint16_t* x;
   int64_t ldx;
+  const uint16_t* rrs;  // fp16 row scales of 8-bit residual scale codes (else unused)
   Stage1Ops s1;    // t of the pass's tokens, computed in the launch
   int n_prod_blocks;  // leading workgroups that compute t
   int64_t tok0;    // first token of this pass
@@ -368,6 +369,7 @@ __device__ __forceinline__ int row_of_lane(int lane) {
 template <int RB, int KD>
 struct ExpOps {
   uint32_t c[RB][KD];   // four int8 codes
+  uint16_t rsc[RB];     // fp16 row scale of 8-bit residual scale codes (unused otherwise)
   uint16_t s[RB][KD];   // fp16 bit pattern of the row scale (kept 16-bit: no extension op right after the load)
 };
 
@@ -407,7 +409,7 @@ __device__ __forceinline__ void apply_expansion(float (&acc)[RB][TOK], const Exp
 }
 
 // One d-iteration of a step: RB rows x one 16-byte chunk per lane.
-template <int TOK, int RB>
+template <int TOK, int RB, bool SC8>
 __device__ __forceinline__ void gemv_chunk(float (&acc)[RB][TOK], const uint4 (&q)[RB],
                                            const uint32_t (&sc)[RB], const uint16_t* sx,
                                            const float* sxb, int d, int C, int c,
@@ -429,7 +431,9 @@ __device__ __forceinline__ void gemv_chunk(float (&acc)[RB][TOK], const uint4 (&
   }
 #pragma unroll
   for (int rb = 0; rb < RB; ++rb) {
-    const float s = f16_to_f32(uint16_t(sc[rb]));
+    // the group scale: fp16, or an 8-bit code (the row scale is applied at
+    // the step's end)
+    const float s = SC8 ? float(sc[rb] & 0xffu) : f16_to_f32(uint16_t(sc[rb]));
     const uint32_t w4[4] = {q[rb].x, q[rb].y, q[rb].z, q[rb].w};
     uint32_t pr[16];
 #pragma unroll
@@ -536,7 +540,7 @@ __device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvA
 #ifndef ARCHEAD_GEMV_WAVES_NARROW
 #define ARCHEAD_GEMV_WAVES_NARROW 2   // segments narrower than the wave
 #endif
-template <int TOK, int LPR, bool CE>
+template <int TOK, int LPR, bool CE, bool SC8>
 __global__ __launch_bounds__(kBlock)
 __attribute__((amdgpu_waves_per_eu(TOK == 1 ? (LPR >= 64 ? ARCHEAD_GEMV_WAVES : ARCHEAD_GEMV_WAVES_NARROW) : 1)))
 void k_gemv(GemvArgs a) {
@@ -658,14 +662,15 @@ void k_gemv(GemvArgs a) {
     // loads in flight)
     constexpr int KD = ExpLanes<LPR>::KD;
     const int rc4 = a.rc / 4, R4 = R / 4;
+    constexpr uint32_t ESZ = SC8 ? 1u : 2u;   // bytes per group scale
     auto load = [&](int64_t stp, int itx, uint4 (&q)[RB], uint32_t (&sc)[RB]) {
       const uint64_t cbytes = uint64_t(a.V - stp * WR) * rowbytes;
-      const uint64_t sbytes = uint64_t(a.V - stp * WR) * ngrp * 2u;
+      const uint64_t sbytes = uint64_t(a.V - stp * WR) * ngrp * ESZ;
       const __amdgpu_buffer_rsrc_t rc_ = __builtin_amdgcn_make_buffer_rsrc(
           const_cast<uint8_t*>(a.codes + uint64_t(stp) * WR * rowbytes), 0,
           int(cbytes < 0xffffffffull ? cbytes : 0xffffffffull), kBufferWord3);
       const __amdgpu_buffer_rsrc_t rs_ = __builtin_amdgcn_make_buffer_rsrc(
-          const_cast<uint16_t*>(a.rs + uint64_t(stp) * WR * ngrp), 0,
+          const_cast<uint8_t*>(reinterpret_cast<const uint8_t*>(a.rs) + uint64_t(stp) * WR * ngrp * ESZ), 0,
           int(sbytes < 0xffffffffull ? sbytes : 0xffffffffull), kBufferWord3);
       const int itoff = itx * LPR * 16;
 #pragma unroll
@@ -675,13 +680,14 @@ void k_gemv(GemvArgs a) {
         q[rb] = make_uint4(v.x, v.y, v.z, v.w);
       }
       // a step's group scales come with its first iteration: lane sl of a
-      // segment takes groups 2 sl, 2 sl + 1 of each of its rows (4 bytes);
-      // the lanes that need them fetch them with ds_bpermute
+      // segment takes groups 2 sl, 2 sl + 1 (fp16) or 4 sl .. 4 sl + 3 (8-bit
+      // codes) of each of its rows (4 bytes); the lanes that need them fetch
+      // them with ds_bpermute
       if (itx == 0) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb)
           sc[rb] = __builtin_amdgcn_raw_buffer_load_b32(
-              rs_, int(svoff * 2u + uint32_t(sl) * 4u), int(uint32_t(rb * SEG) * ngrp * 2u), 0);
+              rs_, int(svoff * ESZ + uint32_t(sl) * 4u), int(uint32_t(rb * SEG) * ngrp * ESZ), 0);
       }
     };
     // expansion operands of step stp (one buffer: the next step's operands
@@ -707,6 +713,10 @@ void k_gemv(GemvArgs a) {
           e.c[rb][kd] = *reinterpret_cast<const uint32_t*>(cb);
           e.s[rb][kd] = *sp;
         }
+      }
+      if constexpr (SC8) {
+#pragma unroll
+        for (int rb = 0; rb < RB; ++rb) e.rsc[rb] = a.rrs[v0 + rb * SEG];
       }
     };
     uint4 q[NB][RB];
@@ -752,16 +762,24 @@ void k_gemv(GemvArgs a) {
       // group of this lane's chunk and the segment lane holding its scale
       const uint32_t c = uint32_t(cit * LPR + sl);
       const uint32_t grp = a.gshift >= 0 ? (c >> a.gshift) : (c * 32u) / uint32_t(a.g);
-      const int src = 4 * (seg * LPR + int(grp >> 1));
-      const uint32_t hsh = (grp & 1u) * 16u;
+      const int src = 4 * (seg * LPR + int(SC8 ? grp >> 2 : grp >> 1));
+      const uint32_t hsh = SC8 ? (grp & 3u) * 8u : (grp & 1u) * 16u;
       uint32_t scv[RB];
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb)
         scv[rb] = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(ssc[rb]))) >> hsh;
-      gemv_chunk<TOK, RB>(acc, q[j], scv, sx, sxb, d, C, int(c), kMask, kMagic);
+      gemv_chunk<TOK, RB, SC8>(acc, q[j], scv, sx, sxb, d, C, int(c), kMask, kMagic);
       if (cit == a.nit - 1) {
         // the step's rank-r expansion, then the next step's operands
         if (!t_ready) fetch_t();
+        if constexpr (SC8) {   // the residual in units of the row scales
+#pragma unroll
+          for (int rb = 0; rb < RB; ++rb) {
+            const float f = f16_to_f32(e.rsc[rb]);
+#pragma unroll
+            for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] *= f;
+          }
+        }
         apply_expansion<TOK, RB, KD, LPR>(acc, e, st, R, sl);
         load_exp(more ? nstep : cstep, e);
         gemv_epilogue<TOK, LPR, RB, CE, false>(acc, a, cstep * WR, uint32_t(WR - 1), seg, sl,
@@ -807,11 +825,22 @@ void k_gemv(GemvArgs a) {
         uint32_t r = uint32_t(seg + rb * SEG);
         r = r < lim ? r : lim;
         q[rb] = load_stream16(cbase + uint64_t(r) * rowbytes + c * 16u);
-        sc[rb] = sbase[uint64_t(r) * ngrp + grp];
+        sc[rb] = SC8 ? reinterpret_cast<const uint8_t*>(a.rs)[uint64_t(row0 + r) * ngrp + grp]
+                     : sbase[uint64_t(r) * ngrp + grp];
       }
-      gemv_chunk<TOK, RB>(acc, q, sc, sx, sxb, d, C, int(c), kMask, kMagic);
+      gemv_chunk<TOK, RB, SC8>(acc, q, sc, sx, sxb, d, C, int(c), kMask, kMagic);
     }
     if (!t_ready) fetch_t();
+    if constexpr (SC8) {
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb) {
+        uint32_t r = uint32_t(seg + rb * SEG);
+        r = r < lim ? r : lim;
+        const float f = f16_to_f32(a.rrs[row0 + r]);
+#pragma unroll
+        for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] *= f;
+      }
+    }
     gemv_epilogue<TOK, LPR, RB, CE, true>(acc, a, row0, lim, seg, sl, lane, my_row, writer, st,
                                           ce);
   }
@@ -1353,6 +1382,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 // block of 16 stored twice.
 struct PrepArgs {
   const uint16_t* rs;
+  const uint16_t* rrs;   // row scales of 8-bit group scale codes, or null (fp16 scales)
   const uint16_t* su;
   const uint16_t* sa;
   int64_t V;
@@ -1384,11 +1414,19 @@ __global__ __launch_bounds__(kBlock) void k_prep(PrepArgs a) {
     const int64_t vt = e / kTN, c = e % kTN;
     const int64_t v = vt * kTN + c < a.V ? vt * kTN + c : a.V - 1;
     const uint16_t* src = a.rs + v * a.ngrp;
+    const uint8_t* src8 = reinterpret_cast<const uint8_t*>(a.rs) + v * a.ngrp;
+    const float rsv = a.rrs ? f16_to_f32(a.rrs[v]) : 0.f;
     float* dst = a.ratio + vt * int64_t(a.nslot) * kTN + c;
     float prev = 0.f;
     int k = 0;
     for (; k < a.ngrp; ++k) {
-      const float s = nz_scale(src[k]);
+      float s;
+      if (a.rrs) {   // rs * q, exact in fp32
+        s = rsv * float(src8[k]);
+        s = s == 0.f ? kZeroScale : s;
+      } else {
+        s = nz_scale(src[k]);
+      }
       dst[int64_t(k) * kTN] = k ? prev / s : 0.f;
       prev = s;
     }
@@ -2600,27 +2638,33 @@ void k_mid(MidArgs a) {
 // ------------------------------------------------------------ dispatch
 using GemvFn = void (*)(GemvArgs);
 
-template <int TOK, bool CE>
+template <int TOK, bool CE, bool SC8>
 GemvFn gemv_by_lpr(int lpr) {
   switch (lpr) {
-    case 1: return k_gemv<TOK, 1, CE>;
-    case 2: return k_gemv<TOK, 2, CE>;
-    case 4: return k_gemv<TOK, 4, CE>;
-    case 8: return k_gemv<TOK, 8, CE>;
-    case 16: return k_gemv<TOK, 16, CE>;
-    case 32: return k_gemv<TOK, 32, CE>;
-    default: return k_gemv<TOK, 64, CE>;
+    case 1: return k_gemv<TOK, 1, CE, SC8>;
+    case 2: return k_gemv<TOK, 2, CE, SC8>;
+    case 4: return k_gemv<TOK, 4, CE, SC8>;
+    case 8: return k_gemv<TOK, 8, CE, SC8>;
+    case 16: return k_gemv<TOK, 16, CE, SC8>;
+    case 32: return k_gemv<TOK, 32, CE, SC8>;
+    default: return k_gemv<TOK, 64, CE, SC8>;
   }
 }
 
-template <bool CE>
-GemvFn gemv_fn(int tok, int lpr) {
+template <bool CE, bool SC8>
+GemvFn gemv_fn_sc(int tok, int lpr) {
   switch (tok) {
-    case 1: return gemv_by_lpr<1, CE>(lpr);
-    case 2: return gemv_by_lpr<2, CE>(lpr);
-    case 3: return gemv_by_lpr<3, CE>(lpr);
-    default: return gemv_by_lpr<4, CE>(lpr);
+    case 1: return gemv_by_lpr<1, CE, SC8>(lpr);
+    case 2: return gemv_by_lpr<2, CE, SC8>(lpr);
+    case 3: return gemv_by_lpr<3, CE, SC8>(lpr);
+    default: return gemv_by_lpr<4, CE, SC8>(lpr);
   }
+}
+
+// the variant for the head's residual scale format (8-bit codes or fp16)
+template <bool CE>
+GemvFn gemv_fn(int tok, int lpr, bool sc8) {
+  return sc8 ? gemv_fn_sc<CE, true>(tok, lpr) : gemv_fn_sc<CE, false>(tok, lpr);
 }
 
 size_t gemv_lds_bytes(const archead_desc& d, int tok) {
@@ -2645,14 +2689,15 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 namespace archead {
 
 int64_t gemv_grid(const archead_handle* h, int tok, bool ce) {
-  const int slot = (ce ? 8 : 0) + tok;
+  const bool sc8 = h->desc.scale_dtype == ARCHEAD_U8;
+  const int slot = (sc8 ? 16 : 0) + (ce ? 8 : 0) + tok;
   archead_handle* mh = const_cast<archead_handle*>(h);
   int cached = mh->grid_cache[slot].load(std::memory_order_relaxed);
   const int64_t steps = (h->desc.V + gemv_rows_per_step(h->desc) - 1) / gemv_rows_per_step(h->desc);
   const int64_t max_blocks = (steps + kWaves - 1) / kWaves;
   if (cached <= 0) {
     const int lpr = lanes_per_row(h->desc);
-    GemvFn fn = ce ? gemv_fn<true>(tok, lpr) : gemv_fn<false>(tok, lpr);
+    GemvFn fn = ce ? gemv_fn<true>(tok, lpr, sc8) : gemv_fn<false>(tok, lpr, sc8);
     int nb = 0;
     const size_t lds = gemv_lds_bytes(h->desc, tok);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, reinterpret_cast<const void*>(fn),
@@ -2805,6 +2850,8 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
   const int nch_u = exp_chunks(d.r_c), nch = nch_u + exp_chunks(d.r_r);
   PrepArgs p;
   p.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
+  p.rrs = d.scale_dtype == ARCHEAD_U8 ? static_cast<const uint16_t*>(h->ptrs.res_row_scales)
+                                      : nullptr;
   p.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
   p.sa = static_cast<const uint16_t*>(h->ptrs.corr_a_scale);
   p.V = d.V;
@@ -2900,9 +2947,13 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, uint64_t
   const int lpr = lanes_per_row(d);
   const int kd = lpr >= 64 ? 1 : 2;   // ExpLanes<LPR>::KD
   const int64_t ngrp = d.d / d.g;
+  const bool sc8 = d.scale_dtype == ARCHEAD_U8;
+  // a step's scales: 2 (fp16) or 4 (8-bit codes) groups per segment lane
+  const int64_t gpl = sc8 ? 4 : 2;
   a.fast = d.r_c % 4 == 0 && d.r_r % 4 == 0 && (d.r_c + d.r_r) / 4 <= int64_t(kd) * lpr &&
            (d.r_c == 0 || aligned(h->ptrs.core_u, 4)) &&
-           (d.r_r == 0 || aligned(h->ptrs.corr_a, 4)) && ngrp % 2 == 0 && ngrp <= 2 * lpr;
+           (d.r_r == 0 || aligned(h->ptrs.corr_a, 4)) && ngrp % gpl == 0 && ngrp <= gpl * lpr;
+  a.rrs = sc8 ? static_cast<const uint16_t*>(h->ptrs.res_row_scales) : a.rs;
   // an absent factor reads the (valid, 16-byte aligned) residual buffers with
   // stride 0 instead; its contribution is masked to zero in the kernel
   a.cu_stride = d.r_c; a.su_stride = d.r_c ? 1 : 0;
@@ -2926,7 +2977,8 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
   hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
   for (int64_t m0 = 0; m0 < M; m0 += 4) {
     const int tok = int(M - m0 < 4 ? M - m0 : 4);
-    GemvFn fn = ce ? gemv_fn<true>(tok, lpr) : gemv_fn<false>(tok, lpr);
+    const bool sc8 = h->desc.scale_dtype == ARCHEAD_U8;
+    GemvFn fn = ce ? gemv_fn<true>(tok, lpr, sc8) : gemv_fn<false>(tok, lpr, sc8);
     const int64_t grid = a.n_prod_blocks + (forced_grid > 0 ? forced_grid : gemv_grid(h, tok, ce));
     a.tok0 = m0;
     const size_t lds = gemv_lds_bytes(h->desc, tok);
@@ -3185,13 +3237,17 @@ archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs
   const archead_desc& d = *desc;
   if (!ptrs->res_codes || !ptrs->res_scales)
     return fail(ARCHEAD_E_INVALID_ARG, "res_codes and res_scales are required");
+  if (d.scale_dtype == ARCHEAD_U8 && (!ptrs->res_row_scales || !aligned(ptrs->res_row_scales, 2)))
+    return fail(ARCHEAD_E_INVALID_ARG,
+                "8-bit scale codes need res_row_scales (fp16 [V], 2-byte aligned)");
   if (d.r_c && (!ptrs->core_u || !ptrs->core_u_scale || !ptrs->core_v || !ptrs->core_v_scale))
     return fail(ARCHEAD_E_INVALID_ARG, "r_c > 0 needs core_u, core_u_scale, core_v, core_v_scale");
   if (d.r_r && (!ptrs->corr_a || !ptrs->corr_a_scale || !ptrs->corr_b || !ptrs->corr_b_scale))
     return fail(ARCHEAD_E_INVALID_ARG, "r_r > 0 needs corr_a, corr_a_scale, corr_b, corr_b_scale");
   if (!aligned(ptrs->res_codes, 16)) return fail(ARCHEAD_E_MISALIGNED, "res_codes must be 16-byte aligned");
-  const void* f16s[] = {ptrs->res_scales, ptrs->core_u_scale, ptrs->core_v_scale,
-                        ptrs->corr_a_scale, ptrs->corr_b_scale};
+  const void* f16s[] = {d.scale_dtype == ARCHEAD_F16 ? ptrs->res_scales : nullptr,
+                        ptrs->core_u_scale, ptrs->core_v_scale, ptrs->corr_a_scale,
+                        ptrs->corr_b_scale};
   for (const void* p : f16s)
     if (p && !aligned(p, 2)) return fail(ARCHEAD_E_MISALIGNED, "fp16 scales must be 2-byte aligned");
   if ((ptrs->core_v && !aligned(ptrs->core_v, 16)) || (ptrs->corr_b && !aligned(ptrs->corr_b, 16)))

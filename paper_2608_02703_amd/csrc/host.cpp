@@ -57,6 +57,7 @@ int dec_tokens_per_pass(const archead_desc& d) {
   // at most 64 groups per row (two scale loads per unit); factor code rows
   // read as dwords; at most 128 dimensions per factor (4 K-chunks)
   if (d.g != 32 && d.g != 64 && d.g != 128) return 0;
+  if (d.scale_dtype != ARCHEAD_F16) return 0;   // reads fp16 group scales
   if ((d.d / d.g) % 4 || d.d / d.g > 64) return 0;
   if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return 0;
   // byte offsets of the code buffer stay 32-bit
@@ -94,6 +95,7 @@ bool mid_supported(const archead_desc& d) {
   // at most 64 groups per row (a unit's scales staged in LDS), factor code rows
   // read as dwords, at most 128 dimensions per factor (4 K-chunks)
   if (d.g != 64 && d.g != 128) return false;
+  if (d.scale_dtype != ARCHEAD_F16) return false;   // reads fp16 group scales
   if (d.d % (2 * kMidWindow) || d.d / d.g > 64) return false;
   if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return false;
   return mid_lds(d).total <= kLdsBytes;
@@ -170,8 +172,8 @@ archead_status archead_validate_desc(const archead_desc* p) {
   }
   if (d.int4_encoding != ARCHEAD_INT4_V1)
     return fail(ARCHEAD_E_INVALID_ARG, "unknown int4_encoding %d", d.int4_encoding);
-  if (d.scale_dtype != ARCHEAD_F16)
-    return fail(ARCHEAD_E_UNSUPPORTED, "scale_dtype must be ARCHEAD_F16");
+  if (d.scale_dtype != ARCHEAD_F16 && d.scale_dtype != ARCHEAD_U8)
+    return fail(ARCHEAD_E_UNSUPPORTED, "scale_dtype must be ARCHEAD_F16 or ARCHEAD_U8");
   if (d.factor_dtype != ARCHEAD_I8)
     return fail(ARCHEAD_E_UNSUPPORTED, "factor_dtype must be ARCHEAD_I8");
   return ARCHEAD_OK;
@@ -181,7 +183,11 @@ uint64_t archead_packed_bytes(const archead_desc* p) {
   if (archead_validate_desc(p) != ARCHEAD_OK) return 0;
   const archead_desc& d = *p;
   const uint64_t V = d.V, D = d.d;
-  uint64_t b = V * D / 2 + V * (D / d.g) * 2;                 // residual codes + scales
+  uint64_t b = V * D / 2;                                     // residual codes
+  if (d.scale_dtype == ARCHEAD_U8)
+    b += V * (D / d.g) + V * 2;                                // 8-bit group codes + fp16 row scales
+  else
+    b += V * (D / d.g) * 2;                                    // fp16 group scales
   if (d.r_c) b += V * d.r_c + V * 2 + d.r_c * D + d.r_c * (D / d.g_v) * 2;
   if (d.r_r) b += V * d.r_r + V * 2 + d.r_r * D + d.r_r * (D / d.g_b) * 2;
   return b;

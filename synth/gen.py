@@ -100,6 +100,7 @@ class HeadArrays:
     corr_a_scale: np.ndarray
     corr_b: np.ndarray
     corr_b_scale: np.ndarray
+    res_row_scales: Optional[np.ndarray] = None   # fp16 [V] with uint8 res_scales
 
     BUFFERS = ("res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
                "core_v_scale", "corr_a", "corr_a_scale", "corr_b",
@@ -122,8 +123,11 @@ def _int8_uniform(rng, shape) -> np.ndarray:
 
 def make_head(cfg="tiny", draw: int = 0, **over) -> HeadArrays:
     """Draw a packed head.  ``over`` may replace V, d, g, rc, rr, gV, gB (for
-    ragged and degenerate shapes); gV/gB default to d (one scale per row)."""
+    ragged and degenerate shapes); gV/gB default to d (one scale per row).
+    ``scales="u8"`` stores the residual group scales as 8-bit codes with an
+    fp16 scale per row (the same draws rounded to rs * q, rs = max / 255)."""
     c = _cfg(cfg)
+    scales = over.pop("scales", "f16")
     unknown = set(over) - {"V", "d", "g", "rc", "rr", "gV", "gB", "cfg_id"}
     if unknown:
         raise TypeError(f"unknown head overrides {sorted(unknown)}")
@@ -148,9 +152,19 @@ def make_head(cfg="tiny", draw: int = 0, **over) -> HeadArrays:
     corr_b = _int8_uniform(r("corr_b"), (rr, d))
     corr_b_scale = _fp16_abs_normal(r("corr_b_scale"), FACTOR_SCALE_SIGMA,
                                     (rr, d // gB))
+    res_row_scales = None
+    if scales == "u8":
+        top = res_scales.astype(np.float64).max(axis=1)
+        res_row_scales = (top / 255.0).astype(np.float16)
+        rs = res_row_scales.astype(np.float64)
+        rs_safe = np.where(rs > 0, rs, 1.0)
+        q = np.rint(res_scales.astype(np.float64) / rs_safe[:, None])
+        res_scales = np.clip(q, 0, 255).astype(np.uint8)
+    elif scales != "f16":
+        raise ValueError(f"scales must be 'f16' or 'u8', not {scales!r}")
     return HeadArrays(V, d, g, rc, rr, gV, gB, res_codes, res_scales, core_u,
                       core_u_scale, core_v, core_v_scale, corr_a, corr_a_scale,
-                      corr_b, corr_b_scale)
+                      corr_b, corr_b_scale, res_row_scales)
 
 
 @functools.lru_cache(maxsize=2)

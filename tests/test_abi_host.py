@@ -56,7 +56,9 @@ def _desc(**kw):
 
 @pytest.mark.parametrize("kw,status", [
     ({}, ab.OK),
-    (dict(abi=2), ab.E_INVALID_ARG),
+    (dict(abi=1), ab.E_INVALID_ARG),           # another ABI version
+    (dict(abi=3), ab.E_INVALID_ARG),
+    (dict(scale_dtype=ab.U8), ab.OK),          # 8-bit group scale codes
     (dict(V=0), ab.E_INVALID_ARG),
     (dict(d=0), ab.E_INVALID_ARG),
     (dict(g=48), ab.E_INVALID_ARG),            # not a multiple of 32
@@ -187,3 +189,17 @@ def test_host_only_build_agrees(tmp_path):
     assert ab.packed_bytes(desc, H) == ab.packed_bytes(desc, ab.lib())
     codes = np.random.default_rng(0).integers(-8, 8, size=(3, 64)).astype(np.int8)
     assert np.array_equal(ab.pack_int4(codes, H), ab.pack_int4(codes, ab.lib()))
+
+
+@pytest.mark.parametrize("V,d,g,rc,rr", [(151936, 4096, 128, 64, 32), (1000, 512, 64, 0, 0),
+                                        (8191, 2560, 128, 16, 0)])
+def test_packed_bytes_with_8bit_scales(L, V, d, g, rc, rr):
+    """8-bit residual scale codes: one byte per group plus an fp16 scale per
+    row, as the oracle counts them; at the Qwen shape the head shrinks from
+    336,475,840 to 331,917,760 bytes."""
+    desc = ab.Desc.make(V, d, g, rc, rr, scale_dtype=ab.U8)
+    got = ab.packed_bytes(desc, L)
+    assert got == obytes.packed_bytes(V, d, g, rc, rr, res_scale_bits=8, res_row_scale_bytes=2)
+    if (V, d, g, rc, rr) == (151936, 4096, 128, 64, 32):
+        assert got == 336_475_840 - V * (d // g) * 2 + V * (d // g) + 2 * V == 331_917_760
+

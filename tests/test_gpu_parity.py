@@ -638,3 +638,66 @@ def test_argmax_gemma_m64_against_oracle():
     say(f"gemma M=64 argmax: {n} clear tokens agree")
     assert n > 0
     assert_logits_close(mx[:, None], ref.max(axis=1)[:, None], what="gemma max logit")
+
+
+# ------------------------------------------------------ 8-bit scale codes
+
+@pytest.mark.parametrize("path", ["gemv", "tiled", "auto"])
+def test_8bit_scale_codes_tiny(path):
+    """Residual group scales stored as 8-bit codes with an fp16 row scale
+    (s = rs * q): the decode GEMV and the tiled kernel (the MFMA decode and
+    several-token kernels do not read this format; "auto" passes those
+    calls on) match the oracle for logits, bf16 logits and CE, and the fused
+    argmax equals the first argmax of the same logits."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", scales="u8")
+    ph = PackedHead.from_arrays(h)
+    ph.force_path(path)
+    for M in (1, 8, 21):
+        x = make_x("tiny", M)
+        ref = ohead.logits(h, x)
+        say(f"8-bit scales tiny {path} M={M}")
+        lg = gpu_logits(ph, x)
+        assert_logits_close(lg, ref, what=f"8-bit scales {path} M={M}")
+        y = make_targets("tiny", M)
+        ce, _ = gpu_ce(ph, x, y)
+        assert_ce_close(ce, ohead.cross_entropy(ref, y), what=f"8-bit scales {path} M={M} CE")
+        idx, mx = gpu_argmax(ph, x)
+        assert np.array_equal(idx, np.argmax(lg, axis=1))
+        bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
+        assert_bf16_output(bits, lg, ref, f"8-bit scales {path} M={M} bf16")
+    ph.close()
+
+
+def test_8bit_scale_codes_identity_probe_bit_exact():
+    """One-hot x, no low-rank parts, 8-bit scale codes: every logit is
+    rs * q * c, exact in fp32, through the decode GEMV bit for bit."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", rc=0, rr=0, scales="u8")
+    ph = PackedHead.from_arrays(h)
+    ph.force_path("gemv")
+    eye = np.zeros((64, h.d), dtype=np.uint16)
+    cols = np.arange(0, h.d, h.d // 64)
+    eye[np.arange(64), cols] = 0x3F80
+    say("8-bit scales identity probe, gemv")
+    lg = gpu_logits(ph, eye).astype(np.float64)
+    assert np.array_equal(lg, ohead.logits(h, eye))
+    ph.close()
+
+
+@pytest.mark.parametrize("M", [1, 16])
+def test_8bit_scale_codes_qwen_sampled(M):
+    """The Qwen-shaped head with 8-bit scale codes through the library's own
+    choice (the GEMV at M = 1, the tiled kernel at M = 16): sampled
+    vocabulary columns against the oracle."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("qwen_decode", scales="u8")
+    ph = PackedHead.from_arrays(h)
+    x = make_x("qwen_decode", M)
+    rng = np.random.default_rng(11)
+    ids = np.unique(np.concatenate([[0, 1, h.V - 1], rng.integers(0, h.V, 400)]))
+    say(f"8-bit scales qwen M={M}, {ids.size} sampled columns")
+    lg = gpu_logits(ph, x)[:, ids]
+    assert_logits_close(lg, ohead.logits(h, x, vocab=ids), what=f"8-bit scales qwen M={M}")
+    ph.close()
+

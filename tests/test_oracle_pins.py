@@ -426,3 +426,30 @@ def test_config_packed_bytes(cfg, expect):
                   V * rr, V * 2, rr * d, rr * 2]
     assert sum(per_buffer) == expect
     assert obytes.packed_bytes(V, d, g, rc, rr) == expect
+
+
+def test_8bit_scale_codes_decode_exactly():
+    """8-bit residual scale codes (the "quantized group scales" of the
+    paper's packed-buffer table, read as q * rs with an fp16 row scale):
+    the oracle's scales are exactly rs * q, the generator's codes stay within
+    half a step of the fp16 draws, and a one-hot x gives logits equal to the
+    exact rational rs * q * c."""
+    from fractions import Fraction
+    h16 = make_head("tiny", V=64, d=128, g=64, rc=0, rr=0)
+    h8 = make_head("tiny", V=64, d=128, g=64, rc=0, rr=0, scales="u8")
+    assert h8.res_scales.dtype == np.uint8 and h8.res_row_scales.dtype == np.float16
+    rs = h8.res_row_scales.astype(np.float64)
+    s8 = ohead.residual_scales(h8, 0, h8.V)
+    assert np.array_equal(s8, rs[:, None] * h8.res_scales.astype(np.float64))
+    s16 = h16.res_scales.astype(np.float64)
+    assert np.all(np.abs(s8 - s16) <= rs[:, None] / 2 + 1e-3 * s16)
+    codes = layout.unpack_int4(h8.res_codes, h8.d)
+    for col in (0, 63, 64, 127):
+        x = np.zeros((1, h8.d), dtype=np.uint16)
+        x[0, col] = 0x3F80
+        lg = ohead.logits(h8, x)[0]
+        for v in (0, 7, 63):
+            exact = (Fraction(float(h8.res_row_scales[v])) * int(h8.res_scales[v, col // h8.g])
+                     * int(codes[v, col]))
+            assert Fraction(lg[v]) == exact
+
