@@ -1763,6 +1763,7 @@ constexpr int kDecCpol = ARCHEAD_DEC_CPOL;     // cache policy of the code loads
 struct DecArgs {
   const uint8_t* codes;
   const uint16_t* rs;
+  const uint16_t* rrs;   // row scales of 8-bit residual scale codes (else unused)
   const int8_t* cu;
   const uint16_t* su;
   const int8_t* ca;
@@ -1802,7 +1803,7 @@ __device__ __forceinline__ bool unroll_until(F& f) {
   return false;
 }
 
-template <int GW, bool CE, int EK>
+template <int GW, bool CE, int EK, bool SC8>
 __global__ __launch_bounds__(kDBlock) __attribute__((amdgpu_waves_per_eu(2)))
 void k_dec(DecArgs a) {
   static_assert(GW == 1 || GW == 2 || GW == 4, "code words per lane and group");
@@ -1870,7 +1871,8 @@ void k_dec(DecArgs a) {
   const lds_u8* const trow = L + a.off_t + 2 * (xr * a.tstr);
   // this lane's byte offsets within a unit's rows
   const int voff_c = int(uint32_t(lr) * rowbytes) + q * (4 * GW);        // codes: row lr, quarter q
-  const int voff_sc = (lane >> 2) * (2 * ngrp) + 16 * (lane & 3);       // scales: row lane/4
+  constexpr int ESZ = SC8 ? 1 : 2;                                      // bytes per group scale
+  const int voff_sc = (lane >> 2) * (ESZ * ngrp) + 16 * (lane & 3);     // scales: row lane/4
   const int voff_u = lr * a.rc + q * (8 * kcu);
   const int voff_a = lr * a.rr + q * (8 * kca);
 
@@ -1895,14 +1897,15 @@ void k_dec(DecArgs a) {
         const_cast<char*>(static_cast<const char*>(base)) + v0 * stride, 0, int(rows * stride),
         kBufferWord3);
   };
-  // The residual scales of a unit (16 rows x d/g fp16, contiguous) arrive as
-  // one 16-byte load per lane and 32 groups (lane l: row l/4, groups
-  // 8 (l % 4) .. +7); a lane takes the scale of its own row from the lane
-  // holding it with ds_bpermute.
+  // The residual scales of a unit (16 rows x d/g, contiguous) arrive as one
+  // 16-byte load per lane and 32 fp16 groups (lane l: row l/4, groups
+  // 8 (l % 4) .. +7) or 64 8-bit codes (groups 16 (l % 4) .. +15); a lane
+  // takes the scales of its own row from the lane holding them with
+  // ds_bpermute.
   auto load_scales = [&](int64_t u, u32x4_t (&dst)[2]) {
-    const __amdgpu_buffer_rsrc_t r_ = unit_rsrc(a.rs, u, 2u * ngrp);
+    const __amdgpu_buffer_rsrc_t r_ = unit_rsrc(a.rs, u, uint32_t(ESZ * ngrp));
     dst[0] = __builtin_amdgcn_raw_buffer_load_b128(r_, voff_sc, 0, 0);
-    if (ngrp > 32) dst[1] = __builtin_amdgcn_raw_buffer_load_b128(r_, voff_sc, 64, 0);
+    if (!SC8 && ngrp > 32) dst[1] = __builtin_amdgcn_raw_buffer_load_b128(r_, voff_sc, 64, 0);
   };
 
   // The head is walked in steps of kDecSG residual groups (one code load
@@ -1995,6 +1998,7 @@ void k_dec(DecArgs a) {
     // loads in flight when the unit's operands are requested
     u32x2_t eu[EK], ea[EK];
     uint16_t esu = 0, esa = 0;
+    uint16_t ers = 0;   // row scale of 8-bit residual scale codes
     auto load_exp = [&]() {
       const __amdgpu_buffer_rsrc_t ru = unit_rsrc(a.cu, cu_, uint32_t(a.rc));
       const __amdgpu_buffer_rsrc_t ra = unit_rsrc(a.ca, cu_, uint32_t(a.rr));
@@ -2008,6 +2012,7 @@ void k_dec(DecArgs a) {
     };
     auto finish_unit = [&]() {
       if (!t_ready) fetch_t();
+      if constexpr (SC8) tot *= f16_to_f32(ers);   // the residual in units of the row scale
       if (kcu + kca > 0) {
         f32x4_t au = {0.f, 0.f, 0.f, 0.f}, aa = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -2065,15 +2070,27 @@ void k_dec(DecArgs a) {
       asm volatile("" ::: "memory");
       if (cS == s_issue) {
         if (kcu + kca > 0) load_exp();
+        if constexpr (SC8)
+          ers = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.rrs, cu_, 2u), 2 * lr, 0, 0);
         if (ck + 1 < nu) load_scales(cu_ + W, snext);
       }
-      // scales of this step's groups 4 cS .. 4 cS + 3 of row lr: dwords
-      // 2 (cS % 2) and 2 (cS % 2) + 1 of lane 4 lr + (cS / 2) % 4's set cS / 8
-      const u32x4_t sv = cS >= 8 ? scur[1] : scur[0];
-      const bool odd = cS & 1;
-      const int src = 4 * (4 * lr + ((cS >> 1) & 3));
-      const uint32_t s01 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(odd ? sv[2] : sv[0])));
-      const uint32_t s23 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(odd ? sv[3] : sv[1])));
+      // scales of this step's groups 4 cS .. 4 cS + 3 of row lr: fp16 in
+      // dwords 2 (cS % 2) and 2 (cS % 2) + 1 of lane 4 lr + (cS / 2) % 4's
+      // set cS / 8; 8-bit codes in dword cS % 4 of lane 4 lr + cS / 4
+      uint32_t s01, s23;
+      if constexpr (SC8) {
+        const u32x4_t sv = scur[0];
+        const int c4 = cS & 3;
+        const uint32_t dw = c4 == 0 ? sv[0] : c4 == 1 ? sv[1] : c4 == 2 ? sv[2] : sv[3];
+        s01 = uint32_t(__builtin_amdgcn_ds_bpermute(4 * (4 * lr + ((cS >> 2) & 3)), int(dw)));
+        s23 = s01;
+      } else {
+        const u32x4_t sv = cS >= 8 ? scur[1] : scur[0];
+        const bool odd = cS & 1;
+        const int src = 4 * (4 * lr + ((cS >> 1) & 3));
+        s01 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(odd ? sv[2] : sv[0])));
+        s23 = uint32_t(__builtin_amdgcn_ds_bpermute(src, int(odd ? sv[3] : sv[1])));
+      }
       f32x4_t acc[SG];
 #pragma unroll
       for (int k = 0; k < SG; ++k) acc[k] = lds_load<f32x4_t>(brow + 64 * (cS * SG + k));
@@ -2088,8 +2105,12 @@ void k_dec(DecArgs a) {
       }
 #pragma unroll
       for (int k = 0; k < SG; ++k) {
-        const uint32_t sw = k < 2 ? s01 : s23;
-        tot += f16_to_f32(uint16_t(k & 1 ? sw >> 16 : sw)) * acc[k];
+        if constexpr (SC8) {
+          tot += float((s01 >> (8 * k)) & 0xffu) * acc[k];
+        } else {
+          const uint32_t sw = k < 2 ? s01 : s23;
+          tot += f16_to_f32(uint16_t(k & 1 ? sw >> 16 : sw)) * acc[k];
+        }
       }
       if (++cS == nsg) {
         finish_unit();
@@ -2999,18 +3020,23 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
 
 using DecFn = void (*)(DecArgs);
 
-template <bool CE, int EK>
+template <bool CE, int EK, bool SC8>
 DecFn dec_fn_ek(int gw) {
   switch (gw) {
-    case 1: return k_dec<1, CE, EK>;
-    case 2: return k_dec<2, CE, EK>;
-    default: return k_dec<4, CE, EK>;
+    case 1: return k_dec<1, CE, EK, SC8>;
+    case 2: return k_dec<2, CE, EK, SC8>;
+    default: return k_dec<4, CE, EK, SC8>;
   }
 }
 
+template <bool CE, bool SC8>
+DecFn dec_fn_sc(int gw, int kcu, int kca) {
+  return kcu <= 2 && kca <= 2 ? dec_fn_ek<CE, 2, SC8>(gw) : dec_fn_ek<CE, 4, SC8>(gw);
+}
+
 template <bool CE>
-DecFn dec_fn(int gw, int kcu, int kca) {
-  return kcu <= 2 && kca <= 2 ? dec_fn_ek<CE, 2>(gw) : dec_fn_ek<CE, 4>(gw);
+DecFn dec_fn(int gw, int kcu, int kca, bool sc8) {
+  return sc8 ? dec_fn_sc<CE, true>(gw, kcu, kca) : dec_fn_sc<CE, false>(gw, kcu, kca);
 }
 
 // One launch per pass of up to dec_tokens_per_pass tokens.  The CE form
@@ -3037,7 +3063,9 @@ archead_status launch_dec(const archead_handle* h, const void* x, int64_t M, int
   a.n_prod_blocks = gr.prod_blocks;
   const int gw = int(d.g / 32);
   const DecLds l0 = dec_lds(d, 1);
-  DecFn fn = ce ? dec_fn<true>(gw, l0.kcu, l0.kca) : dec_fn<false>(gw, l0.kcu, l0.kca);
+  const bool sc8 = d.scale_dtype == ARCHEAD_U8;
+  DecFn fn = ce ? dec_fn<true>(gw, l0.kcu, l0.kca, sc8) : dec_fn<false>(gw, l0.kcu, l0.kca, sc8);
+  a.rrs = sc8 ? static_cast<const uint16_t*>(h->ptrs.res_row_scales) : a.rs;
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
   hipEvent_t ev1 = static_cast<hipEvent_t>(h->ev_stop.load(std::memory_order_relaxed));
   const int64_t grid = gr.prod_blocks + gr.consumer_blocks;

@@ -57,7 +57,7 @@ int dec_tokens_per_pass(const archead_desc& d) {
   // at most 64 groups per row (two scale loads per unit); factor code rows
   // read as dwords; at most 128 dimensions per factor (4 K-chunks)
   if (d.g != 32 && d.g != 64 && d.g != 128) return 0;
-  if (d.scale_dtype != ARCHEAD_F16) return 0;   // reads fp16 group scales
+  // 8-bit scale codes: all 64 groups of a row in one 16-byte load per lane
   if ((d.d / d.g) % 4 || d.d / d.g > 64) return 0;
   if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return 0;
   // byte offsets of the code buffer stay 32-bit

@@ -642,13 +642,13 @@ def test_argmax_gemma_m64_against_oracle():
 
 # ------------------------------------------------------ 8-bit scale codes
 
-@pytest.mark.parametrize("path", ["gemv", "tiled", "auto"])
+@pytest.mark.parametrize("path", ["gemv", "dec", "tiled", "auto"])
 def test_8bit_scale_codes_tiny(path):
     """Residual group scales stored as 8-bit codes with an fp16 row scale
-    (s = rs * q): the decode GEMV and the tiled kernel (the MFMA decode and
-    several-token kernels do not read this format; "auto" passes those
-    calls on) match the oracle for logits, bf16 logits and CE, and the fused
-    argmax equals the first argmax of the same logits."""
+    (s = rs * q): the decode GEMV, the MFMA decode kernel and the tiled
+    kernel (the several-token kernel does not read this format; "auto"
+    passes its calls on) match the oracle for logits, bf16 logits and CE,
+    and the fused argmax equals the first argmax of the same logits."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("tiny", scales="u8")
     ph = PackedHead.from_arrays(h)
@@ -685,11 +685,11 @@ def test_8bit_scale_codes_identity_probe_bit_exact():
     ph.close()
 
 
-@pytest.mark.parametrize("M", [1, 16])
+@pytest.mark.parametrize("M", [1, 16, 40])
 def test_8bit_scale_codes_qwen_sampled(M):
     """The Qwen-shaped head with 8-bit scale codes through the library's own
-    choice (the GEMV at M = 1, the tiled kernel at M = 16): sampled
-    vocabulary columns against the oracle."""
+    choice (the GEMV at M = 1, the MFMA decode kernel at M = 16, the tiled
+    kernel at M = 40): sampled vocabulary columns against the oracle."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("qwen_decode", scales="u8")
     ph = PackedHead.from_arrays(h)
