@@ -13,6 +13,6 @@ Modules
   head       dense head W_hat = W_res + U_c V_c + A B, logits, CE, argmax
   bytes      persistent-byte accounting (sum of numel x element size)
   construct  damped covariance, metric transform, correction fit by exact SVD
-  metrics    PPL and relative PPL
+  metrics    PPL and relative PPL; logit fidelity (KL, top-k agreement, MSE)
 """
 from . import layout, head, bytes as bytes_, construct, metrics  # noqa: F401

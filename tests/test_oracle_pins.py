@@ -453,3 +453,106 @@ def test_8bit_scale_codes_decode_exactly():
                      * int(codes[v, col]))
             assert Fraction(lg[v]) == exact
 
+
+
+# ------------------------------------------------ P12 logit fidelity metrics
+
+def _softmax64(z):
+    from scipy.special import softmax
+    return softmax(np.asarray(z, dtype=np.float64), axis=-1)
+
+
+def test_fidelity_kl_matches_library_relative_entropy():
+    """KL(p_ref || p_test) against scipy's relative entropy of the two
+    softmax distributions; the reverse direction differs (asymmetric
+    case), so swapped operands fail."""
+    from scipy.stats import entropy
+    rng = np.random.default_rng(21)
+    a = 3.0 * rng.standard_normal((6, 37))
+    b = a + rng.standard_normal((6, 37))
+    kl, _, _, _ = metrics.logit_fidelity(a, b)
+    for m in range(6):
+        want = entropy(_softmax64(a[m]), _softmax64(b[m]))
+        rev = entropy(_softmax64(b[m]), _softmax64(a[m]))
+        assert kl[m] == pytest.approx(want, rel=1e-12, abs=1e-15)
+        assert abs(want - rev) > 1e-3 * want
+
+
+def test_fidelity_kl_two_token_closed_form():
+    """V = 2: the softmax of [0, s] is Bernoulli(sigmoid(s)), whose KL has a
+    closed form."""
+    for s, t in [(0.3, -1.2), (4.0, 2.5), (-7.0, 1.0)]:
+        p, q = 1 / (1 + math.exp(-s)), 1 / (1 + math.exp(-t))
+        want = p * math.log(p / q) + (1 - p) * math.log((1 - p) / (1 - q))
+        kl, _, _, _ = metrics.logit_fidelity(np.array([[0.0, s]]), np.array([[0.0, t]]))
+        assert kl[0] == pytest.approx(want, rel=1e-12)
+
+
+def test_fidelity_kl_zero_on_equal_and_shift_invariant():
+    """KL is 0 for equal logits and does not change when a constant is added
+    to one position's logits on either side (softmax is shift invariant); a
+    dropped log-sum-exp term fails this."""
+    rng = np.random.default_rng(22)
+    a = 5.0 * rng.standard_normal((4, 100))
+    b = a + 0.5 * rng.standard_normal((4, 100))
+    kl0, sq0, _, _ = metrics.logit_fidelity(a, a)
+    assert np.all(np.abs(kl0) < 1e-13) and np.all(sq0 == 0)
+    kl, _, _, _ = metrics.logit_fidelity(a, b)
+    assert np.all(kl > 0)
+    shift = np.array([[3.0], [-40.0], [0.25], [900.0]])
+    kl_a, _, _, _ = metrics.logit_fidelity(a + shift, b)
+    kl_b, _, _, _ = metrics.logit_fidelity(a, b - shift)
+    np.testing.assert_allclose(kl_a, kl, rtol=1e-9)
+    np.testing.assert_allclose(kl_b, kl, rtol=1e-9)
+
+
+def test_fidelity_squared_error_closed_form():
+    """A constant offset c on every logit gives V c^2 per position."""
+    a = np.random.default_rng(23).standard_normal((3, 50))
+    _, sq, _, _ = metrics.logit_fidelity(a, a + 0.5)
+    np.testing.assert_allclose(sq, 50 * 0.25, rtol=1e-12)
+
+
+def test_fidelity_mse_is_the_activation_objective():
+    """Mean over positions of the summed squared logit error equals
+    Tr(Delta C Delta^T) with C = H^T H / N and Delta = W - W_hat, the
+    objective of Eq. (1), computed here in its trace form."""
+    rng = np.random.default_rng(24)
+    N, V, D = 40, 30, 12
+    H = rng.standard_normal((N, D))
+    W = rng.standard_normal((V, D))
+    Wh = W + 0.05 * rng.standard_normal((V, D))
+    _, sq, _, _ = metrics.logit_fidelity(H @ W.T, H @ Wh.T)
+    Dl = W - Wh
+    C = H.T @ H / N
+    assert metrics.fidelity_summary(np.zeros(N), sq, np.zeros(N))["mse"] == \
+        pytest.approx(float(np.trace(Dl @ C @ Dl.T)), rel=1e-10)
+
+
+def test_fidelity_rank_hand_fixture_with_ties():
+    """ref's first maximum is index 1; in test, index 2 is larger and index 0
+    ties with index 1 but comes first, so index 1 sits at rank 2."""
+    ref = np.array([[0.0, 5.0, 5.0, 1.0], [1.0, 0.0, 0.0, 0.0], [2.0, 2.0, 2.0, 2.0]])
+    test = np.array([[2.0, 2.0, 7.0, 2.0], [9.0, 9.0, 9.0, 9.0], [1.0, 3.0, 0.0, 3.0]])
+    _, _, idx, rank = metrics.logit_fidelity(ref, test)
+    assert idx.tolist() == [1, 0, 0]
+    assert rank.tolist() == [2, 0, 2]
+
+
+@settings(max_examples=40, deadline=None)
+@given(st.integers(1, 12), st.integers(0, 2 ** 31 - 1))
+def test_fidelity_rank_brute_force_stable_sort(V, seed):
+    """rank = position of the reference's first argmax in a stable
+    descending sort of the test logits (a library sort), with values drawn
+    from a small set so that ties are frequent; top-1 agreement equals
+    equality of the two first-index argmaxes."""
+    rng = np.random.default_rng(seed)
+    a = rng.integers(-2, 3, size=(5, V)).astype(np.float64)
+    b = rng.integers(-2, 3, size=(5, V)).astype(np.float64)
+    _, _, idx, rank = metrics.logit_fidelity(a, b)
+    for m in range(5):
+        order = np.argsort(-b[m], kind="stable")
+        assert idx[m] == ohead.argmax(a[m:m + 1])[0]
+        assert rank[m] == int(np.nonzero(order == idx[m])[0][0])
+    top1 = metrics.fidelity_summary(np.zeros(5), np.zeros(5), rank, ks=(1,))["top1"]
+    assert top1 == pytest.approx(100.0 * np.mean(ohead.argmax(a) == ohead.argmax(b)))
