@@ -253,6 +253,31 @@ archead_status archead_logits_argmax(const archead_handle* h, const void* x, int
                                      int64_t ldx, int64_t* idx, float* max_logit, void* ws,
                                      size_t ws_bytes, void* stream);
 
+/* Logit fidelity of `test` logits to reference logits `ref` (the paper's
+ * "Logit Fidelity" metrics, Section 4 and its Table 8: the packed head
+ * against the dense head on the same positions), per position m < M:
+ *   kl[m]      = KL(p || q) = sum_v p_v (log p_v - log q_v), p = softmax(ref[m]),
+ *                q = softmax(test[m]);
+ *   sq[m]      = sum_v (ref[m, v] - test[m, v])^2 (its mean over positions is
+ *                the logit MSE, the activation objective of Eq. (1));
+ *   ref_idx[m] = the smallest v attaining max_v ref[m, v];
+ *   rank[m]    = the number of v with test[m, v] > test[m, ref_idx[m]], plus
+ *                those equal to it at a smaller index: the reference's top-1
+ *                token is in the test top k exactly when rank < k (top-1
+ *                agreement: rank == 0).
+ *   ref, test  device fp32 [M, ld_ref] / [M, ld_test] row-major, ld >= V
+ *   kl, sq     device fp32 [M];  ref_idx, rank  device int64 [M] (8-byte aligned)
+ *   stream     hipStream_t (NULL = the default stream); asynchronous
+ * Sums are taken in fp64 over fp32 exponentials in a fixed order (the
+ * result is reproducible).  Inputs must be finite.  Needs no handle and no
+ * workspace; M = 0 is a no-op.  ARCHEAD_E_INVALID_ARG for a null pointer,
+ * M < 0, V < 1, V or M >= 2^31 or ld < V; ARCHEAD_E_MISALIGNED for a
+ * misaligned pointer; ARCHEAD_E_HIP when the launch fails. */
+archead_status archead_logit_fidelity(const float* ref, int64_t ld_ref, const float* test,
+                                      int64_t ld_test, int64_t M, int64_t V, float* kl,
+                                      float* sq, int64_t* ref_idx, int64_t* rank,
+                                      void* stream);
+
 /* Largest M served by the decode GEMV kernel when the MFMA decode kernel
  * does not take the call; larger M use the tiled MFMA kernel (unless
  * g % 64 != 0, which always takes the GEMV).

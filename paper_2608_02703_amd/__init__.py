@@ -8,6 +8,8 @@ from .archead import (  # noqa: F401
     ArcheadError,
     Desc,
     PackedHead,
+    fidelity_summary,
+    logit_fidelity,
     lib,
     pack_int4,
     packed_bytes,

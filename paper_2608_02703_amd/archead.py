@@ -69,6 +69,10 @@ _SIGS = {
     "archead_logits_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_logit_fidelity": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                              ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p, ctypes.c_void_p]),
     "archead_set_gemv_max_m": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64]),
     "archead_get_gemv_max_m": (ctypes.c_int64, [ctypes.c_void_p]),
     "archead_set_dec_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
@@ -163,6 +167,42 @@ def unpack_int4(packed: np.ndarray, d: int, L=None) -> np.ndarray:
 
 def _ptr(t) -> int:
     return 0 if t is None else int(t.data_ptr())
+
+
+def logit_fidelity(ref, test):
+    """Per-position fidelity of `test` logits to reference logits `ref`, both
+    fp32 [M, V] CUDA tensors with unit column stride (archead_logit_fidelity):
+    returns (kl fp32 [M], sq fp32 [M], ref_idx int64 [M], rank int64 [M]) on
+    the same device, computed on the current stream."""
+    import torch
+    if ref.dtype != torch.float32 or test.dtype != torch.float32:
+        raise TypeError("logits must be float32")
+    if ref.dim() != 2 or ref.shape != test.shape:
+        raise ValueError("ref and test must both be [M, V]")
+    if ref.stride(1) != 1 or test.stride(1) != 1:
+        raise ValueError("logit rows must be contiguous")
+    M, V = ref.shape
+    dev = ref.device
+    kl = torch.empty(M, dtype=torch.float32, device=dev)
+    sq = torch.empty(M, dtype=torch.float32, device=dev)
+    idx = torch.empty(M, dtype=torch.int64, device=dev)
+    rank = torch.empty(M, dtype=torch.int64, device=dev)
+    L = lib()
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    _check(L.archead_logit_fidelity(_ptr(ref), ref.stride(0), _ptr(test), test.stride(0), M, V,
+                                    _ptr(kl), _ptr(sq), _ptr(idx), _ptr(rank), stream), L)
+    return kl, sq, idx, rank
+
+
+def fidelity_summary(kl, sq, rank, ks=(1, 5, 10)) -> dict:
+    """Aggregates over positions as the paper tabulates them: mean KL, logit
+    MSE (mean of the per-position summed squared error) and top-k agreement
+    in percent (rank < k)."""
+    import torch
+    out = {"kl": float(kl.double().mean()), "mse": float(sq.double().mean())}
+    for k in ks:
+        out[f"top{k}"] = 100.0 * float((rank < k).double().mean())
+    return out
 
 
 class PackedHead:

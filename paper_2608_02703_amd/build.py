@@ -1,7 +1,8 @@
 """Build the ARCHead HIP library for gfx950 (in-tree, no JIT cache).
 
-``python -m paper_2608_02703_amd.build`` compiles csrc/host.cpp and
-csrc/archead.hip with hipcc into paper_2608_02703_amd/libarchead.so, and the
+``python -m paper_2608_02703_amd.build`` compiles csrc/host.cpp,
+csrc/archead.hip and csrc/fidelity.hip with hipcc into
+paper_2608_02703_amd/libarchead.so, and the
 host-only translation unit with g++ (optionally under ASan/UBSan) into
 libarchead_host.so for the CPU tests of the argument checks and packers.
 """
@@ -45,7 +46,8 @@ def _run(cmd, verbose):
 def build_hip(verbose: bool = False, out: str = LIB, defines=()) -> str:
     tmp = out + ".tmp"
     cmd = [_hipcc(), *HIP_FLAGS, *[f"-D{d}" for d in defines], f"-I{INCLUDE}",
-           os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "archead.hip"), "-o", tmp]
+           os.path.join(CSRC, "host.cpp"), os.path.join(CSRC, "archead.hip"),
+           os.path.join(CSRC, "fidelity.hip"), "-o", tmp]
     _run(cmd, verbose)
     os.replace(tmp, out)
     return out

@@ -203,3 +203,21 @@ def test_packed_bytes_with_8bit_scales(L, V, d, g, rc, rr):
     if (V, d, g, rc, rr) == (151936, 4096, 128, 64, 32):
         assert got == 336_475_840 - V * (d // g) * 2 + V * (d // g) + 2 * V == 331_917_760
 
+
+
+@pytest.mark.parametrize("M,V,ld_r,ld_t,null,shift,status", [
+    (0, 10, 10, 10, False, 0, ab.OK),                 # empty: no launch
+    (-1, 10, 10, 10, False, 0, ab.E_INVALID_ARG),
+    (2, 0, 10, 10, False, 0, ab.E_INVALID_ARG),
+    (2, 2 ** 31, 2 ** 31, 2 ** 31, False, 0, ab.E_INVALID_ARG),
+    (2, 10, 9, 10, False, 0, ab.E_INVALID_ARG),       # ld < V
+    (2, 10, 10, 9, False, 0, ab.E_INVALID_ARG),
+    (2, 10, 10, 10, True, 0, ab.E_INVALID_ARG),       # null output
+    (2, 10, 10, 10, False, 2, ab.E_MISALIGNED),       # fp32 buffer off by 2 bytes
+])
+def test_logit_fidelity_argument_checks(L, M, V, ld_r, ld_t, null, shift, status):
+    """archead_logit_fidelity rejects bad shapes and pointers before any HIP
+    call (the pointers here are never dereferenced)."""
+    p = 1 << 20
+    args = [p + shift, ld_r, p, ld_t, M, V, p, p, 0 if null else p, p, None]
+    assert L.archead_logit_fidelity(*args) == status, L.archead_last_error()
