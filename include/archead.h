@@ -114,10 +114,8 @@ typedef enum archead_op {
  *                  res_row_scales one fp16 scale rs per vocabulary row [V],
  *                  s[v, j] = rs[v] * q[v, j] (exact in fp32).  One byte of
  *                  scale per group is the storage the paper's reported head
- *                  sizes imply.  Served by the decode GEMV, the MFMA
- *                  decode kernel and the tiled MFMA kernel (the several-
- *                  token kernel does not read this format, and calls past
- *                  the decode kernel's M range go to the tiled one). */
+ *                  sizes imply.  Served by every kernel (see
+ *                  archead_logits). */
 typedef struct archead_desc {
   uint32_t abi_version; /* ARCHEAD_ABI_VERSION */
   int64_t V, d, g;

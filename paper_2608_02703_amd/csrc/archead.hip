@@ -73,6 +73,13 @@ __device__ __forceinline__ float dot2_bf16(uint32_t a, uint32_t b, float c) {
 __device__ __forceinline__ float f16_to_f32(uint16_t h) {
   return (float)__builtin_bit_cast(_Float16, h);
 }
+// four bytes (integers 0..255, exact in fp16) as four fp16, low byte first
+__device__ __forceinline__ u32x2_t u8x4_to_f16x4(uint32_t w) {
+  auto h = [](uint32_t b) {
+    return uint32_t(__builtin_bit_cast(uint16_t, _Float16(float(b & 0xffu))));
+  };
+  return u32x2_t{h(w) | (h(w >> 8) << 16), h(w >> 16) | (h(w >> 24) << 16)};
+}
 __device__ __forceinline__ float bf16_lo(uint32_t p) { return __uint_as_float(p << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t p) { return __uint_as_float(p & 0xffff0000u); }
 
@@ -2184,6 +2191,7 @@ static_assert(kMidKW == archead::kMidWindow && kMidWaves == archead::kMidWaveCou
 struct MidArgs {
   const uint8_t* codes;
   const uint16_t* rs;
+  const uint16_t* rrs;   // row scales of 8-bit residual scale codes (else unused)
   const int8_t* cu;
   const uint16_t* su;
   const int8_t* ca;
@@ -2222,7 +2230,7 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
-template <int GW, int NF, int NU, bool CE>
+template <int GW, int NF, int NU, bool CE, bool SC8>
 __global__ __launch_bounds__(kMidBlock) __attribute__((amdgpu_waves_per_eu(2)))
 void k_mid(MidArgs a) {
   static_assert(GW == 2 || GW == 4, "groups of 64 or 128 codes");
@@ -2282,8 +2290,9 @@ void k_mid(MidArgs a) {
   float2* const sred = reinterpret_cast<float2*>(mid_lds + a.off_red);
   int64_t* const sy = reinterpret_cast<int64_t*>(mid_lds + a.off_y);
   int* const sidx = reinterpret_cast<int*>(mid_lds + a.off_idx);   // [waves][TM] argmax
-  // residual scales of this wave's units: [unit][row][group] fp16, rows
-  // padded by 4 bytes so the 16 rows read at one step fall on distinct banks
+  // residual scales of this wave's units: [unit][row][group] fp16 (8-bit
+  // codes widened to fp16, exact), rows padded by 4 bytes so the 16 rows
+  // read at one step fall on distinct banks
   const int sstr = 2 * ngrp + 4;
   lds_u8* const ssc = L + a.off_sc + wid * (NU * 16 * sstr);
   if constexpr (CE) {
@@ -2425,16 +2434,22 @@ void k_mid(MidArgs a) {
       uj[j] = ui < nub ? u_lo + ui : a.n_units;   // past the head: no rows
       rcu[j] = unit_rsrc(a.codes, uj[j], rowbytes);
     }
-    // the units' scales (8-byte pieces, issued first so that waiting for
-    // them leaves the code loads in flight), the pass's first code loads,
-    // the first two windows
+    // the units' scales (pieces of 4 groups: 8 bytes of fp16 or 4 bytes of
+    // 8-bit codes, issued first so that waiting for them leaves the code
+    // loads in flight), the pass's first code loads, the first two windows
     {
-      u32x2_t sp[NU][4];
+      using Piece = typename std::conditional<SC8, uint32_t, u32x2_t>::type;
+      Piece sp[NU][4];
 #pragma unroll
       for (int j = 0; j < NU; ++j) {
-        const __amdgpu_buffer_rsrc_t r_ = unit_rsrc(a.rs, uj[j], 2u * ngrp);
+        const __amdgpu_buffer_rsrc_t r_ = unit_rsrc(a.rs, uj[j], uint32_t((SC8 ? 1 : 2) * ngrp));
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sp[j][i] = __builtin_amdgcn_raw_buffer_load_b64(r_, 8 * (lane + 64 * i), 0, 0);
+        for (int i = 0; i < 4; ++i) {
+          if constexpr (SC8)
+            sp[j][i] = __builtin_amdgcn_raw_buffer_load_b32(r_, 4 * (lane + 64 * i), 0, 0);
+          else
+            sp[j][i] = __builtin_amdgcn_raw_buffer_load_b64(r_, 8 * (lane + 64 * i), 0, 0);
+        }
       }
       load_win(std::integral_constant<int, 0>{}, 0);
       load_win(std::integral_constant<int, 1>{}, 1);
@@ -2454,8 +2469,13 @@ void k_mid(MidArgs a) {
             const int row = pc / pr, c = pc - row * pr;
             auto* dst = reinterpret_cast<__attribute__((address_space(3))) uint32_t*>(
                 ssc + (j * 16 + row) * sstr + 8 * c);
-            dst[0] = sp[j][i].x;
-            dst[1] = sp[j][i].y;
+            u32x2_t pv;
+            if constexpr (SC8)
+              pv = u8x4_to_f16x4(sp[j][i]);
+            else
+              pv = sp[j][i];
+            dst[0] = pv.x;
+            dst[1] = pv.y;
           }
         }
     }
@@ -2548,6 +2568,7 @@ void k_mid(MidArgs a) {
     // requested together, then t goes to LDS while they are in flight.
     u32x2_t eu[NU][4], ea[NU][4];
     uint16_t esu[NU], esa[NU];
+    uint16_t ers[NU];   // row scales of 8-bit residual scale codes
 #pragma unroll
     for (int j = 0; j < NU; ++j) {
       const __amdgpu_buffer_rsrc_t ru = unit_rsrc(cu_b, uj[j], uint32_t(a.rc));
@@ -2559,6 +2580,8 @@ void k_mid(MidArgs a) {
       }
       esu[j] = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(su_b, uj[j], a.rc ? 2u : 0u), 2 * lr, 0, 0);
       esa[j] = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(sa_b, uj[j], a.rr ? 2u : 0u), 2 * lr, 0, 0);
+      if constexpr (SC8)
+        ers[j] = __builtin_amdgcn_raw_buffer_load_b16(unit_rsrc(a.rrs, uj[j], 2u), 2 * lr, 0, 0);
     }
     lds_barrier();          // every wave is done with the windows
     if (R > 0) {
@@ -2568,6 +2591,11 @@ void k_mid(MidArgs a) {
 #pragma unroll
     for (int j = 0; j < NU; ++j) {
       if (uj[j] >= a.n_units) continue;
+      if constexpr (SC8) {   // the residual was summed in units of the row scale
+        const float fr = f16_to_f32(ers[j]);
+#pragma unroll
+        for (int f = 0; f < NF; ++f) tot[j][f] *= fr;
+      }
       if (kcu + kca > 0) {
         f32x4_t au[NF], aa[NF];
 #pragma unroll
@@ -3099,8 +3127,9 @@ using MidFn = void (*)(MidArgs);
 // register budget.  (Tiles of 64 tokens with 2 units per wave measured
 // slower than two tiles of 32.)
 template <bool CE>
-MidFn mid_fn(int gw) {
-  return gw == 4 ? k_mid<4, 2, 3, CE> : k_mid<2, 2, 2, CE>;
+MidFn mid_fn(int gw, bool sc8) {
+  if (sc8) return gw == 4 ? k_mid<4, 2, 3, CE, true> : k_mid<2, 2, 2, CE, true>;
+  return gw == 4 ? k_mid<4, 2, 3, CE, false> : k_mid<2, 2, 2, CE, false>;
 }
 
 // One launch per tile of up to 32 tokens.  The CE form writes one softmax
@@ -3111,6 +3140,7 @@ archead_status launch_mid(const archead_handle* h, const void* x, int64_t M, int
   const MidGrid gr = mid_grid(h);
   a.codes = static_cast<const uint8_t*>(h->ptrs.res_codes);
   a.rs = static_cast<const uint16_t*>(h->ptrs.res_scales);
+  a.rrs = d.scale_dtype == ARCHEAD_U8 ? static_cast<const uint16_t*>(h->ptrs.res_row_scales) : a.rs;
   a.cu = static_cast<const int8_t*>(h->ptrs.core_u);
   a.su = static_cast<const uint16_t*>(h->ptrs.core_u_scale);
   a.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
@@ -3130,7 +3160,8 @@ archead_status launch_mid(const archead_handle* h, const void* x, int64_t M, int
   const int64_t grid = gr.prod_blocks + gr.cblocks;
   for (int64_t m0 = 0; m0 < M; m0 += kMidTokMax) {
     const int tok = int(M - m0 < kMidTokMax ? M - m0 : kMidTokMax);
-    MidFn fn = ce ? mid_fn<true>(gw) : mid_fn<false>(gw);
+    const bool sc8 = d.scale_dtype == ARCHEAD_U8;
+    MidFn fn = ce ? mid_fn<true>(gw, sc8) : mid_fn<false>(gw, sc8);
     const MidLds l = mid_lds(d);
     a.tok0 = m0;
     a.M = tok;

@@ -95,7 +95,6 @@ bool mid_supported(const archead_desc& d) {
   // at most 64 groups per row (a unit's scales staged in LDS), factor code rows
   // read as dwords, at most 128 dimensions per factor (4 K-chunks)
   if (d.g != 64 && d.g != 128) return false;
-  if (d.scale_dtype != ARCHEAD_F16) return false;   // reads fp16 group scales
   if (d.d % (2 * kMidWindow) || d.d / d.g > 64) return false;
   if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return false;
   return mid_lds(d).total <= kLdsBytes;

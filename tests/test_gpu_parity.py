@@ -462,6 +462,31 @@ def test_mid_ragged(V, d, g, M, rc, rr):
     ph.close()
 
 
+@pytest.mark.parametrize("path", ["dec", "mid"])
+@pytest.mark.parametrize("V,d,g,M,rc,rr", [(1000, 512, 64, 17, 16, 8), (777, 1024, 128, 40, 20, 4),
+                                           (4099, 1024, 64, 100, 0, 36), (130, 2560, 128, 33, 12, 28),
+                                           (500, 8192, 128, 20, 128, 128)])
+def test_8bit_scale_codes_ragged(path, V, d, g, M, rc, rr):
+    """8-bit scale codes on partial 16-row units, 4 to 64 scale groups per
+    row (64: one 16-byte code load per lane holds a whole row set), several
+    tiles and passes, padded ranks, CE and bf16 output."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("tiny", V=V, d=d, g=g, rc=rc, rr=rr, scales="u8")
+    x = make_x("tiny", M, d=d, basis="identity")
+    ph = PackedHead.from_arrays(h)
+    ph.force_path(path)
+    ref = ohead.logits(h, x)
+    say(f"8-bit ragged {path} V={V} d={d} g={g} M={M} rc={rc} rr={rr}")
+    lg = gpu_logits(ph, x, ld=d + 8)
+    assert_logits_close(lg, ref, what=f"8-bit ragged {path}")
+    y = (np.arange(M) * 7 % V).astype(np.int32)
+    ce, _ = gpu_ce(ph, x, y)
+    assert_ce_close(ce, ohead.cross_entropy(ref, y), what=f"8-bit ragged {path} CE")
+    bits = gpu_logits(ph, x, out_dtype=torch.bfloat16)
+    assert_bf16_output(bits, lg, ref, f"8-bit ragged {path} bf16")
+    ph.close()
+
+
 def test_identity_probe_mid_qwen_sampled_bit_exact():
     """The one-hot probe on the Qwen-shaped head through the several-token
     kernel (a tile of 64 tokens and a partial one), bit for bit."""
@@ -642,13 +667,12 @@ def test_argmax_gemma_m64_against_oracle():
 
 # ------------------------------------------------------ 8-bit scale codes
 
-@pytest.mark.parametrize("path", ["gemv", "dec", "tiled", "auto"])
+@pytest.mark.parametrize("path", ["gemv", "dec", "mid", "tiled", "auto"])
 def test_8bit_scale_codes_tiny(path):
     """Residual group scales stored as 8-bit codes with an fp16 row scale
-    (s = rs * q): the decode GEMV, the MFMA decode kernel and the tiled
-    kernel (the several-token kernel does not read this format; "auto"
-    passes its calls on) match the oracle for logits, bf16 logits and CE,
-    and the fused argmax equals the first argmax of the same logits."""
+    (s = rs * q): every kernel matches the oracle for logits, bf16 logits
+    and CE, and the fused argmax equals the first argmax of the same
+    logits."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("tiny", scales="u8")
     ph = PackedHead.from_arrays(h)
@@ -669,27 +693,31 @@ def test_8bit_scale_codes_tiny(path):
     ph.close()
 
 
-def test_8bit_scale_codes_identity_probe_bit_exact():
+@pytest.mark.parametrize("path", ["gemv", "dec", "mid"])
+def test_8bit_scale_codes_identity_probe_bit_exact(path):
     """One-hot x, no low-rank parts, 8-bit scale codes: every logit is
-    rs * q * c, exact in fp32, through the decode GEMV bit for bit."""
+    rs * q * c, exact in fp32 (11 + 8 + 4 significant bits), bit for bit
+    through the kernels that multiply a group's partial by its code and the
+    row's total by the row scale."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("tiny", rc=0, rr=0, scales="u8")
     ph = PackedHead.from_arrays(h)
-    ph.force_path("gemv")
+    ph.force_path(path)
     eye = np.zeros((64, h.d), dtype=np.uint16)
     cols = np.arange(0, h.d, h.d // 64)
     eye[np.arange(64), cols] = 0x3F80
-    say("8-bit scales identity probe, gemv")
+    say(f"8-bit scales identity probe, {path}")
     lg = gpu_logits(ph, eye).astype(np.float64)
     assert np.array_equal(lg, ohead.logits(h, eye))
     ph.close()
 
 
-@pytest.mark.parametrize("M", [1, 16, 40])
+@pytest.mark.parametrize("M", [1, 16, 40, 130])
 def test_8bit_scale_codes_qwen_sampled(M):
     """The Qwen-shaped head with 8-bit scale codes through the library's own
-    choice (the GEMV at M = 1, the MFMA decode kernel at M = 16, the tiled
-    kernel at M = 40): sampled vocabulary columns against the oracle."""
+    choice (the GEMV at M = 1, the MFMA decode kernel at M = 16, the
+    several-token kernel at M = 40, the tiled kernel at M = 130): sampled
+    vocabulary columns against the oracle."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("qwen_decode", scales="u8")
     ph = PackedHead.from_arrays(h)
