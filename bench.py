@@ -421,7 +421,7 @@ def main():
     ms1, kern1, _ = res[1]
     value = pbytes / ms1 / 1e6          # GB/s
     alg = decode_algorithmic_bytes(h, 1)
-    kname = f"k_gemv<1,{lanes_per_row(h)},false>"
+    kname = f"k_gemv<1,{lanes_per_row(h)},false,false>"
     achieved = alg / kern1 / 1e6
     out = {
         "metric": METRIC,
