@@ -213,19 +213,26 @@ def ms1_for_dense(res):
     return res[1][0]
 
 
-def cpu_baseline(h, xb):
-    """The fp64 oracle on the host cores: full head, one token (M=1)."""
+def cpu_baseline(h, xb, min_sec=10.0, max_tokens=16):
+    """The fp64 oracle on the host cores: full head, decode steps of one
+    token each (M = 1, successive rows of xb) until at least min_sec of CPU
+    work (at most max_tokens steps)."""
     from oracle import head as ohead
     from oracle.bytes import head_bytes
+    n = 0
     t = time.perf_counter()
-    ohead.logits(h, xb[:1])
+    while n < min(max_tokens, xb.shape[0]):
+        ohead.logits(h, xb[n:n + 1])
+        n += 1
+        if time.perf_counter() - t >= min_sec:
+            break
     sec = time.perf_counter() - t
     cores = len(os.sched_getaffinity(0))
     threads = int(os.environ.get("OMP_NUM_THREADS", cores))
-    return {"value": head_bytes(h) / sec / 1e9, "unit": "GB/s", "cores": min(cores, threads),
+    return {"value": n * head_bytes(h) / sec / 1e9, "unit": "GB/s", "cores": min(cores, threads),
             "kind": "oracle",
-            "sample": f"fp64 numpy oracle, full Qwen-shaped head, 1 token: {sec:.2f} s "
-                      f"({1 / sec:.3f} tok/s)"}
+            "sample": f"fp64 numpy oracle, full Qwen-shaped head, {n} decode steps of 1 token: "
+                      f"{sec:.2f} s ({n / sec:.3f} tok/s)"}
 
 
 def profile_run(kind, steps):
