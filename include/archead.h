@@ -265,16 +265,22 @@ archead_status archead_logits_argmax(const archead_handle* h, const void* x, int
  *                agreement: rank == 0).
  *   ref, test  device fp32 [M, ld_ref] / [M, ld_test] row-major, ld >= V
  *   kl, sq     device fp32 [M];  ref_idx, rank  device int64 [M] (8-byte aligned)
+ *   ws         device scratch of archead_fidelity_workspace_bytes(M, V)
+ *              bytes, 256-byte aligned, caller-owned (per-chunk partials)
  *   stream     hipStream_t (NULL = the default stream); asynchronous
  * Sums are taken in fp64 over fp32 exponentials in a fixed order (the
- * result is reproducible).  Inputs must be finite.  Needs no handle and no
- * workspace; M = 0 is a no-op.  ARCHEAD_E_INVALID_ARG for a null pointer,
- * M < 0, V < 1, V or M >= 2^31 or ld < V; ARCHEAD_E_MISALIGNED for a
- * misaligned pointer; ARCHEAD_E_HIP when the launch fails. */
+ * result is reproducible).  Inputs must be finite.  M = 0 is a no-op.
+ * ARCHEAD_E_INVALID_ARG for a null pointer, M < 0 or M > 65535, V < 1 or
+ * V >= 2^31, or ld < V; ARCHEAD_E_MISALIGNED for a misaligned pointer;
+ * ARCHEAD_E_WORKSPACE for a short workspace; ARCHEAD_E_HIP when a launch
+ * fails. */
+/* Bytes of workspace archead_logit_fidelity needs for M positions of V
+ * logits (0 for M < 1 or V < 1). */
+size_t archead_fidelity_workspace_bytes(int64_t M, int64_t V);
 archead_status archead_logit_fidelity(const float* ref, int64_t ld_ref, const float* test,
                                       int64_t ld_test, int64_t M, int64_t V, float* kl,
-                                      float* sq, int64_t* ref_idx, int64_t* rank,
-                                      void* stream);
+                                      float* sq, int64_t* ref_idx, int64_t* rank, void* ws,
+                                      size_t ws_bytes, void* stream);
 
 /* Largest M served by the decode GEMV kernel when the MFMA decode kernel
  * does not take the call; larger M use the tiled MFMA kernel (unless

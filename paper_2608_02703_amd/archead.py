@@ -69,10 +69,12 @@ _SIGS = {
     "archead_logits_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_fidelity_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64]),
     "archead_logit_fidelity": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                               ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                              ctypes.c_void_p, ctypes.c_void_p]),
+                                              ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                              ctypes.c_void_p]),
     "archead_set_gemv_max_m": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64]),
     "archead_get_gemv_max_m": (ctypes.c_int64, [ctypes.c_void_p]),
     "archead_set_dec_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
@@ -188,9 +190,13 @@ def logit_fidelity(ref, test):
     idx = torch.empty(M, dtype=torch.int64, device=dev)
     rank = torch.empty(M, dtype=torch.int64, device=dev)
     L = lib()
+    if M == 0:
+        return kl, sq, idx, rank
+    ws = torch.empty(int(L.archead_fidelity_workspace_bytes(M, V)), dtype=torch.uint8, device=dev)
     stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
     _check(L.archead_logit_fidelity(_ptr(ref), ref.stride(0), _ptr(test), test.stride(0), M, V,
-                                    _ptr(kl), _ptr(sq), _ptr(idx), _ptr(rank), stream), L)
+                                    _ptr(kl), _ptr(sq), _ptr(idx), _ptr(rank), _ptr(ws),
+                                    ws.numel(), stream), L)
     return kl, sq, idx, rank
 
 

@@ -205,19 +205,30 @@ def test_packed_bytes_with_8bit_scales(L, V, d, g, rc, rr):
 
 
 
-@pytest.mark.parametrize("M,V,ld_r,ld_t,null,shift,status", [
-    (0, 10, 10, 10, False, 0, ab.OK),                 # empty: no launch
-    (-1, 10, 10, 10, False, 0, ab.E_INVALID_ARG),
-    (2, 0, 10, 10, False, 0, ab.E_INVALID_ARG),
-    (2, 2 ** 31, 2 ** 31, 2 ** 31, False, 0, ab.E_INVALID_ARG),
-    (2, 10, 9, 10, False, 0, ab.E_INVALID_ARG),       # ld < V
-    (2, 10, 10, 9, False, 0, ab.E_INVALID_ARG),
-    (2, 10, 10, 10, True, 0, ab.E_INVALID_ARG),       # null output
-    (2, 10, 10, 10, False, 2, ab.E_MISALIGNED),       # fp32 buffer off by 2 bytes
+@pytest.mark.parametrize("M,V,ld_r,ld_t,null,shift,ws,status", [
+    (0, 10, 10, 10, False, 0, 1 << 20, ab.OK),                # empty: no launch
+    (-1, 10, 10, 10, False, 0, 1 << 20, ab.E_INVALID_ARG),
+    (65536, 10, 10, 10, False, 0, 1 << 30, ab.E_INVALID_ARG),
+    (2, 0, 10, 10, False, 0, 1 << 20, ab.E_INVALID_ARG),
+    (2, 2 ** 31, 2 ** 31, 2 ** 31, False, 0, 1 << 20, ab.E_INVALID_ARG),
+    (2, 10, 9, 10, False, 0, 1 << 20, ab.E_INVALID_ARG),      # ld < V
+    (2, 10, 10, 9, False, 0, 1 << 20, ab.E_INVALID_ARG),
+    (2, 10, 10, 10, True, 0, 1 << 20, ab.E_INVALID_ARG),      # null output
+    (2, 10, 10, 10, False, 2, 1 << 20, ab.E_MISALIGNED),      # fp32 buffer off by 2 bytes
+    (2, 10, 10, 10, False, 0, 16, ab.E_WORKSPACE),            # short workspace
 ])
-def test_logit_fidelity_argument_checks(L, M, V, ld_r, ld_t, null, shift, status):
-    """archead_logit_fidelity rejects bad shapes and pointers before any HIP
-    call (the pointers here are never dereferenced)."""
+def test_logit_fidelity_argument_checks(L, M, V, ld_r, ld_t, null, shift, ws, status):
+    """archead_logit_fidelity rejects bad shapes, pointers and workspaces
+    before any HIP call (the pointers here are never dereferenced)."""
     p = 1 << 20
-    args = [p + shift, ld_r, p, ld_t, M, V, p, p, 0 if null else p, p, None]
+    args = [p + shift, ld_r, p, ld_t, M, V, p, p, 0 if null else p, p, p, ws, None]
     assert L.archead_logit_fidelity(*args) == status, L.archead_last_error()
+
+
+def test_fidelity_workspace_bytes(L):
+    """Per-chunk partials of 48 bytes for every 8192 logits of a row, then a
+    256-aligned fp32 per position; 0 for an invalid shape."""
+    assert L.archead_fidelity_workspace_bytes(0, 10) == 0
+    assert L.archead_fidelity_workspace_bytes(3, 0) == 0
+    assert L.archead_fidelity_workspace_bytes(1, 1) == 256 + 4
+    assert L.archead_fidelity_workspace_bytes(2, 151936) == 2048 + 8   # 2 x 19 x 48 = 1824 -> 2048

@@ -90,6 +90,30 @@ def test_fidelity_ties_and_equal_rows():
     assert rank[2] == 0 and sq[2] == 0 and abs(kl[2]) < 1e-6
 
 
+def test_fidelity_ties_across_chunks():
+    """Equal maxima of the reference in different 8192-logit chunks (the
+    first one wins), and test logits equal to the one at the reference's
+    argmax before it in its own chunk, before it in an earlier chunk, and
+    after it in a later chunk (only the first two count toward the rank);
+    a maximum in the ragged tail of the last chunk."""
+    rng = np.random.default_rng(8)
+    M, V = 4, 3 * 8192 + 5
+    ref = rng.standard_normal((M, V)).astype(np.float32)
+    test = rng.standard_normal((M, V)).astype(np.float32)
+    ref[0, [9000, 20000]] = 50.0
+    test[0, [9000, 50, 8500, 24000]] = 30.0
+    ref[1, [100, 8192 + 100, V - 1]] = 40.0
+    test[1, 100] = 30.0
+    ref[2, V - 2] = 60.0
+    test[2, [0, V - 1]] = test[2, V - 2] = 30.0
+    test[3] = ref[3]
+    say("fidelity ties across chunks")
+    _, rank = check(ref, test)
+    kl, sq, idx, _ = run(ref, test)
+    assert idx.tolist() == [9000, 100, V - 2, int(np.argmax(ref[3]))]
+    assert rank[0] == 2 and rank[1] == 0 and rank[2] == 1 and rank[3] == 0
+
+
 @pytest.mark.parametrize("pads", [(45, 48), (3, 7)])
 def test_fidelity_strided_rows(pads):
     """Leading dimensions larger than V and different on the two sides: rows
