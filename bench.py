@@ -193,8 +193,23 @@ def time_argmax(heads, x, steps, warmup):
     return _timed_loop(step, steps)
 
 
-def time_prefill(heads, x, y, steps, warmup):
-    """(ms per step, mean CE, mean many-token kernel ms)."""
+def time_prefill(heads, x, y, steps, warmup, prepared=True):
+    """(ms per step, mean CE, mean many-token kernel ms).  prepared: the
+    heads keep the many-token kernel's head-derived tables across calls
+    (built once, as a server or evaluation loop does at load time); else
+    every step rebuilds them in its workspace first."""
+    import torch
+    for hd in heads:
+        hd.prepare(prepared)
+    torch.cuda.synchronize()
+    try:
+        return _time_prefill(heads, x, y, steps, warmup)
+    finally:
+        for hd in heads:
+            hd.prepare(False)
+
+
+def _time_prefill(heads, x, y, steps, warmup):
     import torch
     ws = [hd.workspace(x.shape[0], 1, x.device) for hd in heads]
     res = {}
@@ -265,13 +280,16 @@ def sweep(steps, cfg="sweep128k", Ms=None, paths=("auto", "dec", "mid", "gemv", 
     r_r=64) at every M of a list (default its workload's) through each
     kernel: step time, GB/s over the packed bytes and MFMA utilisation
     (algorithmic flops over the bf16 peak).  One JSON line per (M, kernel);
-    "auto" is the library's own choice."""
+    "auto" is the library's own choice.  The heads keep the many-token
+    kernel's head-derived tables across calls (archead_prepare)."""
     import torch
     from oracle.bytes import head_bytes
     from synth import CONFIGS, make_head, make_x
     h = make_head(cfg)
     pbytes = head_bytes(h)
     heads = upload_copies(h, 2 if pbytes > 400e6 else 3)   # copies exceed the 256 MB Infinity Cache
+    for hd in heads:
+        hd.prepare()
     Ms = Ms or CONFIGS[cfg]["Ms"]
     xb = make_x(cfg, max(Ms))
     x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
@@ -301,7 +319,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--clock-warmup", type=float, default=0.5,
                     help="seconds of untimed decode steps before any timing (GPU clock ramp)")
-    ap.add_argument("--prefill-steps", type=int, default=3)
+    ap.add_argument("--prefill-steps", type=int, default=10)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-u8", action="store_true",
@@ -411,7 +429,8 @@ def main():
         xp = torch.from_numpy(make_x("qwen_prefill", Mp).view(np.int16)).view(
             torch.bfloat16).cuda()
         yp = torch.from_numpy(make_targets("qwen_prefill", Mp)).cuda()
-        ms_p, mean_ce, kern_p = time_prefill(heads, xp, yp, args.prefill_steps, 1)
+        ms_u, _, kern_u = time_prefill(heads, xp, yp, args.prefill_steps, 3, prepared=False)
+        ms_p, mean_ce, kern_p = time_prefill(heads, xp, yp, args.prefill_steps, 3)
         flops = mfma_algorithmic_flops(h, Mp)
         tflops = flops / (kern_p * 1e-3) / 1e12
         prefill = {"M": Mp, "ms_per_step": round(ms_p, 4), "tok_s": round(Mp / ms_p * 1e3, 1),
@@ -420,8 +439,14 @@ def main():
                                    "algorithmic_flops": flops,
                                    "achieved_tflops": round(tflops, 1),
                                    "peak_tflops": PEAK_BF16_TFLOPS,
-                                   "frac": round(tflops / PEAK_BF16_TFLOPS, 4)}}
-        log(f"prefill CE M={Mp}: {ms_p:.2f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s; "
+                                   "frac": round(tflops / PEAK_BF16_TFLOPS, 4)},
+                   "head_tables": "prepared once (archead_prepare)",
+                   "per_call_tables": {"ms_per_step": round(ms_u, 4),
+                                       "tok_s": round(Mp / ms_u * 1e3, 1),
+                                       "kernel_ms": round(kern_u, 4)}}
+        log(f"prefill CE M={Mp}, head tables rebuilt per call: {ms_u:.3f} ms/step, "
+            f"{Mp / ms_u * 1e3:.0f} tok/s")
+        log(f"prefill CE M={Mp}: {ms_p:.3f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s; "
             f"many-token kernel {kern_p:.3f} ms = {tflops:.0f} TFLOP/s "
             f"({100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak)")
 

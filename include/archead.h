@@ -305,6 +305,31 @@ archead_status archead_get_dec_range(const archead_handle* h, int64_t* min_m, in
 archead_status archead_set_mid_range(archead_handle* h, int64_t min_m, int64_t max_m);
 archead_status archead_get_mid_range(const archead_handle* h, int64_t* min_m, int64_t* max_m);
 
+/* Head-derived tables of the many-token kernel (the path of archead_logits
+ * and archead_logits_ce at large M) kept across calls.  Every call on that
+ * path otherwise rebuilds, in its workspace and before stage 1, tables that
+ * depend on the head alone: the ratios of consecutive residual group scales
+ * and of the core and correction row scales, s_U and s_A (Section 3.2: the
+ * three summands of the factorized head, accumulated in one fp32 register
+ * chain), the V_c / B_w codes as bf16, and the U_c / A_w codes of each row
+ * side by side.  archead_prepare builds them once into a caller-owned
+ * buffer buf of bytes >= archead_prepared_bytes(h) bytes (device memory,
+ * 256-byte aligned), asynchronously on `stream`; later calls read them from
+ * there.  The caller keeps buf alive and unmodified, and the head's buffers
+ * unchanged, until it detaches it (buf = NULL, bytes = 0) or destroys the
+ * handle; calls on other streams must be ordered after `stream`'s work.
+ * The workspace size of a call does not change.  Results are bit-identical
+ * with and without a prepared buffer.  Same threading rule as
+ * archead_set_gemv_max_m.
+ * archead_prepared_bytes returns 0 for a NULL handle or a head with no
+ * many-token kernel (g % 64 != 0).  archead_prepare: ARCHEAD_E_INVALID_ARG
+ * for a NULL handle or buf = NULL with bytes > 0; ARCHEAD_E_UNSUPPORTED when
+ * the head has no many-token kernel; ARCHEAD_E_MISALIGNED;
+ * ARCHEAD_E_WORKSPACE for a short buffer; ARCHEAD_E_HIP when the launch
+ * fails (the head is then left without a prepared buffer). */
+size_t archead_prepared_bytes(const archead_handle* h);
+archead_status archead_prepare(archead_handle* h, void* buf, size_t bytes, void* stream);
+
 /* Profiling hook: when start and stop are non-NULL hipEvent_t handles
  * (created by the caller on the handle's device), every later compute call
  * attaches `start` to the dispatch of the kernel that streams the packed head

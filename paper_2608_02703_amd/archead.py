@@ -85,6 +85,9 @@ _SIGS = {
                                              ctypes.POINTER(ctypes.c_int64)]),
     "archead_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p,
                                                  ctypes.c_void_p]),
+    "archead_prepared_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
+    "archead_prepare": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                       ctypes.c_void_p]),
     "archead_packed_bytes": (ctypes.c_uint64, [ctypes.POINTER(Desc)]),
     "archead_pack_int4": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                          ctypes.c_void_p]),
@@ -239,6 +242,7 @@ class PackedHead:
                                         ctypes.byref(h)), self._lib)
         self.handle = h
         self._ws = {}
+        self._prep = None
 
     @classmethod
     def from_arrays(cls, h, device="cuda"):
@@ -305,6 +309,23 @@ class PackedHead:
         p0 = ctypes.c_void_p(start.cuda_event) if start is not None else None
         p1 = ctypes.c_void_p(stop.cuda_event) if stop is not None else None
         _check(self._lib.archead_set_timing_events(self.handle, p0, p1), self._lib)
+
+    def prepare(self, enable: bool = True):
+        """Keep the many-token kernel's head-derived tables in a buffer owned
+        by this object (built once, on the current stream), or drop it."""
+        import torch
+        if not enable:
+            _check(self._lib.archead_prepare(self.handle, None, 0, None), self._lib)
+            self._prep = None
+            return
+        n = int(self._lib.archead_prepared_bytes(self.handle))
+        if n == 0:
+            raise ValueError("this head shape has no many-token kernel")
+        dev = torch.device("cuda", torch.cuda.current_device())
+        buf = torch.empty(n, dtype=torch.uint8, device=dev)
+        _check(self._lib.archead_prepare(self.handle, _ptr(buf), n, self._stream(dev)),
+               self._lib)
+        self._prep = buf
 
     def workspace_bytes(self, M: int, op: int = OP_LOGITS) -> int:
         return int(self._lib.archead_workspace_bytes(self.handle, M, op))

@@ -2807,6 +2807,30 @@ static size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 
 int exp_chunks(int64_t r) { return int((r + kExpDims - 1) / kExpDims); }   // stages per part
 
+// The many-token kernel stages 64 codes of one scale group at a time.
+static bool mfma_ok(const archead_handle* h) { return h->desc.g % 64 == 0; }
+
+PrepLayout prep_layout(const archead_handle* h) {
+  PrepLayout p;
+  if (!h) return p;
+  const archead_desc& d = h->desc;
+  const size_t ngrp = size_t(d.d / d.g);
+  const size_t nslot = ngrp + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
+  const size_t nch = size_t(exp_chunks(d.r_c) + exp_chunks(d.r_r));
+  const size_t n_vt = size_t((d.V + kTN - 1) / kTN);
+  size_t off = 0;
+  p.rat_off = off;
+  off = align256(off + sizeof(float) * n_vt * nslot * kTN);
+  p.fin_off = off;
+  off = align256(off + sizeof(float) * n_vt * kTN);
+  p.wbf_off = off;
+  off = align256(off + sizeof(uint16_t) * size_t(d.r_c + d.r_r) * size_t(d.d));
+  p.uc_off = off;
+  off = align256(off + size_t(d.V) * nch * 32);                    // [c|c] x 16
+  p.total = off;
+  return p;
+}
+
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
   WsLayout w;
   if (!h || M <= 0) return w;
@@ -2824,19 +2848,17 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
     const size_t ngrp = size_t(d.d / d.g);
     const size_t nslot = ngrp + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
     const size_t nch = size_t(exp_chunks(d.r_c) + exp_chunks(d.r_r));
-    const size_t n_mt = size_t((M + kTM - 1) / kTM), n_vt = size_t((d.V + kTN - 1) / kTN);
+    const size_t n_mt = size_t((M + kTM - 1) / kTM);
     w.ts_off = off;
     off = align256(off + sizeof(uint16_t) * size_t(M) * nch * 64);   // [hi|mid|lo|0] x 16
     w.gb_off = off;
     off = align256(off + sizeof(float) * n_mt * nslot * kTM);
-    w.rat_off = off;
-    off = align256(off + sizeof(float) * n_vt * nslot * kTN);
-    w.fin_off = off;
-    off = align256(off + sizeof(float) * n_vt * kTN);
-    w.wbf_off = off;
-    off = align256(off + sizeof(uint16_t) * size_t(d.r_c + d.r_r) * size_t(d.d));
-    w.uc_off = off;
-    off = align256(off + size_t(d.V) * nch * 32);                    // [c|c] x 16
+    const PrepLayout pl = prep_layout(h);
+    w.rat_off = off + pl.rat_off;
+    w.fin_off = off + pl.fin_off;
+    w.wbf_off = off + pl.wbf_off;
+    w.uc_off = off + pl.uc_off;
+    off += pl.total;
   }
   if (op == ARCHEAD_OP_LOGITS_CE || op == ARCHEAD_OP_ARGMAX) {
     // GEMV: all CE passes share one grid (the smallest of the variants
@@ -2890,11 +2912,20 @@ archead_status check_call(const archead_handle* h, const void* x, int64_t M, int
   return ARCHEAD_OK;
 }
 
-// MFMA path prologue: the tile-major residual scales and the bf16 factor
-// codes, then stage 1 (t and the group biases).
-archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int64_t M,
-                                    int64_t ldx, const WsLayout& w, char* ws, hipStream_t s) {
+// Start of the block of head-derived tables a call of the many-token
+// kernel reads: the prepared buffer when the head has one, else the call's
+// workspace.
+char* prep_base(const archead_handle* h, const WsLayout& w, char* ws) {
+  char* p = h->prep.load(std::memory_order_acquire);
+  return p ? p : ws + w.rat_off;
+}
+
+// The head-derived tables (tile-major residual scale ratios, final scales,
+// bf16 factor codes of V_c / B_w, paired U_c / A_w codes) into the block at
+// base, laid out as prep_layout says.
+archead_status launch_prep(const archead_handle* h, char* base, hipStream_t s) {
   const archead_desc& d = h->desc;
+  const PrepLayout pl = prep_layout(h);
   const int R = int(d.r_c + d.r_r);
   const int nch_u = exp_chunks(d.r_c), nch = nch_u + exp_chunks(d.r_r);
   PrepArgs p;
@@ -2907,28 +2938,42 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
   p.ngrp = int(d.d / d.g);
   p.nslot = p.ngrp + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
   p.n_vt = (d.V + kTN - 1) / kTN;
-  p.ratio = reinterpret_cast<float*>(ws + w.rat_off);
-  p.fin = reinterpret_cast<float*>(ws + w.fin_off);
+  p.ratio = reinterpret_cast<float*>(base + pl.rat_off);
+  p.fin = reinterpret_cast<float*>(base + pl.fin_off);
   p.cv = static_cast<const int8_t*>(h->ptrs.core_v);
   p.cb = static_cast<const int8_t*>(h->ptrs.corr_b);
   p.rc = int(d.r_c); p.rr = int(d.r_r); p.d = int(d.d);
-  p.wbf = reinterpret_cast<uint16_t*>(ws + w.wbf_off);
+  p.wbf = reinterpret_cast<uint16_t*>(base + pl.wbf_off);
   p.cu = static_cast<const int8_t*>(h->ptrs.core_u);
   p.ca = static_cast<const int8_t*>(h->ptrs.corr_a);
   p.urow = nch * 32;
   p.rc_pad = nch_u * kExpDims;
-  p.ucodes = reinterpret_cast<int8_t*>(ws + w.uc_off);
+  p.ucodes = reinterpret_cast<int8_t*>(base + pl.uc_off);
   const int64_t work = std::max({p.n_vt * kTN, int64_t(R) * d.d / 8, d.V * (p.urow / 16)});
   const int64_t pblocks =
       std::max<int64_t>(1, std::min<int64_t>((work + kBlock - 1) / kBlock, 4 * int64_t(h->n_cu)));
   hipLaunchKernelGGL(k_prep, dim3(unsigned(pblocks)), dim3(kBlock), 0, s, p);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "prologue launch");
+  return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "prologue launch");
+}
 
+// MFMA path prologue: the head-derived tables (unless the head has them
+// prepared), then stage 1 (t and the group biases).
+archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int64_t M,
+                                    int64_t ldx, const WsLayout& w, char* ws, hipStream_t s) {
+  const archead_desc& d = h->desc;
+  const int R = int(d.r_c + d.r_r);
+  const int nch_u = exp_chunks(d.r_c), nch = nch_u + exp_chunks(d.r_r);
+  const int nslot = int(d.d / d.g) + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
+  char* pb = prep_base(h, w, ws);
+  if (!h->prep.load(std::memory_order_acquire)) {
+    archead_status st = launch_prep(h, pb, s);
+    if (st != ARCHEAD_OK) return st;
+  }
   Stage1MArgs a;
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx; a.M = M; a.d = int(d.d); a.g = int(d.g);
-  a.wbf = p.wbf;
+  a.wbf = reinterpret_cast<const uint16_t*>(pb + prep_layout(h).wbf_off);
   a.sv = static_cast<const uint16_t*>(h->ptrs.core_v_scale);
   a.gv = int(d.r_c ? d.g_v : d.d); a.rc = int(d.r_c);
   a.sb = static_cast<const uint16_t*>(h->ptrs.corr_b_scale);
@@ -2936,13 +2981,13 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
   a.tsplit = reinterpret_cast<uint16_t*>(ws + w.ts_off);
   a.nch = nch; a.nch_u = nch_u;
   a.gbias = reinterpret_cast<float*>(ws + w.gb_off);
-  a.nslot = p.nslot;
+  a.nslot = nslot;
   const int64_t mblocks = (M + kS1MTok - 1) / kS1MTok;
   const int64_t rblocks = R > 0 ? (R + kS1MCols - 1) / kS1MCols : 1;
   if (mblocks > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "M too large");
   hipLaunchKernelGGL(k_stage1m, dim3(unsigned(mblocks), unsigned(rblocks)), dim3(kS1MBlock), 0,
                      s, a);
-  e = hipGetLastError();
+  const hipError_t e = hipGetLastError();
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "stage-1 launch");
 }
 
@@ -3193,10 +3238,12 @@ MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ld
   a.x = static_cast<const uint16_t*>(x);
   a.ldx = ldx;
   a.tsplit = reinterpret_cast<const uint16_t*>(ws + w.ts_off);
-  a.ucodes = reinterpret_cast<const int8_t*>(ws + w.uc_off);
+  const PrepLayout pl = prep_layout(h);
+  const char* pb = prep_base(h, w, ws);
+  a.ucodes = reinterpret_cast<const int8_t*>(pb + pl.uc_off);
   a.gbias = reinterpret_cast<const float*>(ws + w.gb_off);
-  a.ratio = reinterpret_cast<const float*>(ws + w.rat_off);
-  a.fin = reinterpret_cast<const float*>(ws + w.fin_off);
+  a.ratio = reinterpret_cast<const float*>(pb + pl.rat_off);
+  a.fin = reinterpret_cast<const float*>(pb + pl.fin_off);
   a.M = M; a.V = d.V;
   a.d = int(d.d); a.g = int(d.g);
   a.nslot = int(d.d / d.g) + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
@@ -3344,6 +3391,7 @@ archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs
   for (auto& c : h->grid_cache) c.store(0);
   h->ev_start.store(nullptr);
   h->ev_stop.store(nullptr);
+  h->prep.store(nullptr);
   *out = h;
   return ARCHEAD_OK;
 }
@@ -3353,6 +3401,30 @@ void archead_destroy(archead_handle* h) { delete h; }
 size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op) {
   if (!h || M <= 0) return 0;
   return ws_layout(h, M, op).total;
+}
+
+size_t archead_prepared_bytes(const archead_handle* h) {
+  if (!h || !mfma_ok(h)) return 0;
+  return prep_layout(h).total;
+}
+
+archead_status archead_prepare(archead_handle* h, void* buf, size_t bytes, void* stream) {
+  clear_error();
+  if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
+  if (!buf) {
+    if (bytes) return fail(ARCHEAD_E_INVALID_ARG, "buf is NULL with bytes > 0");
+    h->prep.store(nullptr, std::memory_order_release);
+    return ARCHEAD_OK;
+  }
+  if (!mfma_ok(h)) return fail(ARCHEAD_E_UNSUPPORTED, "the head shape has no many-token kernel");
+  if (!aligned(buf, 256)) return fail(ARCHEAD_E_MISALIGNED, "buf must be 256-byte aligned");
+  const size_t need = prep_layout(h).total;
+  if (bytes < need) return fail(ARCHEAD_E_WORKSPACE, "buffer %zu < %zu bytes", bytes, need);
+  h->prep.store(nullptr, std::memory_order_release);
+  archead_status st = launch_prep(h, static_cast<char*>(buf), static_cast<hipStream_t>(stream));
+  if (st != ARCHEAD_OK) return st;
+  h->prep.store(static_cast<char*>(buf), std::memory_order_release);
+  return ARCHEAD_OK;
 }
 
 archead_status archead_logits(const archead_handle* h, const void* x, int64_t M, int64_t ldx,

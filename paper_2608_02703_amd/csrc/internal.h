@@ -25,6 +25,9 @@ struct archead_handle {
   // caller-owned hipEvent_t pair recorded around the head-streaming kernel
   std::atomic<void*> ev_start;
   std::atomic<void*> ev_stop;
+  // caller-owned device buffer holding the many-token kernel's tables
+  // derived from the head (archead_prepare), or null: built per call
+  std::atomic<char*> prep;
 };
 
 namespace archead {
@@ -64,6 +67,15 @@ struct WsLayout {
   int64_t n_part = 0;
 };
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op);
+
+// The many-token kernel's tables that depend on the head only (scale
+// ratios, final scales, bf16 V_c / B_w codes, paired U_c / A_w codes):
+// offsets from the start of their block, in the workspace or in a prepared
+// buffer (the same layout in both).
+struct PrepLayout {
+  size_t rat_off = 0, fin_off = 0, wbf_off = 0, uc_off = 0, total = 0;
+};
+PrepLayout prep_layout(const archead_handle* h);
 bool use_gemv(const archead_handle* h, int64_t M);
 
 // MFMA decode kernel: its LDS layout for a pass of `tok` tokens, the most

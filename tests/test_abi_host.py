@@ -169,6 +169,8 @@ def test_null_handle_calls(L):
                                None) == ab.E_INVALID_ARG
     assert L.archead_set_gemv_max_m(None, 3) == ab.E_INVALID_ARG
     assert L.archead_get_gemv_max_m(None) == -1
+    assert L.archead_prepared_bytes(None) == 0
+    assert L.archead_prepare(None, None, 0, None) == ab.E_INVALID_ARG
     assert L.archead_set_mid_range(None, 2, 3) == ab.E_INVALID_ARG
     assert L.archead_get_mid_range(None, ctypes.byref(ctypes.c_int64()),
                                    ctypes.byref(ctypes.c_int64())) == ab.E_INVALID_ARG
