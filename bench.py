@@ -300,7 +300,7 @@ def sweep(steps, cfg="sweep128k", Ms=None, paths=("auto", "dec", "mid", "gemv", 
                 continue          # 4 tokens per pass: far off the crossover
             for hd in heads:
                 hd.force_path(path)
-            n = steps if M <= 64 else max(3, steps // 8)
+            n = steps if M <= 64 else max(10, steps // 4)
             ms, kern, _ = time_decode(heads, x_all[:M], n, 3)
             flops = mfma_algorithmic_flops(h, M)
             print(json.dumps({"sweep": cfg, "M": M, "kernel": path,
