@@ -170,7 +170,8 @@ void archead_destroy(archead_handle* h);
  * MFMA path split into three bf16 parts), on the tiled path also per-call
  * tables derived from the head (group-scale ratios, the per-group sums of x,
  * the factor codes as bf16 and the U_c / A_w codes side by side: about
- * V * (r_c + r_r + 4 * (d/g + 3)) bytes), and for the CE call the
+ * V * (r_c + r_r + 4 * (d/g + 3)) bytes, used only while the head has no
+ * prepared buffer, see archead_prepare), and for the CE call the
  * per-vocabulary-tile softmax partials.  Returns 0 for a NULL handle or
  * M < 0. */
 size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op);
