@@ -18,8 +18,8 @@ to their sustained-load state (--clock-warmup; a cold GPU runs the first
 ~100 ms of steps ~10% slower); then each line does its own --warmup steps
 and times exactly --steps steps.
 
-Prints one JSON line (rank 0, N=1).  --gpus N > 1 is refused: this build
-runs on one GPU.  --profile decode|prefill runs the same work without timing
+Prints one JSON line (rank 0, N=1).  --gpus N > 1 is refused: the
+benchmark runs on one GPU.  --profile decode|prefill runs the same work without timing
 or JSON, for rocprofv3 (the decode form first copies 256 MiB once, the
 calibration kernel for the HBM byte counters).
 """
@@ -336,8 +336,8 @@ def main():
     ap.add_argument("--sweep-paths", default="auto,dec,mid,gemv,tiled")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py: this build runs on one GPU only; multi-GPU (vocab-parallel) "
-              "runs are not part of it", file=sys.stderr)
+        print("bench.py: runs on one GPU only; multi-GPU (vocab-parallel) "
+              "runs are not implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch

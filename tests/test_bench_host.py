@@ -24,7 +24,7 @@ def _qwen():
 
 @pytest.mark.parametrize("argv,env", [(["--gpus", "2"], {}), ([], {"WORLD_SIZE": "8"})])
 def test_more_than_one_gpu_is_refused(argv, env):
-    """Several GPUs are outside this build: the bench exits with status 2
+    """More than one GPU is refused: the bench exits with status 2
     and says so, before touching torch or a device."""
     r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), *argv],
                        env={**os.environ, **env}, capture_output=True, text=True, timeout=120)
