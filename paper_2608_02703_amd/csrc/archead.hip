@@ -1512,6 +1512,8 @@ struct Stage1MArgs {
   int nch, nch_u;
   float* gbias;            // [n_mt][nslot][kTM]
   int nslot;
+  int ksplit;              // workgroups along d (grid z); > 1: fp32 partials in tpart
+  float* tpart;            // [ksplit][M][R] when ksplit > 1
 };
 
 constexpr int kS1MTok = 16, kS1MCols = 64, kS1MBlock = 512, kS1MWaves = kS1MBlock / 64;
@@ -1525,7 +1527,10 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
   const int64_t tok0 = int64_t(blockIdx.x) * kS1MTok;
   const int kb = blockIdx.y * kS1MCols;           // first factor row of this workgroup
   const int ngrp = a.d / a.g, cpg = a.g / 32;
-  const int c0 = (wid * ngrp / kS1MWaves) * cpg, c1 = ((wid + 1) * ngrp / kS1MWaves) * cpg;
+  // this workgroup's residual groups (split blockIdx.z of ksplit equal
+  // parts), dealt to its waves
+  const int ks = blockIdx.z, gps = ngrp / a.ksplit, g0 = ks * gps;
+  const int c0 = (g0 + wid * gps / kS1MWaves) * cpg, c1 = (g0 + (wid + 1) * gps / kS1MWaves) * cpg;
   const int64_t mrow = tok0 + lr < a.M ? tok0 + lr : a.M - 1;
   const uint16_t* xrow = a.x + mrow * a.ldx + 8 * q;
   const bool do_bias = blockIdx.y == 0;
@@ -1591,7 +1596,7 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) B[nb] = Bn[nb], s[nb] = sn[nb];
   }
-  if (do_bias) {
+  if (do_bias && ks == 0) {
     // zero biases of the expansion slots and zero padding of the split t
     const int nz = a.nslot - ngrp;
     for (int e = threadIdx.x; e < kS1MTok * nz; e += kS1MBlock) {
@@ -1621,6 +1626,10 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
       float v = red[0][tt][c];
 #pragma unroll
       for (int w = 1; w < kS1MWaves; ++w) v += red[w][tt][c];
+      if (a.ksplit > 1) {
+        a.tpart[(int64_t(ks) * a.M + m) * R + k] = v;
+        continue;
+      }
       const __bf16 hi = (__bf16)v;
       const float r1 = v - float(hi);
       const __bf16 md = (__bf16)r1;
@@ -1632,6 +1641,27 @@ __global__ __launch_bounds__(kS1MBlock) void k_stage1m(Stage1MArgs a) {
       dst[32] = __builtin_bit_cast(uint16_t, lo);
     }
   }
+}
+
+// t[m][k] as the sum of the ksplit partials in split order, then split
+// into three bf16 parts as k_stage1m does when it is not split.
+__global__ __launch_bounds__(kBlock) void k_stage1m_fin(Stage1MArgs a) {
+  const int R = a.rc + a.rr;
+  const int64_t e = int64_t(blockIdx.x) * kBlock + threadIdx.x;
+  if (e >= a.M * R) return;
+  const int64_t m = e / R;
+  const int k = int(e % R);
+  float v = a.tpart[m * R + k];
+  for (int ks = 1; ks < a.ksplit; ++ks) v += a.tpart[(int64_t(ks) * a.M + m) * R + k];
+  const __bf16 hi = (__bf16)v;
+  const float r1 = v - float(hi);
+  const __bf16 md = (__bf16)r1;
+  const __bf16 lo = (__bf16)(r1 - float(md));
+  const int dim = k < a.rc ? k : kExpDims * a.nch_u + (k - a.rc);
+  uint16_t* dst = a.tsplit + (m * a.nch + dim / kExpDims) * 64 + dim % kExpDims;
+  dst[0] = __builtin_bit_cast(uint16_t, hi);
+  dst[16] = __builtin_bit_cast(uint16_t, md);
+  dst[32] = __builtin_bit_cast(uint16_t, lo);
 }
 
 // ---------------------------------------------------------------- CE merge
@@ -2810,6 +2840,21 @@ int exp_chunks(int64_t r) { return int((r + kExpDims - 1) / kExpDims); }   // st
 // The many-token kernel stages 64 codes of one scale group at a time.
 static bool mfma_ok(const archead_handle* h) { return h->desc.g % 64 == 0; }
 
+// Workgroups along d of the tiled path's stage 1: doubled (while every wave
+// keeps at least one residual group and the groups split evenly) until the
+// grid has 256 workgroups, so a call with few token blocks still spreads
+// the factor-code reads over the chip.
+static int s1_ksplit(const archead_handle* h, int64_t M) {
+  const archead_desc& d = h->desc;
+  const int64_t R = d.r_c + d.r_r;
+  if (R == 0 || M <= 0) return 1;
+  const int64_t ngrp = d.d / d.g;
+  const int64_t blocks = ((M + kS1MTok - 1) / kS1MTok) * ((R + kS1MCols - 1) / kS1MCols);
+  int ks = 1;
+  while (blocks * ks < 256 && ngrp % (2 * ks) == 0 && ngrp / (2 * ks) >= kS1MWaves) ks *= 2;
+  return ks;
+}
+
 PrepLayout prep_layout(const archead_handle* h) {
   PrepLayout p;
   if (!h) return p;
@@ -2859,6 +2904,11 @@ WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
     w.wbf_off = off + pl.wbf_off;
     w.uc_off = off + pl.uc_off;
     off += pl.total;
+    const int ks = s1_ksplit(h, M);
+    if (ks > 1) {
+      w.s1p_off = off;
+      off = align256(off + sizeof(float) * size_t(ks) * size_t(M) * size_t(d.r_c + d.r_r));
+    }
   }
   if (op == ARCHEAD_OP_LOGITS_CE || op == ARCHEAD_OP_ARGMAX) {
     // GEMV: all CE passes share one grid (the smallest of the variants
@@ -2982,12 +3032,20 @@ archead_status launch_mfma_prologue(const archead_handle* h, const void* x, int6
   a.nch = nch; a.nch_u = nch_u;
   a.gbias = reinterpret_cast<float*>(ws + w.gb_off);
   a.nslot = nslot;
+  a.ksplit = s1_ksplit(h, M);
+  a.tpart = reinterpret_cast<float*>(ws + w.s1p_off);
   const int64_t mblocks = (M + kS1MTok - 1) / kS1MTok;
   const int64_t rblocks = R > 0 ? (R + kS1MCols - 1) / kS1MCols : 1;
   if (mblocks > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "M too large");
-  hipLaunchKernelGGL(k_stage1m, dim3(unsigned(mblocks), unsigned(rblocks)), dim3(kS1MBlock), 0,
-                     s, a);
-  const hipError_t e = hipGetLastError();
+  hipLaunchKernelGGL(k_stage1m, dim3(unsigned(mblocks), unsigned(rblocks), unsigned(a.ksplit)),
+                     dim3(kS1MBlock), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e == hipSuccess && a.ksplit > 1) {
+    const int64_t n = M * R;
+    hipLaunchKernelGGL(k_stage1m_fin, dim3(unsigned((n + kBlock - 1) / kBlock)), dim3(kBlock), 0,
+                       s, a);
+    e = hipGetLastError();
+  }
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "stage-1 launch");
 }
 

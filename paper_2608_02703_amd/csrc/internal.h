@@ -60,6 +60,7 @@ struct WsLayout {
   size_t fin_off = 0;    // fp32 [n_vt][256] final scales
   size_t wbf_off = 0;    // bf16 [r_c + r_r][d] factor codes of V_c and B_w
   size_t uc_off = 0;     // int8 [V][blocks][2][16] codes of U_c and A_w, padded, twice
+  size_t s1p_off = 0;    // fp32 [ksplit][M][r_c + r_r] stage-1 partials (split along d)
   size_t part_off = 0;   // float2 [M, n_part] (CE)
   size_t tgt_off = 0;    // fp32 [M] (CE)
   size_t pidx_off = 0;   // int32 [M, n_part] (argmax)

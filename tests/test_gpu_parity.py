@@ -548,10 +548,13 @@ def test_zero_scales_many_token_kernel():
 
 
 @pytest.mark.parametrize("V,d,g,M", [(1000, 512, 64, 130), (777, 256, 64, 33),
-                                     (300, 1024, 256, 5), (513, 192, 64, 300)])
+                                     (300, 1024, 256, 5), (513, 192, 64, 300),
+                                     (1000, 2048, 64, 40), (777, 1536, 64, 17)])
 def test_mfma_ragged_tiles(V, d, g, M):
     """Token and vocabulary counts that leave partial MFMA tiles; ranks that
-    are not multiples of 32; row strides wider than the rows."""
+    are not multiples of 32; row strides wider than the rows.  The last two
+    shapes have few token blocks and 32 / 24 residual groups, so stage 1 is
+    split along d over 4 / 2 workgroups and summed in a second kernel."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("tiny", V=V, d=d, g=g, rc=40, rr=12)
     x = make_x("tiny", M, d=d, basis="identity")
