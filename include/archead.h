@@ -195,7 +195,7 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *     which streams the head once per pass of up to 16 tokens (fewer when
  *     16 rows of x do not fit in LDS);
  *   - otherwise M in the range of archead_set_mid_range (default: from one
- *     past the decode kernel's range to 96) with g in {64, 128},
+ *     past the decode kernel's range to 64) with g in {64, 128},
  *     d % 512 == 0, d/g <= 64, r_c and r_r multiples of 4 and at most 128
  *     each: the several-token kernel, which streams the head once per tile
  *     of up to 32 tokens (x held in LDS in windows of 256 elements of d);
