@@ -64,12 +64,18 @@ def upload_copies(h, n):
     return heads
 
 
-def decode_algorithmic_bytes(h, M):
-    """Bytes one decode launch must move: the whole packed head once (the
-    residual codes and scales, the factors and their scales, V_c and B_w for
-    the in-launch stage 1), x, and the fp32 logits it writes."""
-    from oracle.bytes import head_bytes
-    return head_bytes(h) + M * h.d * 2 + M * h.V * 4
+def lib_packed_bytes(ph):
+    """The packed head's persistent bytes as the library counts them
+    (archead_packed_bytes: sum of element count x element size)."""
+    from paper_2608_02703_amd import packed_bytes
+    return packed_bytes(ph.desc)
+
+
+def decode_algorithmic_bytes(pbytes, h, M):
+    """Bytes one decode launch must move: the whole packed head once (pbytes:
+    the residual codes and scales, the factors and their scales, V_c and B_w
+    for the in-launch stage 1), x, and the fp32 logits it writes."""
+    return pbytes + M * h.d * 2 + M * h.V * 4
 
 
 def lanes_per_row(h):
@@ -123,6 +129,24 @@ def _timed_loop(fn, steps):
     return t0.elapsed_time(t1) / steps
 
 
+def _step_times(fn, steps):
+    """Per-step durations (ms) from events recorded between consecutive
+    steps on the stream (a separate pass from the unmarked timed loop)."""
+    import torch
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    for i in range(steps):
+        ev[i].record()
+        fn(i)
+    ev[steps].record()
+    torch.cuda.synchronize()
+    return [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+
+
+def _pct(v, q):
+    return float(np.percentile(np.asarray(v, dtype=np.float64), q))
+
+
 def _kernel_times(heads, fn, steps):
     """Per-call durations (ms) of the head-streaming kernel: HIP events
     attached to its dispatch (a separate pass; the markers cost a few us per
@@ -163,8 +187,9 @@ def clock_warmup(heads, x, seconds):
     return n
 
 
-def time_decode(heads, x, steps, warmup, ws=None):
-    """(ms per step, mean head-kernel ms, median head-kernel ms)."""
+def time_decode(heads, x, steps, warmup, ws=None, percentiles=False):
+    """(ms per step, mean head-kernel ms, median head-kernel ms[, step-time
+    percentiles p10 / p50 / p90 in ms])."""
     import torch
     M = x.shape[0]
     outs = [torch.empty((M, heads[0].V), device="cuda") for _ in heads]
@@ -177,7 +202,78 @@ def time_decode(heads, x, steps, warmup, ws=None):
         step(i)
     ms = _timed_loop(step, steps)
     kern = _kernel_times(heads, step, min(steps, 100))
-    return ms, float(np.mean(kern)), float(np.median(kern))
+    out = (ms, float(np.mean(kern)), float(np.median(kern)))
+    if percentiles:
+        st = _step_times(step, steps)
+        out += ({"p10": _pct(st, 10), "p50": _pct(st, 50), "p90": _pct(st, 90)},)
+    return out
+
+
+class ClockSampler:
+    """Samples the GPU's current shader clock (the level marked '*' in the
+    driver's pp_dpm_sclk table) from a host thread while the GPU runs the
+    timed steps; None where the table is not readable."""
+
+    def __init__(self, period=0.01):
+        import glob
+        import threading
+        self.paths = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.period = period
+        self.samples = []
+        self._stop = threading.Event()
+        self._t = threading.Thread(target=self._run, daemon=True)
+
+    def _read(self):
+        for p in self.paths:
+            try:
+                for line in open(p):
+                    if line.rstrip().endswith("*"):
+                        m = re.search(r"(\d+)\s*[Mm][Hh]z", line)
+                        if m:
+                            return int(m.group(1))
+            except OSError:
+                continue
+        return None
+
+    def _run(self):
+        while not self._stop.is_set():
+            v = self._read()
+            if v is not None:
+                self.samples.append(v)
+            self._stop.wait(self.period)
+
+    def __enter__(self):
+        if self.paths:
+            self._t.start()
+        return self
+
+    def __exit__(self, *a):
+        self._stop.set()
+        if self.paths:
+            self._t.join()
+
+    def summary(self):
+        if not self.samples:
+            return {"sclk_mhz": None, "source": "pp_dpm_sclk not readable"}
+        return {"sclk_mhz_median": _pct(self.samples, 50), "sclk_mhz_min": min(self.samples),
+                "sclk_mhz_max": max(self.samples), "samples": len(self.samples),
+                "source": "pp_dpm_sclk current level, sampled during the decode M=1 timing"}
+
+
+def copy_bandwidth(nbytes=512 << 20, iters=20):
+    """Device-to-device copy of nbytes (torch copy_): GB/s counting the bytes
+    read and written, the HBM rate a plain streaming kernel reaches here."""
+    import torch
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda").fill_(1)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    ms = _timed_loop(lambda i: dst.copy_(src), iters)
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"bytes": nbytes, "ms": round(ms, 4), "gbs_read_plus_write": round(2 * nbytes / ms / 1e6, 1),
+            "frac_of_8tbs": round(2 * nbytes / ms / 1e6 / PEAK_HBM_GBS, 4),
+            "op": "torch copy_ of a 512 MiB device buffer"}
 
 
 def time_argmax(heads, x, steps, warmup):
@@ -194,7 +290,7 @@ def time_argmax(heads, x, steps, warmup):
 
 
 def time_prefill(heads, x, y, steps, warmup, prepared=True):
-    """(ms per step, mean CE, mean many-token kernel ms).  prepared: the
+    """(ms per step, mean CE, median many-token kernel ms).  prepared: the
     heads keep the many-token kernel's head-derived tables across calls
     (built once, as a server or evaluation loop does at load time); else
     every step rebuilds them in its workspace first."""
@@ -221,19 +317,27 @@ def _time_prefill(heads, x, y, steps, warmup):
         step(i)
     ms = _timed_loop(step, steps)
     kern = _kernel_times(heads, step, steps)
-    return ms, float(res["ce"][1].cpu()[0]), float(np.mean(kern))
+    return ms, float(res["ce"][1].cpu()[0]), float(np.median(kern))
 
 
 def ms1_for_dense(res):
     return res[1][0]
 
 
-def cpu_baseline(h, xb, min_sec=10.0, max_tokens=16):
-    """The fp64 oracle on the host cores: full head, decode steps of one
-    token each (M = 1, successive rows of xb) until at least min_sec of CPU
-    work (at most max_tokens steps)."""
+def _oracle_threads():
+    cores = len(os.sched_getaffinity(0))
+    return min(cores, int(os.environ.get("OMP_NUM_THREADS", cores)))
+
+
+def cpu_baseline(h, pbytes, xb, min_sec=10.0, max_tokens=16, legs=True):
+    """The fp64 oracle on the host cores (the oracle as it stands, never
+    tuned): the headline leg runs decode steps of one token each over the
+    full Qwen-shaped head (successive rows of xb) until at least min_sec of
+    CPU work (at most max_tokens steps).  With legs, two bounded samples
+    more: one decode token over the full Gemma-shaped head (logits), and the
+    prefill / CE workload's first 256 tokens over the Qwen-shaped head (logits
+    then CE), each timed around the oracle call alone."""
     from oracle import head as ohead
-    from oracle.bytes import head_bytes
     n = 0
     t = time.perf_counter()
     while n < min(max_tokens, xb.shape[0]):
@@ -242,37 +346,93 @@ def cpu_baseline(h, xb, min_sec=10.0, max_tokens=16):
         if time.perf_counter() - t >= min_sec:
             break
     sec = time.perf_counter() - t
-    cores = len(os.sched_getaffinity(0))
-    threads = int(os.environ.get("OMP_NUM_THREADS", cores))
-    return {"value": n * head_bytes(h) / sec / 1e9, "unit": "GB/s", "cores": min(cores, threads),
-            "kind": "oracle",
-            "sample": f"fp64 numpy oracle, full Qwen-shaped head, {n} decode steps of 1 token: "
-                      f"{sec:.2f} s ({n / sec:.3f} tok/s)"}
+    out = {"value": n * pbytes / sec / 1e9, "unit": "GB/s", "cores": _oracle_threads(),
+           "kind": "oracle",
+           "sample": f"fp64 numpy oracle, full Qwen-shaped head, {n} decode steps of 1 token: "
+                     f"{sec:.2f} s ({n / sec:.3f} tok/s)"}
+    if not legs:
+        return out
+    from oracle.bytes import head_bytes
+    from synth import make_head, make_targets, make_x
+    hg = make_head("gemma")
+    xg = make_x("gemma", 1)
+    t = time.perf_counter()
+    ohead.logits(hg, xg)
+    sg = time.perf_counter() - t
+    out["gemma_decode_m1"] = {"sec": round(sg, 3), "tok_s": round(1 / sg, 4),
+                              "gbs_packed": round(head_bytes(hg) / sg / 1e9, 4),
+                              "sample": "1 token, full Gemma-shaped head (V=262144, d=2560), logits"}
+    del hg
+    Mc = 256
+    xp = make_x("qwen_prefill", Mc)
+    yp = make_targets("qwen_prefill", Mc)
+    t = time.perf_counter()
+    ce = ohead.cross_entropy(ohead.logits(h, xp), yp)
+    sp = time.perf_counter() - t
+    out["qwen_prefill_ce"] = {"sec": round(sp, 3), "tok_s": round(Mc / sp, 2),
+                              "mean_ce_sample": round(float(ce.mean()), 6),
+                              "sample": f"first {Mc} of the 4096 prefill tokens, full Qwen-shaped "
+                                        "head, logits then CE"}
+    return out
 
 
 def profile_run(kind, steps):
-    """The bench's work without timing, for rocprofv3."""
+    """The bench's work without timing markers, for rocprofv3: clock warm-up
+    (decode steps), a few warm-up calls, then `steps` calls back to back;
+    trace summaries take the last `steps` dispatches of the kernel."""
     import torch
     from synth import CONFIGS, make_head, make_targets, make_x
     h = make_head("qwen_decode")
     heads = upload_copies(h, N_COPIES)
+    x1 = torch.from_numpy(make_x("qwen_decode", 1).view(np.int16)).view(torch.bfloat16).cuda()
     if kind == "decode":
         src = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda").fill_(3)
         dst = torch.empty_like(src)
         dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
-        x = torch.from_numpy(make_x("qwen_decode", 1).view(np.int16)).view(torch.bfloat16).cuda()
-        clock_warmup(heads, x, 0.3)
-        time_decode(heads, x, steps, 5)
+        clock_warmup(heads, x1, 0.5)
+        outs = [torch.empty((1, h.V), device="cuda") for _ in heads]
+        wss = [hd.workspace(1, 0, x1.device) for hd in heads]
+        for i in range(5 + steps):
+            k = i % len(heads)
+            heads[k].logits(x1, out=outs[k], ws=wss[k])
     else:
         Mp = CONFIGS["qwen_prefill"]["Ms"][0]
         x = torch.from_numpy(make_x("qwen_prefill", Mp).view(np.int16)).view(
             torch.bfloat16).cuda()
         y = torch.from_numpy(make_targets("qwen_prefill", Mp)).cuda()
-        time_prefill(heads, x, y, steps, 1)
+        for hd in heads:
+            hd.prepare()
+        clock_warmup(heads, x1, 0.5)
+        ws = [hd.workspace(Mp, 1, x.device) for hd in heads]
+        for i in range(3 + steps):
+            k = i % len(heads)
+            heads[k].logits_ce(x, y, ws=ws[k])
     torch.cuda.synchronize()
     print(f"profile run {kind}: done", flush=True)
+
+
+def trace_summary(csv_path, last, match=""):
+    """Per-kernel durations from a rocprofv3 kernel-trace CSV over each
+    kernel's last `last` dispatches (after the profile run's warm-up): count,
+    mean, median, p10, p90 in us.  Prints one JSON line per kernel whose name
+    contains `match`."""
+    import csv
+    per = {}
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            name = r.get("Kernel_Name") or r.get("KernelName") or ""
+            if match not in name:
+                continue
+            per.setdefault(name, []).append((int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    for name, ts in per.items():
+        ts.sort()
+        d = np.array([(e - b) / 1e3 for b, e in ts[-last:]])
+        print(json.dumps({"kernel": name, "dispatches": len(ts), "summarised": int(d.size),
+                          "mean_us": round(float(d.mean()), 2),
+                          "median_us": round(float(np.median(d)), 2),
+                          "p10_us": round(_pct(d, 10), 2), "p90_us": round(_pct(d, 90), 2)}))
 
 
 def sweep(steps, cfg="sweep128k", Ms=None, paths=("auto", "dec", "mid", "gemv", "tiled")):
@@ -283,11 +443,12 @@ def sweep(steps, cfg="sweep128k", Ms=None, paths=("auto", "dec", "mid", "gemv", 
     "auto" is the library's own choice.  The heads keep the many-token
     kernel's head-derived tables across calls (archead_prepare)."""
     import torch
-    from oracle.bytes import head_bytes
     from synth import CONFIGS, make_head, make_x
     h = make_head(cfg)
-    pbytes = head_bytes(h)
-    heads = upload_copies(h, 2 if pbytes > 400e6 else 3)   # copies exceed the 256 MB Infinity Cache
+    heads = upload_copies(h, 3)
+    pbytes = lib_packed_bytes(heads[0])
+    if pbytes > 400e6:
+        heads.pop().close()                  # two copies already exceed the cache   # copies exceed the 256 MB Infinity Cache
     for hd in heads:
         hd.prepare()
     Ms = Ms or CONFIGS[cfg]["Ms"]
@@ -334,14 +495,21 @@ def main():
     ap.add_argument("--sweep-ms", default="",
                     help="comma-separated M values of the sweep (default: the head's workload)")
     ap.add_argument("--sweep-paths", default="auto,dec,mid,gemv,tiled")
+    ap.add_argument("--trace-summary", metavar="CSV",
+                    help="summarise a rocprofv3 kernel-trace CSV (no GPU needed): the last "
+                         "--trace-last dispatches of each kernel whose name contains --trace-match")
+    ap.add_argument("--trace-last", type=int, default=200)
+    ap.add_argument("--trace-match", default="")
     args = ap.parse_args()
+    if args.trace_summary:
+        trace_summary(args.trace_summary, args.trace_last, args.trace_match)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py: runs on one GPU only; multi-GPU (vocab-parallel) "
               "runs are not implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch
-    from oracle.bytes import head_bytes
     from synth import CONFIGS, make_head, make_targets, make_x
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
@@ -357,18 +525,23 @@ def main():
     cfg = "qwen_decode"
     log("generating the packed head ...")
     h = make_head(cfg)
-    pbytes = head_bytes(h)
     heads = upload_copies(h, N_COPIES)
+    pbytes = lib_packed_bytes(heads[0])
     xb = make_x(cfg, 64)
     x_all = torch.from_numpy(xb.view(np.int16)).view(torch.bfloat16).cuda()
 
     n_clock = clock_warmup(heads, x_all[:1], args.clock_warmup)
     log(f"clock warm-up: {n_clock} untimed decode steps in {args.clock_warmup} s")
     res = {}
+    pcts = None
     for M in (1, 4, 16, 32, 64):
         x = x_all[:M]
-        ms, kern_ms, kern_med = time_decode(heads, x, args.steps if M == 1 else
-                                            max(20, args.steps // 4), args.warmup)
+        if M == 1:
+            with ClockSampler() as clk:
+                ms, kern_ms, kern_med, pcts = time_decode(heads, x, args.steps, args.warmup,
+                                                          percentiles=True)
+        else:
+            ms, kern_ms, kern_med = time_decode(heads, x, max(20, args.steps // 4), args.warmup)
         res[M] = (ms, kern_ms, kern_med)
         log(f"decode M={M}: {ms * 1e3:.1f} us/step, head kernel {kern_ms * 1e3:.1f} us "
             f"(median {kern_med * 1e3:.1f}), {pbytes / ms / 1e6:.0f} GB/s over packed bytes")
@@ -378,12 +551,12 @@ def main():
     u8 = None
     if not args.no_u8:
         h8 = make_head(cfg, scales="u8")
-        b8 = head_bytes(h8)
         heads8 = upload_copies(h8, N_COPIES)
+        b8 = lib_packed_bytes(heads8[0])
         torch.cuda.synchronize()
         clock_warmup(heads8, x_all[:1], 0.2)
-        ms8, k8, _ = time_decode(heads8, x_all[:1], args.steps, args.warmup)
-        u8 = {"us_per_step": round(ms8 * 1e3, 2), "kernel_us": round(k8 * 1e3, 2),
+        ms8, _, k8 = time_decode(heads8, x_all[:1], args.steps, args.warmup)
+        u8 = {"us_per_step": round(ms8 * 1e3, 2), "kernel_us_median": round(k8 * 1e3, 2),
               "packed_bytes": b8, "gbs_packed": round(b8 / ms8 / 1e6, 1)}
         log(f"decode M=1, 8-bit scale codes: {ms8 * 1e3:.1f} us/step, {b8 / 1e6:.1f} MB packed, "
             f"{b8 / ms8 / 1e6:.0f} GB/s")
@@ -435,24 +608,28 @@ def main():
         tflops = flops / (kern_p * 1e-3) / 1e12
         prefill = {"M": Mp, "ms_per_step": round(ms_p, 4), "tok_s": round(Mp / ms_p * 1e3, 1),
                    "mean_ce": mean_ce,
-                   "mfma_kernel": {"kernel": "k_mfma<true>", "kernel_ms": round(kern_p, 4),
+                   "mfma_kernel": {"kernel": "k_mfma<true>", "kernel_ms_median": round(kern_p, 4),
                                    "algorithmic_flops": flops,
                                    "achieved_tflops": round(tflops, 1),
                                    "peak_tflops": PEAK_BF16_TFLOPS,
                                    "frac": round(tflops / PEAK_BF16_TFLOPS, 4)},
                    "head_tables": "prepared once (archead_prepare)",
+                   "prepared_bytes": heads[0].prepared_bytes(),
+                   "packed_plus_prepared_bytes": pbytes + heads[0].prepared_bytes(),
                    "per_call_tables": {"ms_per_step": round(ms_u, 4),
                                        "tok_s": round(Mp / ms_u * 1e3, 1),
-                                       "kernel_ms": round(kern_u, 4)}}
+                                       "kernel_ms_median": round(kern_u, 4)}}
         log(f"prefill CE M={Mp}, head tables rebuilt per call: {ms_u:.3f} ms/step, "
             f"{Mp / ms_u * 1e3:.0f} tok/s")
         log(f"prefill CE M={Mp}: {ms_p:.3f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s; "
             f"many-token kernel {kern_p:.3f} ms = {tflops:.0f} TFLOP/s "
             f"({100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak)")
 
-    ms1, kern1, _ = res[1]
+    copy = copy_bandwidth()
+    log(f"device copy: {copy['gbs_read_plus_write']} GB/s (read + write)")
+    ms1, kern1_mean, kern1 = res[1]
     value = pbytes / ms1 / 1e6          # GB/s
-    alg = decode_algorithmic_bytes(h, 1)
+    alg = decode_algorithmic_bytes(pbytes, h, 1)
     kname = f"k_gemv<1,{lanes_per_row(h)},false,false>"
     achieved = alg / kern1 / 1e6
     out = {
@@ -477,9 +654,15 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": measured_traffic(), "kernel": kname,
-                     "kernel_us": round(kern1 * 1e3, 2), "algorithmic_bytes": alg},
+                     "kernel_us_median": round(kern1 * 1e3, 2),
+                     "kernel_us_mean": round(kern1_mean * 1e3, 2), "algorithmic_bytes": alg,
+                     "timing": "HIP events attached to the kernel's dispatch, median of 100 "
+                               "dispatches after the timed loop"},
+        "step_us_percentiles": {k: round(v * 1e3, 2) for k, v in pcts.items()},
+        "gpu_clock": clk.summary(),
+        "hbm_copy": copy,
         "decode": {str(M): {"us_per_step": round(v[0] * 1e3, 2),
-                            "kernel_us": round(v[1] * 1e3, 2),
+                            "kernel_us_median": round(v[2] * 1e3, 2),
                             "gbs_packed": round(pbytes / v[0] / 1e6, 1)}
                    for M, v in res.items()},
         "greedy_argmax": greedy,
@@ -489,7 +672,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         log("timing the CPU oracle (1 token, full head) ...")
-        out["cpu_baseline"] = cpu_baseline(h, xb)
+        out["cpu_baseline"] = cpu_baseline(h, pbytes, xb)
     print(json.dumps(out), flush=True)
 
 

@@ -8,7 +8,6 @@ from .archead import (  # noqa: F401
     ArcheadError,
     Desc,
     PackedHead,
-    fidelity_summary,
     logit_fidelity,
     lib,
     pack_int4,

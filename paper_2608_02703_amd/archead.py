@@ -203,17 +203,6 @@ def logit_fidelity(ref, test):
     return kl, sq, idx, rank
 
 
-def fidelity_summary(kl, sq, rank, ks=(1, 5, 10)) -> dict:
-    """Aggregates over positions as the paper tabulates them: mean KL, logit
-    MSE (mean of the per-position summed squared error) and top-k agreement
-    in percent (rank < k)."""
-    import torch
-    out = {"kl": float(kl.double().mean()), "mse": float(sq.double().mean())}
-    for k in ks:
-        out[f"top{k}"] = 100.0 * float((rank < k).double().mean())
-    return out
-
-
 class PackedHead:
     """A packed head resident on the current GPU plus its library handle.
 
@@ -326,6 +315,11 @@ class PackedHead:
         _check(self._lib.archead_prepare(self.handle, _ptr(buf), n, self._stream(dev)),
                self._lib)
         self._prep = buf
+
+    def prepared_bytes(self) -> int:
+        """archead_prepared_bytes: size of the many-token kernel's head-derived
+        tables kept by prepare() (0 where the head has no such kernel)."""
+        return int(self._lib.archead_prepared_bytes(self.handle))
 
     def workspace_bytes(self, M: int, op: int = OP_LOGITS) -> int:
         return int(self._lib.archead_workspace_bytes(self.handle, M, op))

@@ -1770,11 +1770,14 @@ __global__ __launch_bounds__(kBlock) void k_mean(const float* v, int64_t n, floa
 //    the group's offset bias -136 * (sum of x over the group), so the chain
 //    yields the group partial sum c x; the fp16 group scale multiplies it
 //    into the running fp32 total.
-//  * then the rank-r expansion, 16 GW rank dimensions per iteration (U_c
-//    part first, then A_w; each zero-padded): lane (j, q) loads the int8
-//    codes of dims q 4GW .. +4GW-1 and fp32 MFMAs (v_mfma_f32_16x16x4_f32)
-//    multiply them with t (fp32, exact codes); the row scale s_U or s_A
-//    multiplies the result into the total.
+//  * then the rank-r expansion in K-chunks of 32 rank dimensions (U_c part
+//    first, then A_w; each zero-padded to whole chunks): lane (j, q) loads
+//    the int8 codes of dims 8q .. 8q+7 of each chunk of its row, converts
+//    them exactly to bf16, and three bf16 MFMAs (v_mfma_f32_16x16x32_bf16)
+//    per chunk multiply them with t held in LDS as three bf16 parts
+//    hi = bf16(t), mid = bf16(t - hi), lo = bf16(t - hi - mid), whose sum is
+//    t to fp32 precision; the row scale s_U or s_A multiplies the result
+//    into the total.
 // Output lane (j, q) holds tokens 4q .. 4q+3 of row j.
 //
 // Stage 1 (t = x V_c^T, x B_w^T) runs in the same launch: the first

@@ -42,12 +42,50 @@ def test_mfma_algorithmic_flops_at_prefill_shape():
 def test_decode_algorithmic_bytes_at_decode_shape():
     """Packed head once + x (bf16) + fp32 logits; at the Qwen shape and
     M = 1 that is 337,091,776 B."""
-    from synth import make_head
-    h = make_head("tiny")
+    q = _qwen()
+    assert bench.decode_algorithmic_bytes(336475840, q, 1) == 337091776
+    assert bench.decode_algorithmic_bytes(10, q, 3) == 10 + 3 * 4096 * 2 + 3 * 151936 * 4
+
+
+def test_bench_byte_count_is_the_librarys():
+    """The bench divides by archead_packed_bytes of the head's descriptor;
+    the oracle's independent count agrees (the cross-check the bench no
+    longer needs at run time)."""
     from oracle.bytes import head_bytes
-    assert bench.decode_algorithmic_bytes(h, 3) == head_bytes(h) + 3 * h.d * 2 + 3 * h.V * 4
-    # the Qwen figure quoted beside the traffic counters
-    assert 336475840 + 4096 * 2 + 151936 * 4 == 337091776
+    from paper_2608_02703_amd import archead as ab
+    from synth import make_head
+    L = ab.host_lib()
+    for scales in ("f16", "u8"):
+        h = make_head("tiny", scales=scales)
+        desc = ab.Desc.make(h.V, h.d, h.g, h.rc, h.rr, h.gV, h.gB,
+                            scale_dtype=ab.U8 if scales == "u8" else ab.F16)
+        ph = types.SimpleNamespace(desc=desc)
+        import unittest.mock as um
+        with um.patch("paper_2608_02703_amd.archead.lib", lambda: L):
+            assert bench.lib_packed_bytes(ph) == head_bytes(h)
+
+
+def test_trace_summary_takes_the_last_dispatches(tmp_path, capsys):
+    """--trace-summary: per kernel, the last N dispatches of a rocprofv3
+    kernel-trace CSV (warm-up dispatches excluded), median and mean in us."""
+    import json
+    rows = ["Kernel_Name,Start_Timestamp,End_Timestamp"]
+    t = 0
+    for i in range(10):             # 10 warm-up dispatches of 90 us, then 5 of 50 us
+        dur = 90000 if i < 10 else 0
+        rows.append(f"k_a,{t},{t + dur}")
+        t += 100000
+    for i in range(5):
+        rows.append(f"k_a,{t},{t + 50000 + 1000 * i}")
+        t += 100000
+    rows.append(f"k_b,{t},{t + 7000}")
+    p = tmp_path / "kt.csv"
+    p.write_text("\n".join(rows) + "\n")
+    bench.trace_summary(str(p), 5, "k_a")
+    out = [json.loads(line) for line in capsys.readouterr().out.splitlines()]
+    assert len(out) == 1 and out[0]["kernel"] == "k_a"
+    assert out[0]["dispatches"] == 15 and out[0]["summarised"] == 5
+    assert out[0]["median_us"] == 52.0 and out[0]["mean_us"] == 52.0
 
 
 def test_traffic_summary_is_well_formed():

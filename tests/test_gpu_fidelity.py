@@ -139,7 +139,8 @@ def test_fidelity_packed_head_against_its_oracle():
     oracle's fp64 logits of the same head: agreement is near perfect (top-1
     differs only where the oracle's top-2 gap is within rounding), and the
     kernel's figures match the oracle's on the same arrays."""
-    from paper_2608_02703_amd import PackedHead, fidelity_summary
+    from oracle.metrics import fidelity_summary
+    from paper_2608_02703_amd import PackedHead
     h = make_head("tiny")
     ph = PackedHead.from_arrays(h)
     x = make_x("tiny", 24)
@@ -152,6 +153,6 @@ def test_fidelity_packed_head_against_its_oracle():
     gap = ohead.top2_gap(ohead.logits(h, x))
     assert np.all(orank[gap > 1e-2] == 0)
     kl, sq, idx, rank = run(ref, test.cpu().numpy())
-    s = fidelity_summary(torch.from_numpy(kl), torch.from_numpy(sq), torch.from_numpy(rank))
+    s = fidelity_summary(kl, sq, rank)
     assert s["top10"] == 100.0
     ph.close()

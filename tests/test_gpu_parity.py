@@ -148,21 +148,6 @@ def test_logits_parity(cfg, M):
         say(f"  argmax equal on {n} tokens ({excl} near-ties excluded)")
 
 
-@pytest.mark.timeout(600)
-def test_logits_parity_sweep128k_sampled():
-    cfg = "sweep128k"
-    h = cached_head(cfg)
-    ph = packed(cfg)
-    x_all = make_x(cfg, 512)
-    rng = np.random.default_rng(9)
-    vocab = np.unique(np.concatenate([[0, 1, h.V - 1], rng.integers(0, h.V, 3000)]))
-    ref_all = ohead.logits(h, x_all, vocab=vocab)
-    for M in CONFIGS[cfg]["Ms"]:
-        say(f"sweep128k M={M}")
-        lg = gpu_logits(ph, x_all[:M])
-        assert_logits_close(lg[:, vocab], ref_all[:M], what=f"sweep128k M={M}")
-
-
 @pytest.mark.parametrize("cfg,M", [("tiny", 8), ("qwen_decode", 4)])
 def test_bf16_logits(cfg, M):
     Mmax = max(CONFIGS[cfg]["Ms"])
@@ -193,24 +178,6 @@ def test_ce_parity_gemma_m64_int64_targets():
     y = make_targets(cfg, 64)
     ce, mean = gpu_ce(packed(cfg), make_x(cfg, 64), y, dtype=torch.int64)
     assert_ce_close(ce, ohead.cross_entropy(ref_lg, y), what="gemma CE")
-
-
-@pytest.mark.timeout(600)
-def test_ce_parity_qwen_prefill_sampled():
-    cfg = "qwen_prefill"
-    M = CONFIGS[cfg]["Ms"][0]
-    x = make_x(cfg, M)
-    y = make_targets(cfg, M)
-    say(f"prefill CE M={M}")
-    ce, mean = gpu_ce(packed("qwen_decode"), x, y)
-    assert np.isfinite(ce).all()
-    rng = np.random.default_rng(4)
-    rows = np.unique(np.concatenate([[0, M - 1], rng.integers(0, M, 30)]))
-    h = cached_head("qwen_decode")
-    ref = ohead.cross_entropy(ohead.logits(h, x[rows]), y[rows])
-    err = assert_ce_close(ce[rows], ref, what="prefill CE sampled")
-    say(f"prefill CE sampled max err {err:.2e}, mean CE {mean:.4f}")
-    assert abs(mean - float(np.mean(ce.astype(np.float64)))) <= 1e-5
 
 
 def test_ce_target_out_of_range_is_nan():
