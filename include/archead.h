@@ -252,6 +252,32 @@ archead_status archead_logits_argmax(const archead_handle* h, const void* x, int
                                      int64_t ldx, int64_t* idx, float* max_logit, void* ws,
                                      size_t ws_bytes, void* stream);
 
+/* Bytes of the static workspace of archead_logits_noalloc, one array per
+ * device the library runs on (kept until the process ends). */
+#define ARCHEAD_NOALLOC_SCRATCH_BYTES (4u << 20)
+
+/* archead_logits without a caller workspace, for callers that cannot
+ * allocate device memory: code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation.  Same arguments, results and
+ * kernels as archead_logits (bit-identical logits), except that the
+ * workspace is a static device array of ARCHEAD_NOALLOC_SCRATCH_BYTES bytes
+ * inside the library, whose device address archead_create takes once per
+ * device.  The call allocates nothing (no hipMalloc, no allocating library
+ * routine).
+ *   Limit: M whose archead_workspace_bytes(h, M, ARCHEAD_OP_LOGITS) exceeds
+ *   ARCHEAD_NOALLOC_SCRATCH_BYTES is rejected with ARCHEAD_E_WORKSPACE (the
+ *   decode-shaped paths fit: at the Qwen3-8B shape, r_c + r_r = 96, every M
+ *   up to 64; the many-token path's per-call tables do not).
+ *   All calls on one GPU share that GPU's array, which keeps the last call's
+ *   contents (no call needs it cleared): calls that overlap on one GPU, on
+ *   different streams or from different threads, race and give undefined
+ *   results; serialise them.
+ * Errors as archead_logits, plus ARCHEAD_E_HIP when the array's address
+ * could not be taken at create time. */
+archead_status archead_logits_noalloc(const archead_handle* h, const void* x, int64_t M,
+                                      int64_t ldx, void* out, archead_dtype out_dtype,
+                                      int64_t ldo, void* stream);
+
 /* Logit fidelity of `test` logits to reference logits `ref` (the paper's
  * "Logit Fidelity" metrics, Section 4 and its Table 8: the packed head
  * against the dense head on the same positions), per position m < M:

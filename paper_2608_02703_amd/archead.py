@@ -21,6 +21,7 @@ OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
 F32, BF16, F16, I32, I64, I8, U8 = range(7)
 INT4_V1 = 1
 OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX = 0, 1, 2
+NOALLOC_SCRATCH_BYTES = 4 << 20   # ARCHEAD_NOALLOC_SCRATCH_BYTES of include/archead.h
 
 
 class ArcheadError(RuntimeError):
@@ -69,6 +70,9 @@ _SIGS = {
     "archead_logits_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_logits_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
+                                              ctypes.c_int64, ctypes.c_void_p]),
     "archead_fidelity_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64, ctypes.c_int64]),
     "archead_logit_fidelity": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
                                               ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
@@ -353,6 +357,22 @@ class PackedHead:
         _check(self._lib.archead_logits(
             self.handle, _ptr(x), M, x.stride(0), _ptr(out), code, out.stride(0),
             _ptr(ws), ws.numel(), self._stream(x.device)), self._lib)
+        return out
+
+    def logits_noalloc(self, x, out=None, out_dtype=None):
+        """archead_logits_noalloc: the logits with the library's static
+        workspace (no workspace tensor).  x: torch.bfloat16 [M, d] on the GPU."""
+        import torch
+        if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+            raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+        M = x.shape[0]
+        if out is None:
+            out = torch.empty((M, self.V), dtype=out_dtype or torch.float32,
+                              device=x.device)
+        code = {torch.float32: F32, torch.bfloat16: BF16}[out.dtype]
+        _check(self._lib.archead_logits_noalloc(
+            self.handle, _ptr(x), M, x.stride(0), _ptr(out), code, out.stride(0),
+            self._stream(x.device)), self._lib)
         return out
 
     def logits_argmax(self, x, idx=None, max_logit=None, ws=None):

@@ -3430,6 +3430,8 @@ archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs
   if (strncmp(prop.gcnArchName, "gfx950", 6) != 0)
     return fail(ARCHEAD_E_UNSUPPORTED, "device %d is %s, this library is built for gfx950", dev,
                 prop.gcnArchName);
+  st = scratch_setup(dev);
+  if (st != ARCHEAD_OK) return st;
   archead_handle* h = new (std::nothrow) archead_handle();
   if (!h) return fail(ARCHEAD_E_INVALID_ARG, "out of host memory");
   h->desc = d;

@@ -47,6 +47,11 @@ constexpr int kMidWaveCount = 8;          // its waves per workgroup
 archead_status fail(archead_status s, const char* fmt, ...);
 void clear_error();
 
+// Device address of the static workspace of archead_logits_noalloc on
+// `device` (the current device), taken once per device; called by
+// archead_create.
+archead_status scratch_setup(int device);
+
 // chunk = 32 consecutive INT4 codes = 16 bytes; lanes per row of the GEMV
 int lanes_per_row(const archead_desc& d);
 
