@@ -365,6 +365,75 @@ archead_status archead_prepare(archead_handle* h, void* buf, size_t bytes, void*
  * archead_set_gemv_max_m. */
 archead_status archead_set_timing_events(archead_handle* h, void* start, void* stop);
 
+/* ------------------------------------------------------------------------
+ * Construction of a packed head from a dense head and calibration hidden
+ * states (the paper's Algorithm 1 "ARCHead compression" and Algorithm 2
+ * "Expanded packed-head construction"; Section 3.1 for the activation
+ * metric, Section 3.2 for QuantizeCore and the correction):
+ *   C_lambda = H^T H / N + lambda cbar I  (cbar = mean diagonal of H^T H / N)
+ *   T_p = Q Lambda^p Q^T from C_lambda = Q Lambda Q^T, and T_p^-1
+ *   A_c B_c = rank-r_c truncated SVD of W (A_c = U Sigma, B_c = V^T)
+ *   QuantizeCore: core_u = Q5(A_c) (5-bit codes in [-15, 15] stored in the
+ *     int8 container, one fp16 scale per row), core_v = Q8(B_c) (one scale
+ *     per row), residual = Q_SC4(W - A_c B_c) in groups of g (the residual
+ *     against the unquantized core)
+ *   E = W - W_d (the realized error of the quantized core)
+ *   E T_p ~ U_r Sigma_r V_r^T by a randomized SVD with the caller's
+ *     Gaussian sketch omega and power_iters subspace iterations;
+ *     A_w = U_r Sigma_r, B_w = V_r^T T_p^-1
+ *   QuantizeINT8: corr_a per row, corr_b in groups of g_b along d.
+ * Every quantizer: scale = fp16(absmax / qmax) (nearest even, from fp64),
+ * code = clip(rint(value / scale), -qmax, qmax), qmax = 7 / 15 / 127; an
+ * all-zero group gets scale 0 and codes 0.  All arithmetic is fp64 (rocBLAS
+ * GEMMs, rocSOLVER eigen- and singular-value solvers, and this library's
+ * kernels).  The randomized SVD's result is the truncated SVD of E T_p only
+ * approximately (its error is bounded below by the exact tail).
+ *
+ * The written head has g_v = d and the descriptor
+ * {V, d, g, r_c, r_r, g_v = d, g_b, ARCHEAD_INT4_V1, ARCHEAD_F16, ARCHEAD_I8}.
+ */
+typedef struct archead_build_desc {
+  uint32_t abi_version;     /* ARCHEAD_ABI_VERSION */
+  int64_t V, d, N;          /* dense head rows, hidden size, calibration tokens */
+  int64_t g;                /* residual group along d (g % 32 == 0, d % g == 0) */
+  int64_t r_c, r_r;         /* core and correction ranks (0 = component absent) */
+  int64_t g_b;              /* group of the corr_b scales along d (d = one per row) */
+  double p, lambda;         /* metric exponent, damping */
+  int64_t oversample;       /* extra sketch columns of the randomized SVD */
+  int64_t power_iters;      /* its subspace iterations */
+} archead_build_desc;
+
+/* Device workspace bytes archead_build_head needs (0 for an invalid
+ * descriptor): about 17 V d + 8 N d + 56 d^2 bytes plus the factor-sized
+ * buffers (fp64 copies of W, the residual / realized error, H, and the d x d
+ * metric matrices). */
+size_t archead_build_workspace_bytes(const archead_build_desc* b);
+
+/* Build a packed head on the current device.
+ *   W      fp32 [V, ldw] device, the dense head (ldw >= d)
+ *   H      fp32 [N, ldh] device, calibration hidden states (ldh >= d)
+ *   omega  fp64 [r_r + oversample, d] device, row-major: the sketch of the
+ *          randomized SVD (i.i.d. standard normal draws; ignored when r_r = 0)
+ *   out    device buffers to fill, in the layouts of archead_ptrs with the
+ *          descriptor above (res_codes 4-byte aligned; res_row_scales unused)
+ *   a_w, b_w  optional fp64 device outputs of the unquantized correction
+ *          factors, [V, r_r] and [r_r, d] row-major (NULL to skip)
+ *   ws     device workspace of archead_build_workspace_bytes(b) bytes,
+ *          256-byte aligned
+ *   stream hipStream_t (NULL = the default stream)
+ * Synchronous: returns after the work on `stream` has finished.  The dense
+ * library calls run through a rocBLAS handle created for the call, whose own
+ * device workspace rocBLAS manages; the forward entry points never do this.
+ * ARCHEAD_E_INVALID_ARG for a bad descriptor, a NULL buffer of a present
+ * component, or a damped covariance that is not positive definite;
+ * ARCHEAD_E_MISALIGNED; ARCHEAD_E_WORKSPACE; ARCHEAD_E_UNSUPPORTED for
+ * shapes beyond 32-bit library sizes; ARCHEAD_E_HIP when a launch fails or
+ * a solver does not converge. */
+archead_status archead_build_head(const archead_build_desc* b, const float* W, int64_t ldw,
+                                  const float* H, int64_t ldh, const double* omega,
+                                  const archead_ptrs* out, double* a_w, double* b_w, void* ws,
+                                  size_t ws_bytes, void* stream);
+
 /* Persistent bytes of the packed head: the sum over its buffers of element
  * count times element size (the paper's bytes(ARCHead), Section 3.3).
  * 0 for an invalid descriptor. */

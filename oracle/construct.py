@@ -92,6 +92,7 @@ def quantize_core(W: np.ndarray, rc: int, g: int):
         core_q = dequantize(out["core_u"], out["core_u_scale"]) @ \
             dequantize(out["core_v"], out["core_v_scale"])
         R = W - Ac @ Bc
+        out["A_c"], out["B_c"] = Ac, Bc          # the unquantized core factors
     else:
         core_q = np.zeros_like(W)
         R = W
@@ -122,7 +123,8 @@ def build_head(W: np.ndarray, H: np.ndarray, rc: int, rr: int, g: int,
     h.core_u_scale = core.get("core_u_scale", np.zeros((V, 1), np.float16))[:, 0]
     h.core_v = core.get("core_v", np.zeros((0, d), np.int8))
     h.core_v_scale = core.get("core_v_scale", np.zeros((0, 1), np.float16))
-    info = dict(T=T, Tinv=Tinv, W_d=W_d, E=E, C_lam=C_lam)
+    info = dict(T=T, Tinv=Tinv, W_d=W_d, E=E, C_lam=C_lam, A_c=core.get("A_c"),
+                B_c=core.get("B_c"))
     if rr:
         A_w, B_w = fit_correction(E, T, Tinv, rr)
         h.corr_a, sa = quantize_symmetric(A_w, 8, rr)

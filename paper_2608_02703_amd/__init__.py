@@ -6,7 +6,9 @@ device memory and streams only.
 """
 from .archead import (  # noqa: F401
     ArcheadError,
+    BuildDesc,
     Desc,
+    build_head,
     PackedHead,
     logit_fidelity,
     lib,

@@ -45,6 +45,15 @@ class Desc(ctypes.Structure):
                    d if gB is None else gB, enc, scale_dtype, factor_dtype)
 
 
+class BuildDesc(ctypes.Structure):
+    """archead_build_desc: shape and parameters of a head construction."""
+    _fields_ = [("abi_version", ctypes.c_uint32), ("V", ctypes.c_int64), ("d", ctypes.c_int64),
+                ("N", ctypes.c_int64), ("g", ctypes.c_int64), ("r_c", ctypes.c_int64),
+                ("r_r", ctypes.c_int64), ("g_b", ctypes.c_int64), ("p", ctypes.c_double),
+                ("lam", ctypes.c_double), ("oversample", ctypes.c_int64),
+                ("power_iters", ctypes.c_int64)]
+
+
 class Ptrs(ctypes.Structure):
     _fields_ = [(n, ctypes.c_void_p) for n in (
         "res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
@@ -79,6 +88,12 @@ _SIGS = {
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                               ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                               ctypes.c_void_p]),
+    "archead_build_workspace_bytes": (ctypes.c_size_t, [ctypes.POINTER(BuildDesc)]),
+    "archead_build_head": (ctypes.c_int, [ctypes.POINTER(BuildDesc), ctypes.c_void_p,
+                                          ctypes.c_int64, ctypes.c_void_p, ctypes.c_int64,
+                                          ctypes.c_void_p, ctypes.POINTER(Ptrs), ctypes.c_void_p,
+                                          ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                          ctypes.c_void_p]),
     "archead_set_gemv_max_m": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64]),
     "archead_get_gemv_max_m": (ctypes.c_int64, [ctypes.c_void_p]),
     "archead_set_dec_range": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64]),
@@ -205,6 +220,57 @@ def logit_fidelity(ref, test):
                                     _ptr(kl), _ptr(sq), _ptr(idx), _ptr(rank), _ptr(ws),
                                     ws.numel(), stream), L)
     return kl, sq, idx, rank
+
+
+def build_head(W, H, rc: int, rr: int, g: int, p: float = 0.75, lam: float = 1e-3, gB=None,
+               oversample: int = 8, power_iters: int = 4, seed: int = 0,
+               return_factors: bool = False):
+    """archead_build_head: construct a packed head on the GPU from a dense
+    head W (fp32 [V, d] CUDA tensor) and calibration hidden states H (fp32
+    [N, d] CUDA tensor), with the randomized SVD's Gaussian sketch drawn here
+    from a seeded torch generator.  Returns a PackedHead over the written
+    buffers (and the unquantized A_w, B_w as fp64 tensors when
+    return_factors)."""
+    import torch
+    if W.dtype != torch.float32 or H.dtype != torch.float32 or W.dim() != 2 or H.dim() != 2:
+        raise TypeError("W and H must be 2-D float32 tensors")
+    if W.stride(1) != 1 or H.stride(1) != 1 or W.shape[1] != H.shape[1]:
+        raise ValueError("W and H need unit column stride and the same width d")
+    V, d = W.shape
+    N = H.shape[0]
+    gB = d if gB is None else gB
+    dev = W.device
+    desc = BuildDesc(ABI_VERSION, V, d, N, g, rc, rr, gB, p, lam, oversample, power_iters)
+    L = lib()
+    need = int(L.archead_build_workspace_bytes(ctypes.byref(desc)))
+    if need == 0:
+        raise ArcheadError(E_INVALID_ARG, "invalid construction descriptor")
+
+    def buf(shape, dtype):
+        n = int(np.prod(shape))
+        return torch.zeros(shape, dtype=dtype, device=dev) if n else None
+    bufs = {"res_codes": buf((V, d // 2), torch.uint8), "res_scales": buf((V, d // g), torch.float16),
+            "core_u": buf((V, rc), torch.int8), "core_u_scale": buf((V,), torch.float16) if rc else None,
+            "core_v": buf((rc, d), torch.int8), "core_v_scale": buf((rc, 1), torch.float16) if rc else None,
+            "corr_a": buf((V, rr), torch.int8), "corr_a_scale": buf((V,), torch.float16) if rr else None,
+            "corr_b": buf((rr, d), torch.int8),
+            "corr_b_scale": buf((rr, d // gB), torch.float16) if rr else None,
+            "res_row_scales": None}
+    k = rr + oversample if rr else 0
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(seed)
+    omega = torch.randn((max(k, 1), d), dtype=torch.float64, device=dev, generator=gen)
+    a_w = torch.empty((V, rr), dtype=torch.float64, device=dev) if (return_factors and rr) else None
+    b_w = torch.empty((rr, d), dtype=torch.float64, device=dev) if (return_factors and rr) else None
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    ptrs = Ptrs(*[_ptr(bufs.get(n)) for n in PackedHead.BUFFERS])
+    stream = ctypes.c_void_p(torch.cuda.current_stream(dev).cuda_stream)
+    _check(L.archead_build_head(ctypes.byref(desc), _ptr(W), W.stride(0), _ptr(H), H.stride(0),
+                                _ptr(omega), ctypes.byref(ptrs), _ptr(a_w), _ptr(b_w), _ptr(ws),
+                                ws.numel(), stream), L)
+    del ws
+    ph = PackedHead(V, d, g, rc, rr, bufs, d, gB)
+    return (ph, a_w, b_w) if return_factors else ph
 
 
 class PackedHead:

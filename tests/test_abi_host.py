@@ -234,3 +234,54 @@ def test_fidelity_workspace_bytes(L):
     assert L.archead_fidelity_workspace_bytes(3, 0) == 0
     assert L.archead_fidelity_workspace_bytes(1, 1) == 256 + 4
     assert L.archead_fidelity_workspace_bytes(2, 151936) == 2048 + 8   # 2 x 19 x 48 = 1824 -> 2048
+
+
+def _bdesc(**kw):
+    base = dict(V=1000, d=256, N=512, g=64, r_c=8, r_r=4, g_b=256, p=0.75, lam=1e-3,
+                oversample=8, power_iters=2)
+    base.update(kw)
+    abi = base.pop("abi", ab.ABI_VERSION)
+    return ab.BuildDesc(abi, base["V"], base["d"], base["N"], base["g"], base["r_c"],
+                        base["r_r"], base["g_b"], base["p"], base["lam"], base["oversample"],
+                        base["power_iters"])
+
+
+@pytest.mark.parametrize("kw,ok", [({}, True), (dict(abi=1), False), (dict(g=48), False),
+                                   (dict(d=288), False), (dict(r_c=-1), False),
+                                   (dict(g_b=100), False), (dict(r_r=0, g_b=0), True),
+                                   (dict(r_r=250, oversample=8), False), (dict(N=0), False),
+                                   (dict(lam=-1.0), False), (dict(d=65536, g=64), False)])
+def test_build_workspace_bytes(L, kw, ok):
+    """archead_build_workspace_bytes: positive for a valid construction
+    descriptor (at least the two fp64 V x d buffers and H), 0 otherwise."""
+    n = L.archead_build_workspace_bytes(ctypes.byref(_bdesc(**kw)))
+    if ok:
+        b = _bdesc(**kw)
+        assert n >= 2 * 8 * b.V * b.d + 8 * b.N * b.d
+    else:
+        assert n == 0
+
+
+def test_build_head_argument_checks_before_any_device_call(L):
+    """archead_build_head rejects bad arguments on the host (the pointers
+    here are never dereferenced)."""
+    b = _bdesc()
+    need = L.archead_build_workspace_bytes(ctypes.byref(b))
+    p = 1 << 20
+    full = ab.Ptrs(*([p] * 10 + [0]))
+    ptrs = ctypes.byref(full)
+
+    def call(desc=b, W=p, ldw=256, H=p, ldh=256, om=p, out=ptrs, ws=p, n=need):
+        return L.archead_build_head(ctypes.byref(desc) if desc is not None else None, W, ldw, H,
+                                    ldh, om, out, None, None, ws, n, None)
+    assert call(desc=None) == ab.E_INVALID_ARG
+    assert call(desc=_bdesc(g=48)) == ab.E_INVALID_ARG
+    assert call(W=None) == ab.E_INVALID_ARG
+    assert call(ldw=255) == ab.E_INVALID_ARG
+    assert call(ldh=100) == ab.E_INVALID_ARG
+    assert call(om=None) == ab.E_INVALID_ARG                     # r_r > 0 needs a sketch
+    no_core = ab.Ptrs(*([p] * 2 + [0] * 8 + [0]))
+    assert call(out=ctypes.byref(no_core)) == ab.E_INVALID_ARG   # r_c > 0 needs its buffers
+    assert call(ws=p + 64) == ab.E_MISALIGNED
+    assert call(n=need - 1) == ab.E_WORKSPACE
+    assert L.archead_last_error()
