@@ -45,7 +45,9 @@ N_COPIES = 3
 CALIBRATION_BYTES = 256 << 20
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "gemv_qwen_decode_traffic.md")
 SWEEP_PEAK_NOTE = "bf16 dense MFMA 2.5 PFLOP/s, HBM 8 TB/s"
-KERNEL_SOURCE = os.path.join(ROOT, "paper_2608_02703_amd", "csrc", "archead.hip")
+# the decode GEMV's sources: the counters are valid while these are unchanged
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_02703_amd", "csrc", f)
+                  for f in ("dev_common.cuh", "dev_gemv.cuh", "k_gemv.hip")]
 
 
 def log(*a):
@@ -97,8 +99,11 @@ def mfma_algorithmic_flops(h, M):
 
 
 def source_sha256():
-    with open(KERNEL_SOURCE, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    h = hashlib.sha256()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def measured_traffic():
@@ -485,6 +490,9 @@ def main():
     ap.add_argument("--no-prefill", action="store_true")
     ap.add_argument("--no-u8", action="store_true",
                     help="skip the decode line of the head with 8-bit residual scale codes")
+    ap.add_argument("--no-paper-storage", action="store_true",
+                    help="skip the lines of the head in the paper's own storage (5-bit U_c, "
+                         "r_c=10, r_r=6, g=64, 8-bit scale codes)")
     ap.add_argument("--no-dense", action="store_true",
                     help="skip the dense bf16 head context line")
     ap.add_argument("--profile", choices=["decode", "prefill"])
@@ -563,6 +571,37 @@ def main():
         for hd in heads8:
             hd.close()
         del heads8
+        torch.cuda.empty_cache()
+
+    # the paper's own Qwen3-8B storage: r_c = 10 with 5-bit core-left words,
+    # r_r = 6, residual groups of 64 with 8-bit scale codes
+    paper = None
+    if not args.no_paper_storage:
+        hp = make_head(cfg, g=64, rc=10, rr=6, core_u="i5", scales="u8")
+        headsp = upload_copies(hp, N_COPIES)
+        bp = lib_packed_bytes(headsp[0])
+        clock_warmup(headsp, x_all[:1], 0.2)
+        msp, _, kp = time_decode(headsp, x_all[:1], args.steps, args.warmup)
+        paper = {"config": "V=151936 d=4096 g=64 r_c=10 (5-bit ARCHEAD_I5) r_r=6, 8-bit scale codes",
+                 "packed_bytes": bp, "packed_mib": round(bp / 2 ** 20, 2),
+                 "decode_m1": {"us_per_step": round(msp * 1e3, 2), "kernel_us_median": round(kp * 1e3, 2),
+                               "gbs_packed": round(bp / msp / 1e6, 1)}}
+        log(f"paper storage head: {bp / 2 ** 20:.2f} MiB, decode M=1 {msp * 1e3:.1f} us/step, "
+            f"{bp / msp / 1e6:.0f} GB/s")
+        if not args.no_prefill:
+            Mp = CONFIGS["qwen_prefill"]["Ms"][0]
+            xpp = torch.from_numpy(make_x("qwen_prefill", Mp).view(np.int16)).view(
+                torch.bfloat16).cuda()
+            ypp = torch.from_numpy(make_targets("qwen_prefill", Mp)).cuda()
+            ms_pp, ce_pp, k_pp = time_prefill(headsp, xpp, ypp, args.prefill_steps, 3)
+            paper["prefill_m4096"] = {"ms_per_step": round(ms_pp, 4),
+                                      "tok_s": round(Mp / ms_pp * 1e3, 1), "mean_ce": ce_pp,
+                                      "kernel_ms_median": round(k_pp, 4)}
+            log(f"paper storage head: prefill CE M={Mp} {ms_pp:.3f} ms/step")
+            del xpp, ypp
+        for hd in headsp:
+            hd.close()
+        del headsp
         torch.cuda.empty_cache()
 
     # greedy decoding: the fused argmax step (no [M, V] logits written)
@@ -667,6 +706,7 @@ def main():
                    for M, v in res.items()},
         "greedy_argmax": greedy,
         "decode_u8_scales": u8,
+        "paper_storage_head": paper,
         "prefill": prefill,
         "dense_bf16_head": dense,
     }

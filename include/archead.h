@@ -29,7 +29,9 @@
  *   res_scales    fp16    [V, d/g]     residual group scales (groups of g
  *                                      consecutive elements along d)
  *   core_u        int8    [V, r_c]     core left codes (A_c side; any code
- *                                      range that fits int8, e.g. 5-bit)
+ *                                      range that fits int8, e.g. 5-bit), or
+ *                 uint32  [V, ceil(r_c/6)]  the same codes bit-packed in
+ *                                      ARCHEAD_I5 (desc.core_u_dtype)
  *   core_u_scale  fp16    [V]          per-row scales of core_u
  *   core_v        int8    [r_c, d]     core right codes (B_c side)
  *   core_v_scale  fp16    [r_c, d/g_v] group scales of core_v (g_v = d: one
@@ -69,7 +71,7 @@
 extern "C" {
 #endif
 
-#define ARCHEAD_ABI_VERSION 2u
+#define ARCHEAD_ABI_VERSION 3u
 
 typedef enum archead_status {
   ARCHEAD_OK = 0,
@@ -87,7 +89,8 @@ typedef enum archead_dtype {
   ARCHEAD_I32 = 3,
   ARCHEAD_I64 = 4,
   ARCHEAD_I8 = 5,
-  ARCHEAD_U8 = 6
+  ARCHEAD_U8 = 6,
+  ARCHEAD_I5 = 7   /* signed 5-bit codes, six per little-endian 32-bit word */
 } archead_dtype;
 
 typedef enum archead_int4_encoding { ARCHEAD_INT4_V1 = 1 } archead_int4_encoding;
@@ -115,7 +118,20 @@ typedef enum archead_op {
  *                  s[v, j] = rs[v] * q[v, j] (exact in fp32).  One byte of
  *                  scale per group is the storage the paper's reported head
  *                  sizes imply.  Served by every kernel (see
- *                  archead_logits). */
+ *                  archead_logits).
+ *   core_u_dtype: the core left factor's codes (the paper stores Q5(A_c),
+ *   5-bit codes, Section 3.2 and the packed state-dictionary table):
+ *     ARCHEAD_I8: int8 [V, r_c], one code per byte;
+ *     ARCHEAD_I5: bit-packed, ARCHEAD_I5 layout: row v of core_u is
+ *                 W5 = ceil(r_c / 6) little-endian 32-bit words (4 * W5
+ *                 bytes, rows back to back); code k of the row is bits
+ *                 [5 (k % 6), 5 (k % 6) + 5) of word k / 6, a 5-bit two's
+ *                 complement value in [-16, 15]; bits 30-31 of every word and
+ *                 the fields past r_c are zero.  core_u must then be 4-byte
+ *                 aligned.  Every kernel reads this layout directly.
+ *   Ranks need not be multiples of 4 on any kernel (the several-token and
+ *   MFMA decode kernels read factor codes in pieces that need no alignment
+ *   when a rank is not). */
 typedef struct archead_desc {
   uint32_t abi_version; /* ARCHEAD_ABI_VERSION */
   int64_t V, d, g;
@@ -124,6 +140,7 @@ typedef struct archead_desc {
   int32_t int4_encoding;
   int32_t scale_dtype;
   int32_t factor_dtype;
+  int32_t core_u_dtype;  /* ARCHEAD_I8 or ARCHEAD_I5 (ABI 3) */
 } archead_desc;
 
 /* Device pointers to the packed buffers (layouts above).  res_codes must
@@ -438,6 +455,14 @@ archead_status archead_build_head(const archead_build_desc* b, const float* W, i
  * count times element size (the paper's bytes(ARCHead), Section 3.3).
  * 0 for an invalid descriptor. */
 uint64_t archead_packed_bytes(const archead_desc* desc);
+
+/* Host-side 5-bit packing to / from ARCHEAD_I5 (no HIP call).
+ * codes: int8 [rows, r] with values in [-16, 15]; packed: uint32
+ * [rows, ceil(r / 6)].  pack returns ARCHEAD_E_INVALID_ARG for a code out of
+ * range, r < 1 or rows < 0. */
+archead_status archead_pack_int5(const int8_t* codes, int64_t rows, int64_t r, uint32_t* packed);
+archead_status archead_unpack_int5(const uint32_t* packed, int64_t rows, int64_t r,
+                                   int8_t* codes);
 
 /* Host-side INT4 packing to / from ARCHEAD_INT4_V1 (no HIP call).
  * codes: int8 [rows, d] with values in [-8, 7]; packed: uint8 [rows, d/2];

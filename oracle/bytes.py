@@ -55,9 +55,20 @@ def dense_bf16_bytes(V: int, d: int) -> int:
     return V * d * 2
 
 
+def i5_row_bytes(rc: int) -> int:
+    """Bytes per row of 5-bit codes packed six per 32-bit word."""
+    return 4 * ((rc + 5) // 6)
+
+
 def head_bytes(h) -> int:
-    """packed_bytes of a head object carrying the shape attributes."""
+    """packed_bytes of a head object carrying the shape attributes and
+    buffers (8-bit residual scale codes and 5-bit core-left words are
+    recognised by their array types)."""
+    kw = {}
     if getattr(h, "res_scales", None) is not None and h.res_scales.dtype == "uint8":
-        return packed_bytes(h.V, h.d, h.g, h.rc, h.rr, h.gV, h.gB, res_scale_bits=8,
-                            res_row_scale_bytes=2)
-    return packed_bytes(h.V, h.d, h.g, h.rc, h.rr, h.gV, h.gB)
+        kw.update(res_scale_bits=8, res_row_scale_bytes=2)
+    b = packed_bytes(h.V, h.d, h.g, h.rc, h.rr, h.gV, h.gB, **kw)
+    cu = getattr(h, "core_u", None)
+    if h.rc and cu is not None and cu.dtype == "uint32":
+        b += h.V * i5_row_bytes(h.rc) - h.V * h.rc   # words instead of one byte per code
+    return b

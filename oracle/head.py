@@ -21,6 +21,10 @@ fp16 scale rs per vocabulary row: s_res[v, j] = rs[v] * q[v, j] (a uint8
 res_scales array plus res_row_scales [V]; the format is this library's
 reading, the paper leaves it open).
 
+The core left factor's codes are int8, or 5-bit codes bit-packed six per
+32-bit word (uint32 [V, ceil(r_c/6)], the paper's "packed 5-bit" Q5(A_c);
+layout in oracle.layout.unpack_int5).
+
 A rank of zero means the component is absent (the paper's "core only" and
 "Group INT4" ablations).  The head object is any object with the attributes
 V, d, g, rc, rr, gV, gB and the ten buffers (res_codes, res_scales, core_u,
@@ -34,7 +38,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from .layout import bf16_to_f64, fp16_to_f64, unpack_int4
+from .layout import bf16_to_f64, fp16_to_f64, unpack_int4, unpack_int5
 
 ROW_CHUNK = 4096
 
@@ -55,9 +59,14 @@ def residual_scales(h, v0: int, v1: int) -> np.ndarray:
     return fp16_to_f64(sc)
 
 
-def left_factor(codes, scales) -> np.ndarray:
-    """Row-scaled left factor: s[v] * codes[v, k] (U_c or A_w)."""
-    return fp16_to_f64(scales)[:, None] * np.asarray(codes).astype(np.float64)
+def left_factor(codes, scales, rank: int = None) -> np.ndarray:
+    """Row-scaled left factor: s[v] * codes[v, k] (U_c or A_w).  codes are
+    int8 [n, rank], or uint32 ARCHEAD_I5 words [n, ceil(rank/6)] of 5-bit
+    codes (then rank is required)."""
+    codes = np.asarray(codes)
+    if codes.dtype == np.uint32:
+        codes = unpack_int5(codes, rank)
+    return fp16_to_f64(scales)[:, None] * codes.astype(np.float64)
 
 
 def right_factor(codes, scales, group: int) -> np.ndarray:
@@ -70,7 +79,7 @@ def right_factor(codes, scales, group: int) -> np.ndarray:
 def core_rows(h, v0: int, v1: int) -> np.ndarray:
     if h.rc == 0:
         return np.zeros((v1 - v0, h.d))
-    return left_factor(h.core_u[v0:v1], h.core_u_scale[v0:v1]) @ \
+    return left_factor(h.core_u[v0:v1], h.core_u_scale[v0:v1], h.rc) @ \
         right_factor(h.core_v, h.core_v_scale, h.gV)
 
 
@@ -143,7 +152,7 @@ def logits_factorized(h, x) -> np.ndarray:
         out[:, v0:v1] = X @ residual_rows(h, v0, v1).T
     if h.rc:
         t_c = X @ right_factor(h.core_v, h.core_v_scale, h.gV).T
-        out += t_c @ left_factor(h.core_u, h.core_u_scale).T
+        out += t_c @ left_factor(h.core_u, h.core_u_scale, h.rc).T
     if h.rr:
         t_w = X @ right_factor(h.corr_b, h.corr_b_scale, h.gB).T
         out += t_w @ left_factor(h.corr_a, h.corr_a_scale).T

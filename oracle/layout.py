@@ -52,6 +52,36 @@ def pack_int4(codes: np.ndarray) -> np.ndarray:
     return q.astype("<u4").view(np.uint8).reshape(R, d // 2)
 
 
+def unpack_int5(words: np.ndarray, r: int) -> np.ndarray:
+    """ARCHEAD_I5 words uint32 [R, ceil(r/6)] -> int8 codes [R, r].
+
+    Layout (the library's reading of the paper's "packed 5-bit" core-left
+    factor): code k of a row sits in word k // 6 at bits [5 (k % 6),
+    5 (k % 6) + 5) as a 5-bit two's complement value in [-16, 15]."""
+    words = np.ascontiguousarray(words, dtype=np.uint32)
+    R = words.shape[0]
+    if r < 1 or words.shape != (R, (r + 5) // 6):
+        raise ValueError(f"words shape {words.shape} != ({R}, {(r + 5) // 6})")
+    out = np.empty((R, r), dtype=np.int8)
+    for k in range(r):
+        f = (words[:, k // 6].astype(np.int64) >> (5 * (k % 6))) & 31
+        out[:, k] = np.where(f >= 16, f - 32, f)
+    return out
+
+
+def pack_int5(codes: np.ndarray) -> np.ndarray:
+    """int codes [R, r] in [-16, 15] -> ARCHEAD_I5 words uint32 [R, ceil(r/6)]
+    (inverse of unpack_int5; unused bits zero)."""
+    codes = np.asarray(codes, dtype=np.int64)
+    R, r = codes.shape
+    if codes.min(initial=0) < -16 or codes.max(initial=0) > 15:
+        raise ValueError("5-bit codes must lie in [-16, 15]")
+    w = np.zeros((R, (r + 5) // 6), dtype=np.int64)
+    for k in range(r):
+        w[:, k // 6] |= (codes[:, k] & 31) << (5 * (k % 6))
+    return w.astype(np.uint32)
+
+
 def fp16_to_f64(a) -> np.ndarray:
     """fp16 values (float16 array or uint16 bit patterns) -> float64, exact."""
     a = np.asarray(a)

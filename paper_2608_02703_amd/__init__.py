@@ -13,7 +13,9 @@ from .archead import (  # noqa: F401
     logit_fidelity,
     lib,
     pack_int4,
+    pack_int5,
     packed_bytes,
     unpack_int4,
+    unpack_int5,
     validate_desc,
 )

@@ -16,9 +16,9 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libarchead.so")
 HOST_LIB_PATH = os.path.join(_PKG, "libarchead_host.so")
 
-ABI_VERSION = 2
+ABI_VERSION = 3
 OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
-F32, BF16, F16, I32, I64, I8, U8 = range(7)
+F32, BF16, F16, I32, I64, I8, U8, I5 = range(8)
 INT4_V1 = 1
 OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX = 0, 1, 2
 NOALLOC_SCRATCH_BYTES = 4 << 20   # ARCHEAD_NOALLOC_SCRATCH_BYTES of include/archead.h
@@ -36,13 +36,13 @@ class Desc(ctypes.Structure):
                 ("r_c", ctypes.c_int64), ("r_r", ctypes.c_int64),
                 ("g_v", ctypes.c_int64), ("g_b", ctypes.c_int64),
                 ("int4_encoding", ctypes.c_int32), ("scale_dtype", ctypes.c_int32),
-                ("factor_dtype", ctypes.c_int32)]
+                ("factor_dtype", ctypes.c_int32), ("core_u_dtype", ctypes.c_int32)]
 
     @classmethod
     def make(cls, V, d, g, rc, rr, gV=None, gB=None, abi=ABI_VERSION,
-             enc=INT4_V1, scale_dtype=F16, factor_dtype=I8):
+             enc=INT4_V1, scale_dtype=F16, factor_dtype=I8, core_u_dtype=I8):
         return cls(abi, V, d, g, rc, rr, d if gV is None else gV,
-                   d if gB is None else gB, enc, scale_dtype, factor_dtype)
+                   d if gB is None else gB, enc, scale_dtype, factor_dtype, core_u_dtype)
 
 
 class BuildDesc(ctypes.Structure):
@@ -110,6 +110,10 @@ _SIGS = {
     "archead_packed_bytes": (ctypes.c_uint64, [ctypes.POINTER(Desc)]),
     "archead_pack_int4": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                          ctypes.c_void_p]),
+    "archead_pack_int5": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                         ctypes.c_void_p]),
+    "archead_unpack_int5": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
+                                           ctypes.c_void_p]),
     "archead_unpack_int4": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64,
                                            ctypes.c_void_p]),
     "archead_status_str": (ctypes.c_char_p, [ctypes.c_int]),
@@ -119,7 +123,8 @@ _SIGS = {
 HOST_SYMBOLS = ("archead_validate_desc", "archead_set_gemv_max_m", "archead_set_timing_events",
                 "archead_get_gemv_max_m", "archead_set_dec_range", "archead_get_dec_range",
                 "archead_set_mid_range", "archead_get_mid_range",
-                "archead_packed_bytes", "archead_pack_int4",
+                "archead_packed_bytes", "archead_pack_int4", "archead_pack_int5",
+                "archead_unpack_int5",
                 "archead_unpack_int4", "archead_status_str", "archead_last_error")
 
 _libs = {}
@@ -175,6 +180,26 @@ def pack_int4(codes: np.ndarray, L=None) -> np.ndarray:
     rows, d = c.shape
     out = np.empty((rows, d // 2), dtype=np.uint8)
     _check(L.archead_pack_int4(c.ctypes.data, rows, d, out.ctypes.data), L)
+    return out
+
+
+def pack_int5(codes: np.ndarray, L=None) -> np.ndarray:
+    """int codes [rows, r] in [-16, 15] -> ARCHEAD_I5 words uint32 [rows, ceil(r/6)]."""
+    L = L or lib()
+    c = np.ascontiguousarray(codes, dtype=np.int8)
+    rows, r = c.shape
+    out = np.empty((rows, (r + 5) // 6), dtype=np.uint32)
+    _check(L.archead_pack_int5(c.ctypes.data, rows, r, out.ctypes.data), L)
+    return out
+
+
+def unpack_int5(words: np.ndarray, r: int, L=None) -> np.ndarray:
+    L = L or lib()
+    w = np.ascontiguousarray(words, dtype=np.uint32)
+    if w.shape[1] != (r + 5) // 6:
+        raise ValueError("ARCHEAD_I5 rows must hold ceil(r / 6) words")
+    out = np.empty((w.shape[0], r), dtype=np.int8)
+    _check(L.archead_unpack_int5(w.ctypes.data, w.shape[0], r, out.ctypes.data), L)
     return out
 
 
@@ -279,7 +304,8 @@ class PackedHead:
     ``buffers`` maps the buffer names to torch tensors on the device (the
     caller keeps ownership; the handle only borrows them).  A uint8
     ``res_scales`` selects 8-bit group scale codes, with ``res_row_scales``
-    (fp16 [V]) the per-row scale."""
+    (fp16 [V]) the per-row scale; an int32 ``core_u`` of ceil(rc/6) columns
+    holds ARCHEAD_I5 words (5-bit codes)."""
 
     BUFFERS = ("res_codes", "res_scales", "core_u", "core_u_scale", "core_v",
                "core_v_scale", "corr_a", "corr_a_scale", "corr_b", "corr_b_scale",
@@ -293,7 +319,10 @@ class PackedHead:
         self.buffers = buffers
         sc = buffers.get("res_scales")
         u8 = sc is not None and str(sc.dtype) == "torch.uint8"
-        self.desc = Desc.make(V, d, g, rc, rr, self.gV, self.gB, scale_dtype=U8 if u8 else F16)
+        cu = buffers.get("core_u")
+        i5 = cu is not None and str(cu.dtype) == "torch.int32"
+        self.desc = Desc.make(V, d, g, rc, rr, self.gV, self.gB, scale_dtype=U8 if u8 else F16,
+                              core_u_dtype=I5 if i5 else I8)
         self.ptrs = Ptrs(*[_ptr(buffers.get(n)) for n in self.BUFFERS])
         self._lib = lib()
         h = ctypes.c_void_p()
@@ -320,6 +349,8 @@ class PackedHead:
                 continue
             if a.dtype == np.float16:
                 t = torch.from_numpy(a.view(np.int16)).view(torch.float16)
+            elif a.dtype == np.uint32:               # ARCHEAD_I5 words
+                t = torch.from_numpy(a.view(np.int32))
             elif a.dtype == np.uint8:
                 t = torch.from_numpy(a)
             else:

@@ -21,6 +21,15 @@ archead_status fail(archead_status s, const char* fmt, ...) {
 
 void clear_error() { g_err[0] = 0; }
 
+int64_t core_u_row_bytes(const archead_desc& d) {
+  return d.core_u_dtype == ARCHEAD_I5 ? 4 * ((d.r_c + 5) / 6) : d.r_c;
+}
+
+int gen_codes(const archead_desc& d) {
+  if (d.core_u_dtype == ARCHEAD_I5 && d.r_c) return 2;
+  return d.r_c % 4 || d.r_r % 4 ? 1 : 0;
+}
+
 int lanes_per_row(const archead_desc& d) {
   // a segment of 16 lanes per row reads 256 contiguous bytes per row and 4
   // rows per load instruction, which streams faster than one row per
@@ -59,7 +68,7 @@ int dec_tokens_per_pass(const archead_desc& d) {
   if (d.g != 32 && d.g != 64 && d.g != 128) return 0;
   // 8-bit scale codes: all 64 groups of a row in one 16-byte load per lane
   if ((d.d / d.g) % 4 || d.d / d.g > 64) return 0;
-  if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return 0;
+  if (d.r_c > 128 || d.r_r > 128) return 0;
   // byte offsets of the code buffer stay 32-bit
   if (d.V * (d.d / 2) >= (int64_t(1) << 31)) return 0;
   for (int tok = kDecTok; tok >= 1; --tok)
@@ -96,7 +105,7 @@ bool mid_supported(const archead_desc& d) {
   // read as dwords, at most 128 dimensions per factor (4 K-chunks)
   if (d.g != 64 && d.g != 128) return false;
   if (d.d % (2 * kMidWindow) || d.d / d.g > 64) return false;
-  if (d.r_c % 4 || d.r_r % 4 || d.r_c > 128 || d.r_r > 128) return false;
+  if (d.r_c > 128 || d.r_r > 128) return false;
   return mid_lds(d).total <= kLdsBytes;
 }
 
@@ -175,6 +184,8 @@ archead_status archead_validate_desc(const archead_desc* p) {
     return fail(ARCHEAD_E_UNSUPPORTED, "scale_dtype must be ARCHEAD_F16 or ARCHEAD_U8");
   if (d.factor_dtype != ARCHEAD_I8)
     return fail(ARCHEAD_E_UNSUPPORTED, "factor_dtype must be ARCHEAD_I8");
+  if (d.core_u_dtype != ARCHEAD_I8 && d.core_u_dtype != ARCHEAD_I5)
+    return fail(ARCHEAD_E_UNSUPPORTED, "core_u_dtype must be ARCHEAD_I8 or ARCHEAD_I5");
   return ARCHEAD_OK;
 }
 
@@ -187,9 +198,42 @@ uint64_t archead_packed_bytes(const archead_desc* p) {
     b += V * (D / d.g) + V * 2;                                // 8-bit group codes + fp16 row scales
   else
     b += V * (D / d.g) * 2;                                    // fp16 group scales
-  if (d.r_c) b += V * d.r_c + V * 2 + d.r_c * D + d.r_c * (D / d.g_v) * 2;
+  if (d.r_c) b += V * uint64_t(core_u_row_bytes(d)) + V * 2 + d.r_c * D + d.r_c * (D / d.g_v) * 2;
   if (d.r_r) b += V * d.r_r + V * 2 + d.r_r * D + d.r_r * (D / d.g_b) * 2;
   return b;
+}
+
+archead_status archead_pack_int5(const int8_t* codes, int64_t rows, int64_t r, uint32_t* packed) {
+  if (!codes || !packed || rows < 0 || r < 1)
+    return fail(ARCHEAD_E_INVALID_ARG, "pack_int5: bad pointers or shape (r >= 1)");
+  const int64_t w5 = (r + 5) / 6;
+  for (int64_t row = 0; row < rows; ++row) {
+    for (int64_t w = 0; w < w5; ++w) {
+      uint32_t q = 0;
+      for (int64_t j = 0; j < 6 && 6 * w + j < r; ++j) {
+        const int v = codes[row * r + 6 * w + j];
+        if (v < -16 || v > 15)
+          return fail(ARCHEAD_E_INVALID_ARG, "pack_int5: code %d out of [-16, 15] at (%lld, %lld)",
+                      v, (long long)row, (long long)(6 * w + j));
+        q |= (uint32_t(v) & 31u) << (5 * j);
+      }
+      packed[row * w5 + w] = q;
+    }
+  }
+  return ARCHEAD_OK;
+}
+
+archead_status archead_unpack_int5(const uint32_t* packed, int64_t rows, int64_t r,
+                                   int8_t* codes) {
+  if (!codes || !packed || rows < 0 || r < 1)
+    return fail(ARCHEAD_E_INVALID_ARG, "unpack_int5: bad pointers or shape (r >= 1)");
+  const int64_t w5 = (r + 5) / 6;
+  for (int64_t row = 0; row < rows; ++row)
+    for (int64_t k = 0; k < r; ++k) {
+      const uint32_t f = (packed[row * w5 + k / 6] >> (5 * (k % 6))) & 31u;
+      codes[row * r + k] = int8_t(f >= 16 ? int(f) - 32 : int(f));
+    }
+  return ARCHEAD_OK;
 }
 
 archead_status archead_pack_int4(const int8_t* codes, int64_t rows, int64_t d,

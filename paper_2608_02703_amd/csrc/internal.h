@@ -52,6 +52,12 @@ void clear_error();
 // archead_create.
 archead_status scratch_setup(int device);
 
+// bytes per vocabulary row of core_u (int8 codes, or ARCHEAD_I5 words)
+int64_t core_u_row_bytes(const archead_desc& d);
+// how the kernels read the factor codes: 0 aligned int8 (ranks multiples of
+// 4); 1 int8 of any rank; 2 with the core-left codes in ARCHEAD_I5 words
+int gen_codes(const archead_desc& d);
+
 // chunk = 32 consecutive INT4 codes = 16 bytes; lanes per row of the GEMV
 int lanes_per_row(const archead_desc& d);
 

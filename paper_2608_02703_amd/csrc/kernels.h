@@ -1,0 +1,28 @@
+// Kernel entry points of the packed-head forward, one translation unit per
+// kernel family: each selector returns the device function to launch (with
+// hipExtLaunchKernel / hipLaunchKernel) for a variant.
+#pragma once
+
+namespace archead {
+namespace kern {
+
+// decode GEMV k_gemv<TOK, LPR, CE, SC8, GEN>: tok 1..4 tokens per pass, lpr
+// lanes per vocabulary row (1, 2, 4, ..., 64), ce fused softmax, sc8 8-bit
+// scales, gen the factor-code reads (0 aligned int8; 1 int8 of any rank; 2
+// with ARCHEAD_I5 core-left codes; 1 and 2 only for lpr 8 and 16, else null)
+const void* gemv(int tok, int lpr, bool ce, bool sc8, int gen);
+// MFMA decode kernel k_dec<GW, CE, EK, SC8, GEN>: gw = g / 32 code words per
+// lane and group (1, 2, 4), ek expansion K-chunks held (2 or 4), gen as for
+// gemv (every variant exists)
+const void* dec(int gw, bool ce, int ek, bool sc8, int gen);
+// several-token kernel k_mid: gw = g / 32 (2 or 4), gen as for dec
+const void* mid(int gw, bool ce, bool sc8, int gen);
+// tiled many-token kernel k_mfma<CE, TM> (tm = 256 or 128 token rows per
+// tile) and its prologue kernels
+const void* mfma(bool ce, int tm);
+const void* prep();
+const void* stage1m();
+const void* stage1m_fin();
+
+}  // namespace kern
+}  // namespace archead

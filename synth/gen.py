@@ -79,6 +79,7 @@ class HeadArrays:
                                        the layout notes in include/archead.h)
     res_scales   float16 [V, d/g]
     core_u       int8    [V, rc]       core_u_scale float16 [V]
+                 (or uint32 [V, ceil(rc/6)]: 5-bit codes, six per word)
     core_v       int8    [rc, d]       core_v_scale float16 [rc, d/gV]
     corr_a       int8    [V, rr]       corr_a_scale float16 [V]
     corr_b       int8    [rr, d]       corr_b_scale float16 [rr, d/gB]
@@ -125,9 +126,14 @@ def make_head(cfg="tiny", draw: int = 0, **over) -> HeadArrays:
     """Draw a packed head.  ``over`` may replace V, d, g, rc, rr, gV, gB (for
     ragged and degenerate shapes); gV/gB default to d (one scale per row).
     ``scales="u8"`` stores the residual group scales as 8-bit codes with an
-    fp16 scale per row (the same draws rounded to rs * q, rs = max / 255)."""
+    fp16 scale per row (the same draws rounded to rs * q, rs = max / 255).
+    ``core_u="i5"`` draws 5-bit core-left codes uniform in [-15, 15] and
+    stores them six per 32-bit word (uint32 [V, ceil(rc/6)]: field k of a
+    row at bits 5 (k % 6) of word k // 6, two's complement, unused bits
+    zero)."""
     c = _cfg(cfg)
     scales = over.pop("scales", "f16")
+    core_u_fmt = over.pop("core_u", "i8")
     unknown = set(over) - {"V", "d", "g", "rc", "rr", "gV", "gB", "cfg_id"}
     if unknown:
         raise TypeError(f"unknown head overrides {sorted(unknown)}")
@@ -142,7 +148,16 @@ def make_head(cfg="tiny", draw: int = 0, **over) -> HeadArrays:
     r = functools.partial(_rng, cid, draw=draw)
     res_codes = r("res_codes").integers(0, 256, size=(V, d // 2), dtype=np.uint8)
     res_scales = _fp16_abs_normal(r("res_scales"), RES_SCALE_SIGMA, (V, d // g))
-    core_u = _int8_uniform(r("core_u"), (V, rc))
+    if core_u_fmt == "i5":
+        f = r("core_u").integers(-15, 16, size=(V, rc)).astype(np.int64) & 31
+        w = np.zeros((V, (rc + 5) // 6), dtype=np.int64)
+        for k in range(rc):
+            w[:, k // 6] |= f[:, k] << (5 * (k % 6))
+        core_u = w.astype(np.uint32)
+    elif core_u_fmt == "i8":
+        core_u = _int8_uniform(r("core_u"), (V, rc))
+    else:
+        raise ValueError(f"core_u must be 'i8' or 'i5', not {core_u_fmt!r}")
     core_u_scale = _fp16_abs_normal(r("core_u_scale"), FACTOR_SCALE_SIGMA, (V,))
     core_v = _int8_uniform(r("core_v"), (rc, d))
     core_v_scale = _fp16_abs_normal(r("core_v_scale"), FACTOR_SCALE_SIGMA,

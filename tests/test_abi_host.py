@@ -49,7 +49,7 @@ def _desc(**kw):
     base = dict(V=1000, d=256, g=64, rc=8, rr=4)
     base.update(kw)
     extra = {k: base.pop(k) for k in ("gV", "gB", "abi", "enc", "scale_dtype",
-                                       "factor_dtype") if k in base}
+                                       "factor_dtype", "core_u_dtype") if k in base}
     return ab.Desc.make(base["V"], base["d"], base["g"], base["rc"], base["rr"],
                         **extra)
 
@@ -57,7 +57,10 @@ def _desc(**kw):
 @pytest.mark.parametrize("kw,status", [
     ({}, ab.OK),
     (dict(abi=1), ab.E_INVALID_ARG),           # another ABI version
-    (dict(abi=3), ab.E_INVALID_ARG),
+    (dict(abi=4), ab.E_INVALID_ARG),
+    (dict(abi=2), ab.E_INVALID_ARG),           # before the core_u_dtype field
+    (dict(core_u_dtype=ab.I5), ab.OK),
+    (dict(core_u_dtype=ab.BF16), ab.E_UNSUPPORTED),
     (dict(scale_dtype=ab.U8), ab.OK),          # 8-bit group scale codes
     (dict(V=0), ab.E_INVALID_ARG),
     (dict(d=0), ab.E_INVALID_ARG),
