@@ -464,7 +464,7 @@ void k_gemv(GemvArgs a) {
         const_cast<int8_t*>(a.cu), 0, int((a.cu_bytes + 3) & ~int64_t(3)), kBufferWord3);
     const __amdgpu_buffer_rsrc_t rca = __builtin_amdgcn_make_buffer_rsrc(
         const_cast<int8_t*>(a.ca), 0, int((a.ca_bytes + 3) & ~int64_t(3)), kBufferWord3);
-    auto load_exp = [&](int64_t stp, ExpOps<RB, KD>& e) {
+    auto load_exp = [&](int64_t stp, ExpOps<RB, KD>& e) __attribute__((always_inline)) {
       const int64_t v0 = stp * WR + seg;
 #pragma unroll
       for (int kd = 0; kd < KD; ++kd) {
