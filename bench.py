@@ -294,6 +294,22 @@ def time_argmax(heads, x, steps, warmup):
     return _timed_loop(step, steps)
 
 
+def time_topk(heads, x, k, steps, warmup):
+    """ms per top-k selection step (fused into the GEMV pass at M = 1)."""
+    import torch
+    M = x.shape[0]
+    wss = [hd.workspace(M, 3, x.device) for hd in heads]
+    vals = torch.empty((M, k), dtype=torch.float32, device=x.device)
+    idx = torch.empty((M, k), dtype=torch.int64, device=x.device)
+
+    def step(i):
+        j = i % len(heads)
+        heads[j].logits_topk(x, k, vals=vals, idx=idx, ws=wss[j])
+    for i in range(warmup):
+        step(i)
+    return _timed_loop(step, steps)
+
+
 def time_prefill(heads, x, y, steps, warmup, prepared=True):
     """(ms per step, mean CE, median many-token kernel ms).  prepared: the
     heads keep the many-token kernel's head-derived tables across calls
@@ -611,6 +627,14 @@ def main():
         greedy[str(M)] = {"us_per_step": round(gms * 1e3, 2),
                           "gbs_packed": round(pbytes / gms / 1e6, 1)}
         log(f"greedy (fused argmax) M={M}: {gms * 1e3:.1f} us/step")
+    # top-k selection (k = 10: the paper's largest top-k agreement; fused
+    # into the head pass at M = 1, over the logits in the workspace above)
+    topk = {}
+    for M in (1, 16):
+        tms = time_topk(heads, x_all[:M], 10, max(20, args.steps // 2), args.warmup)
+        topk[str(M)] = {"k": 10, "us_per_step": round(tms * 1e3, 2),
+                        "fused": M == 1}
+        log(f"top-10 selection M={M}: {tms * 1e3:.1f} us/step")
 
     # context: the same decode step through a dense bf16 head of the same
     # shape (torch linear, random weights), the bytes the packed head avoids
@@ -705,6 +729,7 @@ def main():
                             "gbs_packed": round(pbytes / v[0] / 1e6, 1)}
                    for M, v in res.items()},
         "greedy_argmax": greedy,
+        "topk_selection": topk,
         "decode_u8_scales": u8,
         "paper_storage_head": paper,
         "prefill": prefill,

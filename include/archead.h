@@ -98,7 +98,8 @@ typedef enum archead_int4_encoding { ARCHEAD_INT4_V1 = 1 } archead_int4_encoding
 typedef enum archead_op {
   ARCHEAD_OP_LOGITS = 0,    /* archead_logits    */
   ARCHEAD_OP_LOGITS_CE = 1, /* archead_logits_ce */
-  ARCHEAD_OP_ARGMAX = 2     /* archead_logits_argmax */
+  ARCHEAD_OP_ARGMAX = 2,    /* archead_logits_argmax */
+  ARCHEAD_OP_TOPK = 3       /* archead_logits_topk */
 } archead_op;
 
 /* Shape and encoding of a packed head (the "integer shapes/groups" metadata
@@ -268,6 +269,34 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x,
 archead_status archead_logits_argmax(const archead_handle* h, const void* x, int64_t M,
                                      int64_t ldx, int64_t* idx, float* max_logit, void* ws,
                                      size_t ws_bytes, void* stream);
+
+/* Largest k of archead_logits_topk. */
+#define ARCHEAD_TOPK_MAX 64
+
+/* Top-k selection over the packed head: for m < M and j < k, idx[m * ldk +
+ * j] is the j-th vocabulary index when the fp32 logits of token m (those
+ * archead_logits computes for the same M) are sorted by decreasing value,
+ * equal values by increasing index; vals[m * ldk + j] is its logit.  j = 0
+ * is archead_logits_argmax's index.  This is the candidate set of top-k
+ * decoding and of the top-k agreement metric ("Logit Fidelity", Section 4 and
+ * its Table 8: top-1, top-5, top-10).  A single token on the decode GEMV
+ * (M = 1 at the default ranges) selects inside the head pass: the [V]
+ * logits are never written, each workgroup leaves its k best pairs in the
+ * workspace and a merge kernel combines them.  Otherwise the logits of up to
+ * 256 tokens at a time go to the workspace in fp32 (about 256 * V * 4
+ * bytes) and a selection kernel reads them back.
+ *   k          1 <= k <= min(ARCHEAD_TOPK_MAX, V)
+ *   vals       device fp32 [M, ldk], 4-byte aligned, or NULL
+ *   idx        device int64 [M, ldk], 8-byte aligned; ldk >= k
+ *   ws         archead_workspace_bytes(h, M, ARCHEAD_OP_TOPK) bytes (it
+ *              holds lists of ARCHEAD_TOPK_MAX entries, so any k fits)
+ * NaN logits are never selected; slots that fewer than k non-NaN logits
+ * leave empty get (-inf, -1).  Other arguments and errors as
+ * archead_logits, plus ARCHEAD_E_INVALID_ARG for k out of range or
+ * ldk < k. */
+archead_status archead_logits_topk(const archead_handle* h, const void* x, int64_t M,
+                                   int64_t ldx, int32_t k, float* vals, int64_t* idx,
+                                   int64_t ldk, void* ws, size_t ws_bytes, void* stream);
 
 /* Bytes of the static workspace of archead_logits_noalloc, one array per
  * device the library runs on (kept until the process ends). */

@@ -70,6 +70,28 @@ def logit_fidelity(ref: np.ndarray, test: np.ndarray):
     return kl, sq, ref_idx, rank
 
 
+def topk(logits: np.ndarray, k: int):
+    """Top-k selection per row of `logits` [M, V]: the k entries that come
+    first when a row is sorted by decreasing value, equal values by
+    increasing index (the order behind the top-k agreement above and the
+    first-index argmax; the candidate set of top-k decoding).  NaN entries
+    are never selected; slots left empty (fewer than k non-NaN entries) are
+    (-inf, -1).  Returns (vals [M, k] in the input's precision, idx [M, k]
+    int64).  One library sort per row on the key (-value, index).
+    """
+    a = np.asarray(logits)
+    assert a.ndim == 2 and k >= 1
+    M, V = a.shape
+    vals = np.full((M, k), -np.inf, dtype=a.dtype)
+    idx = np.full((M, k), -1, dtype=np.int64)
+    for m in range(M):
+        ok = np.flatnonzero(~np.isnan(a[m]))
+        order = ok[np.lexsort((ok, -a[m, ok]))][:k]   # last key is the primary one
+        vals[m, :order.size] = a[m, order]
+        idx[m, :order.size] = order
+    return vals, idx
+
+
 def fidelity_summary(kl, sq, rank, ks=(1, 5, 10)) -> dict:
     """Table 8's aggregates over positions: mean KL, MSE (mean squared
     logit error summed over the vocabulary) and top-k agreement in percent."""

@@ -20,7 +20,8 @@ ABI_VERSION = 3
 OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
 F32, BF16, F16, I32, I64, I8, U8, I5 = range(8)
 INT4_V1 = 1
-OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX = 0, 1, 2
+OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX, OP_TOPK = 0, 1, 2, 3
+TOPK_MAX = 64
 NOALLOC_SCRATCH_BYTES = 4 << 20   # ARCHEAD_NOALLOC_SCRATCH_BYTES of include/archead.h
 
 
@@ -79,6 +80,10 @@ _SIGS = {
     "archead_logits_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_logits_topk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
+                                           ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                                           ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                                           ctypes.c_size_t, ctypes.c_void_p]),
     "archead_logits_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                               ctypes.c_int64, ctypes.c_void_p, ctypes.c_int,
                                               ctypes.c_int64, ctypes.c_void_p]),
@@ -487,6 +492,27 @@ class PackedHead:
             self.handle, _ptr(x), M, x.stride(0), _ptr(idx), _ptr(max_logit), _ptr(ws),
             ws.numel(), self._stream(x.device)), self._lib)
         return idx, max_logit
+
+    def logits_topk(self, x, k, vals=None, idx=None, ws=None):
+        """Top-k selection: returns (vals fp32 [M, k], idx int64 [M, k]), each
+        token's k largest logits in decreasing order, equal logits by
+        increasing index (archead_logits_topk)."""
+        import torch
+        if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+            raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+        M = x.shape[0]
+        if vals is None:
+            vals = torch.empty((M, k), dtype=torch.float32, device=x.device)
+        if idx is None:
+            idx = torch.empty((M, k), dtype=torch.int64, device=x.device)
+        if idx.dim() != 2 or idx.stride(1) != 1 or vals.dim() != 2 or vals.stride(1) != 1 or \
+                vals.stride(0) != idx.stride(0):
+            raise ValueError("vals and idx must be 2-D with unit column stride and one row stride")
+        ws = self.workspace(M, OP_TOPK, x.device) if ws is None else ws
+        _check(self._lib.archead_logits_topk(
+            self.handle, _ptr(x), M, x.stride(0), int(k), _ptr(vals), _ptr(idx), idx.stride(0),
+            _ptr(ws), ws.numel(), self._stream(x.device)), self._lib)
+        return vals, idx
 
     def logits_ce(self, x, targets, ce=None, mean=None, ws=None):
         """Fused log-softmax + cross-entropy; returns (ce [M], mean [1])."""

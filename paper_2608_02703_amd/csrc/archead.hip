@@ -185,17 +185,17 @@ bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) %
 
 namespace archead {
 
-int64_t gemv_grid(const archead_handle* h, int tok, bool ce) {
+int64_t gemv_grid(const archead_handle* h, int tok, bool ce, bool topk) {
   const bool sc8 = h->desc.scale_dtype == ARCHEAD_U8;
   const int gen = gemv_mode(h).gen;
-  const int slot = (gen ? 32 : 0) + (sc8 ? 16 : 0) + (ce ? 8 : 0) + tok;
+  const int slot = (topk ? 64 : 0) + (gen ? 32 : 0) + (sc8 ? 16 : 0) + (ce ? 8 : 0) + tok;
   archead_handle* mh = const_cast<archead_handle*>(h);
   int cached = mh->grid_cache[slot].load(std::memory_order_relaxed);
   const int64_t steps = (h->desc.V + gemv_rows_per_step(h->desc) - 1) / gemv_rows_per_step(h->desc);
   const int64_t max_blocks = (steps + kWaves - 1) / kWaves;
   if (cached <= 0) {
     const int lpr = lanes_per_row(h->desc);
-    const void* fn = kern::gemv(tok, lpr, ce, sc8, gen);
+    const void* fn = topk ? kern::gemv_topk(lpr, sc8, gen) : kern::gemv(tok, lpr, ce, sc8, gen);
     int nb = 0;
     const size_t lds = gemv_lds_bytes(h->desc, tok);
     if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn,
@@ -295,12 +295,68 @@ PrepLayout prep_layout(const archead_handle* h) {
   return p;
 }
 
+// Whether a top-k call of M tokens runs fused in the single-token GEMV.
+bool topk_fused(const archead_handle* h, int64_t M) {
+  return M == 1 && choose_path(h, 1) == Path::kGemv &&
+         kern::gemv_topk(lanes_per_row(h->desc), h->desc.scale_dtype == ARCHEAD_U8,
+                         gemv_mode(h).gen) != nullptr;
+}
+
+// Slices per token row of the top-k of a chunk of logits: enough that the
+// chunk's rows give about a thousand workgroups, at most 64.
+int64_t topk_row_parts(int64_t chunk) {
+  const int64_t np = (1024 + chunk - 1) / chunk;
+  return np < 1 ? 1 : (np > 64 ? 64 : np);
+}
+
+static WsLayout topk_layout(const archead_handle* h, int64_t M) {
+  WsLayout w;
+  const archead_desc& d = h->desc;
+  size_t off = 0;
+  int64_t rows = 1;
+  if (topk_fused(h, M)) {
+    w = ws_layout(h, 1, ARCHEAD_OP_LOGITS);   // the GEMV's stage-1 words
+    off = w.total;
+    w.tk_fused = true;
+    w.n_part = gemv_grid(h, 1, false, true);
+  } else {
+    const int64_t chunk = M < kTopKChunk ? M : kTopKChunk;
+    w.tk_chunk = chunk;
+    w.tk_lg_off = 0;
+    off = align256(sizeof(float) * size_t(chunk) * size_t(d.V));
+    w.tk_in_off = off;
+    // every chunk runs on the kernel the whole call would take, so the
+    // logits are those archead_logits gives for the same M
+    w.tk_path = choose_path(h, M);
+    size_t inner = ws_layout_path(h, chunk, ARCHEAD_OP_LOGITS, w.tk_path).total;
+    if (M % chunk) {
+      const size_t t = ws_layout_path(h, M % chunk, ARCHEAD_OP_LOGITS, w.tk_path).total;
+      inner = t > inner ? t : inner;
+    }
+    off = align256(off + inner);
+    w.n_part = topk_row_parts(chunk);
+    rows = chunk;
+  }
+  const size_t lists = size_t(rows) * size_t(w.n_part) * kTopKMaxK;
+  w.tk_pv_off = off;
+  off = align256(off + sizeof(float) * lists);
+  w.tk_pi_off = off;
+  off = align256(off + sizeof(int32_t) * lists);
+  w.total = off;
+  return w;
+}
+
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
+  if (h && M > 0 && op == ARCHEAD_OP_TOPK) return topk_layout(h, M);
+  return ws_layout_path(h, M, op, h ? choose_path(h, M) : Path::kGemv);
+}
+
+// The layout for M tokens on the kernel `path`.
+WsLayout ws_layout_path(const archead_handle* h, int64_t M, archead_op op, Path path) {
   WsLayout w;
   if (!h || M <= 0) return w;
   const archead_desc& d = h->desc;
   size_t off = 0;
-  const Path path = choose_path(h, M);
   const bool dec = path == Path::kDec, mid = path == Path::kMid, gemv = path == Path::kGemv;
   if (dec || mid) {
     w.tst_off = off;
@@ -538,7 +594,7 @@ GemvArgs gemv_args(const archead_handle* h, const void* x, int64_t ldx, uint64_t
 // One launch per group of up to 4 tokens.  forced_grid > 0 fixes the grid
 // (the CE passes, whose partials are indexed by workgroup).
 archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M, bool ce,
-                                  int64_t forced_grid, hipStream_t s) {
+                                  int64_t forced_grid, hipStream_t s, bool topk = false) {
   const int lpr = lanes_per_row(h->desc);
   // timing events (if set) are attached to the first and last dispatch
   // packets themselves, so they bracket exactly the kernel execution
@@ -547,7 +603,8 @@ archead_status launch_gemv_passes(const archead_handle* h, GemvArgs a, int64_t M
   for (int64_t m0 = 0; m0 < M; m0 += 4) {
     const int tok = int(M - m0 < 4 ? M - m0 : 4);
     const bool sc8 = h->desc.scale_dtype == ARCHEAD_U8;
-    const void* fn = kern::gemv(tok, lpr, ce, sc8, gemv_mode(h).gen);
+    const void* fn = topk ? kern::gemv_topk(lpr, sc8, gemv_mode(h).gen)
+                          : kern::gemv(tok, lpr, ce, sc8, gemv_mode(h).gen);
     const int64_t grid = a.n_prod_blocks + (forced_grid > 0 ? forced_grid : gemv_grid(h, tok, ce));
     a.tok0 = m0;
     const size_t lds = gemv_lds_bytes(h->desc, tok);
@@ -777,6 +834,50 @@ archead_status launch_softmax_partials(const archead_handle* h, const void* x, i
   return launch_gemv_passes(h, a, M, true, n_part, s);
 }
 
+// The logits of archead_logits after its checks (also the first half of
+// the unfused top-k).
+archead_status logits_run(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
+                          void* out, archead_dtype out_dtype, int64_t ldo, void* ws,
+                          hipStream_t s, Path path) {
+  archead_status st = ARCHEAD_OK;
+  const WsLayout w = ws_layout_path(h, M, ARCHEAD_OP_LOGITS, path);
+  if (path == Path::kDec) {
+    DecArgs a;
+    memset(&a, 0, sizeof a);
+    a.out = out;
+    a.ldo = ldo;
+    a.out_bf16 = out_dtype == ARCHEAD_BF16;
+    return launch_dec(h, x, M, ldx,
+                      reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off), a, false,
+                      s);
+  }
+  if (path == Path::kMid) {
+    MidArgs a;
+    memset(&a, 0, sizeof a);
+    a.out = out;
+    a.ldo = ldo;
+    a.out_bf16 = out_dtype == ARCHEAD_BF16;
+    return launch_mid(h, x, M, ldx,
+                      reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off), a, false,
+                      s);
+  }
+  if (path == Path::kTiled) {
+    st = launch_mfma_prologue(h, x, M, ldx, w, static_cast<char*>(ws), s);
+    if (st != ARCHEAD_OK) return st;
+    MfmaArgs a = mfma_args(h, x, M, ldx, w, static_cast<char*>(ws));
+    a.out = out;
+    a.ldo = ldo;
+    a.out_bf16 = out_dtype == ARCHEAD_BF16;
+    return launch_mfma(h, a, false, s);
+  }
+  GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off));
+  a.out = out;
+  a.ldo = ldo;
+  a.out_bf16 = out_dtype == ARCHEAD_BF16;
+  return launch_gemv_passes(h, a, M, false, 0, s);
+}
+
+
 }  // namespace
 
 extern "C" {
@@ -892,43 +993,8 @@ archead_status archead_logits(const archead_handle* h, const void* x, int64_t M,
   if (ldo < h->desc.V) return fail(ARCHEAD_E_INVALID_ARG, "ldo < V");
   if (!aligned(out, out_dtype == ARCHEAD_F32 ? 4 : 2))
     return fail(ARCHEAD_E_MISALIGNED, "out is not aligned to its element size");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const WsLayout w = ws_layout(h, M, ARCHEAD_OP_LOGITS);
-  const Path path = choose_path(h, M);
-  if (path == Path::kDec) {
-    DecArgs a;
-    memset(&a, 0, sizeof a);
-    a.out = out;
-    a.ldo = ldo;
-    a.out_bf16 = out_dtype == ARCHEAD_BF16;
-    return launch_dec(h, x, M, ldx,
-                      reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off), a, false,
-                      s);
-  }
-  if (path == Path::kMid) {
-    MidArgs a;
-    memset(&a, 0, sizeof a);
-    a.out = out;
-    a.ldo = ldo;
-    a.out_bf16 = out_dtype == ARCHEAD_BF16;
-    return launch_mid(h, x, M, ldx,
-                      reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off), a, false,
-                      s);
-  }
-  if (path == Path::kTiled) {
-    st = launch_mfma_prologue(h, x, M, ldx, w, static_cast<char*>(ws), s);
-    if (st != ARCHEAD_OK) return st;
-    MfmaArgs a = mfma_args(h, x, M, ldx, w, static_cast<char*>(ws));
-    a.out = out;
-    a.ldo = ldo;
-    a.out_bf16 = out_dtype == ARCHEAD_BF16;
-    return launch_mfma(h, a, false, s);
-  }
-  GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(static_cast<char*>(ws) + w.tst_off));
-  a.out = out;
-  a.ldo = ldo;
-  a.out_bf16 = out_dtype == ARCHEAD_BF16;
-  return launch_gemv_passes(h, a, M, false, 0, s);
+  return logits_run(h, x, M, ldx, out, out_dtype, ldo, ws, static_cast<hipStream_t>(stream),
+                    choose_path(h, M));
 }
 
 archead_status archead_logits_ce(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
@@ -983,6 +1049,61 @@ archead_status archead_logits_argmax(const archead_handle* h, const void* x, int
                      w.n_part, idx, max_logit);
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "argmax merge launch");
+}
+
+archead_status archead_logits_topk(const archead_handle* h, const void* x, int64_t M,
+                                   int64_t ldx, int32_t k, float* vals, int64_t* idx,
+                                   int64_t ldk, void* ws, size_t ws_bytes, void* stream) {
+  clear_error();
+  if (h && (k < 1 || k > kTopKMaxK || int64_t(k) > h->desc.V))
+    return fail(ARCHEAD_E_INVALID_ARG, "k = %d is outside 1 .. min(%d, V)", int(k), kTopKMaxK);
+  archead_status st = check_call(h, x, M, ldx, ws, ws_bytes, ARCHEAD_OP_TOPK);
+  if (st != ARCHEAD_OK || M == 0) return st;
+  if (!idx) return fail(ARCHEAD_E_INVALID_ARG, "idx is required");
+  if (ldk < k) return fail(ARCHEAD_E_INVALID_ARG, "ldk < k");
+  if (!aligned(idx, 8) || (vals && !aligned(vals, 4)))
+    return fail(ARCHEAD_E_MISALIGNED, "idx / vals misaligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const WsLayout w = ws_layout(h, M, ARCHEAD_OP_TOPK);
+  char* base = static_cast<char*>(ws);
+  float* pv = reinterpret_cast<float*>(base + w.tk_pv_off);
+  int* pi = reinterpret_cast<int*>(base + w.tk_pi_off);
+  int64_t np = w.n_part;
+  hipError_t e;
+  if (w.tk_fused) {
+    GemvArgs a = gemv_args(h, x, ldx, reinterpret_cast<uint64_t*>(base + w.tst_off));
+    a.tk_val = pv;
+    a.tk_idx = pi;
+    a.tk_k = k;
+    a.n_part = np;
+    st = launch_gemv_passes(h, a, 1, false, np, s, true);
+    if (st != ARCHEAD_OK) return st;
+    void* margs[] = {&pv, &pi, &np, &k, &vals, &idx, &ldk};
+    e = hipLaunchKernel(kern::topk_merge(), dim3(1), dim3(kBlock), margs, 0, s);
+    return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "top-k merge launch");
+  }
+  const int64_t V = h->desc.V;
+  float* lg = reinterpret_cast<float*>(base + w.tk_lg_off);
+  // slices of whole 64-logit steps
+  int64_t slice = (V + np - 1) / np;
+  slice = (slice + 63) / 64 * 64;
+  for (int64_t m0 = 0; m0 < M; m0 += w.tk_chunk) {
+    const int64_t mc = M - m0 < w.tk_chunk ? M - m0 : w.tk_chunk;
+    st = logits_run(h, static_cast<const uint16_t*>(x) + m0 * ldx, mc, ldx, lg, ARCHEAD_F32, V,
+                    base + w.tk_in_off, s, w.tk_path);
+    if (st != ARCHEAD_OK) return st;
+    int64_t ldl = V;
+    void* rargs[] = {&lg, &ldl, const_cast<int64_t*>(&V), &k, &slice, &pv, &pi};
+    e = hipLaunchKernel(kern::topk_rows(), dim3(unsigned(np), unsigned(mc)), dim3(kBlock), rargs,
+                        0, s);
+    if (e != hipSuccess) return hip_fail(e, "top-k rows launch");
+    float* vo = vals ? vals + m0 * ldk : nullptr;
+    int64_t* io = idx + m0 * ldk;
+    void* margs[] = {&pv, &pi, &np, &k, &vo, &io, &ldk};
+    e = hipLaunchKernel(kern::topk_merge(), dim3(unsigned(mc)), dim3(kBlock), margs, 0, s);
+    if (e != hipSuccess) return hip_fail(e, "top-k merge launch");
+  }
+  return ARCHEAD_OK;
 }
 
 }  // extern "C"

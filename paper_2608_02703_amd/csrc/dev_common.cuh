@@ -324,12 +324,15 @@ __device__ __forceinline__ int fcode1(const uint8_t* rowp, int k, bool u5) {
   return int(int8_t(rowp[k]));
 }
 
-// Per-lane softmax state of the fused CE epilogue.
+// Per-lane state of the fused epilogues (softmax, argmax, top-k).
 template <int TOK>
 struct CeState {
   float mx[TOK], se[TOK];
   int am[TOK];      // smallest vocabulary index attaining mx so far
   int64_t y[TOK];
+  // top-k variants: this lane's slot of the wave's list and the list's bar
+  float tv[TOK], bv[TOK];
+  int ti[TOK], bi[TOK];
 };
 
 // "no index yet" for the argmax partials: larger than any vocabulary index
@@ -441,6 +444,75 @@ __device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint32_t w0, uint32_t w1) {
     p[j] = __builtin_amdgcn_perm(__float_as_uint(hi), __float_as_uint(lo), 0x07060302u);
   }
   return __builtin_bit_cast(bf16x8_t, p);
+}
+
+// ------------------------------------------------------------ top-k lists
+// A wave keeps the k best (value, index) pairs it has seen as one sorted
+// list spread over its lanes: lane j < k holds the j-th best, in the order
+// "larger value first, equal values by smaller index" (the order of the
+// first-index argmax); lanes j >= k and unfilled slots hold the empty entry
+// (-inf, kNoIdx), which no entry is ranked below.  NaN values never enter.
+// Every helper here is called by all 64 lanes of the wave together, with a
+// wave-uniform k (1 <= k <= 64).
+constexpr int kTopKMax = 64;
+
+__device__ __forceinline__ bool tk_better(float av, int ai, float bv, int bi) {
+  return av > bv || (av == bv && ai < bi);
+}
+
+__device__ __forceinline__ float rlane_f(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+
+// Insert the wave-uniform pair (cv, ci): it lands at the first slot it is
+// ranked above, the entries from there on move down one lane, the k-th drops
+// out.  (bv, bi), the list's k-th entry (the bar a pair must beat to enter),
+// is refreshed.
+__device__ __forceinline__ void tk_insert(float& lv, int& li, float& bv, int& bi, float cv,
+                                          int ci, int lane, int k) {
+  const float pv = __shfl_up(lv, 1, 64);
+  const int pi = __shfl_up(li, 1, 64);
+  const bool here = lane < k && tk_better(cv, ci, lv, li);
+  const bool above = lane > 0 && tk_better(cv, ci, pv, pi);
+  lv = here ? (above ? pv : cv) : lv;
+  li = here ? (above ? pi : ci) : li;
+  bv = rlane_f(lv, k - 1);
+  bi = __builtin_amdgcn_readlane(li, k - 1);
+}
+
+// Offer one pair per lane (taken where ok): the pairs that beat the bar
+// enter one at a time, in lane order.
+__device__ __forceinline__ void tk_offer(float& lv, int& li, float& bv, int& bi, float v, int i,
+                                         bool ok, int lane, int k) {
+  uint64_t m = __ballot(ok && tk_better(v, i, bv, bi));
+  while (m) {
+    const int s = __builtin_ctzll(m);
+    m &= m - 1;
+    const float cv = rlane_f(v, s);
+    const int ci = __builtin_amdgcn_readlane(i, s);
+    if (tk_better(cv, ci, bv, bi)) tk_insert(lv, li, bv, bi, cv, ci, lane, k);
+  }
+}
+
+// Merge the lists of a workgroup's NW waves into wave 0's (the other waves'
+// lists are inserted in wave order; each is sorted, so its first entry
+// that fails the bar ends it).  sv / si: LDS of NW * 64 entries.  Contains
+// a barrier: every wave of the workgroup calls it.
+template <int NW>
+__device__ __forceinline__ void tk_block_merge(float& lv, int& li, float& bv, int& bi, int lane,
+                                               int wid, int k, float* sv, int* si) {
+  sv[wid * 64 + lane] = lv;
+  si[wid * 64 + lane] = li;
+  __syncthreads();
+  if (wid == 0) {
+    for (int w = 1; w < NW; ++w)
+      for (int j = 0; j < k; ++j) {
+        const float cv = __int_as_float(__builtin_amdgcn_readfirstlane(__float_as_int(sv[w * 64 + j])));
+        const int ci = __builtin_amdgcn_readfirstlane(si[w * 64 + j]);
+        if (!tk_better(cv, ci, bv, bi)) break;
+        tk_insert(lv, li, bv, bi, cv, ci, lane, k);
+      }
+  }
 }
 
 

@@ -48,6 +48,11 @@ struct GemvArgs {
   int* part_idx;   // [M, n_part] argmax partials, or null
   int64_t n_part;
   float* tgt_logit;  // [M]
+  // fused top-k (single-token variants): per workgroup the k best
+  // (logit, index) pairs of the token, [n_part][k]
+  float* tk_val;
+  int* tk_idx;
+  int tk_k;
 };
 
 // Sum RB per-lane values over the LPR lanes of each segment.  The first
@@ -213,7 +218,7 @@ __device__ __forceinline__ void gemv_chunk(float (&acc)[RB][TOK], const uint4 (&
 // End of a step: add the rank-r expansions of the lane's rows, reduce over
 // the segment and store the logits (or fold them into the softmax state).
 // Row rb of the lane is row0 + min(seg + rb * SEG, lim).
-template <int TOK, int LPR, int RB, bool CE, bool EXPAND>
+template <int TOK, int LPR, int RB, bool CE, bool EXPAND, bool TK>
 __device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvArgs& a,
                                               int64_t row0, uint32_t lim, int seg, int sl,
                                               int lane, int my_row, bool writer,
@@ -253,7 +258,9 @@ __device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvA
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) col[rb] = acc[rb][tt];
     const float l = seg_reduce_rows<LPR, RB>(col, lane);
-    if (store) {
+    if constexpr (TK) {
+      tk_offer(ce.tv[tt], ce.ti[tt], ce.bv[tt], ce.bi[tt], l, int(v), store, lane, a.tk_k);
+    } else if (store) {
       if constexpr (!CE) {
         const int64_t o = (a.tok0 + tt) * a.ldo + v;
         if (a.out_bf16)
@@ -291,7 +298,8 @@ __device__ __forceinline__ void gemv_epilogue(float (&acc)[RB][TOK], const GemvA
 // GEN: how the pipelined path reads the rank-r codes: 0 as aligned dwords
 // (int8 codes, ranks that are multiples of 4); 1 through fcodes4 (int8 codes,
 // any rank); 2 the same with the core-left codes in ARCHEAD_I5 words.
-template <int TOK, int LPR, bool CE, bool SC8, int GEN>
+// TK: the single-token top-k variant (no logit store; CE false).
+template <int TOK, int LPR, bool CE, bool SC8, int GEN, bool TK = false>
 __global__ __launch_bounds__(kBlock)
 __attribute__((amdgpu_waves_per_eu(TOK == 1 ? (LPR >= 64 ? ARCHEAD_GEMV_WAVES : ARCHEAD_GEMV_WAVES_NARROW) : 1)))
 void k_gemv(GemvArgs a) {
@@ -387,6 +395,10 @@ void k_gemv(GemvArgs a) {
     ce.se[tt] = 0.f;
     ce.am[tt] = kNoIdx;
     ce.y[tt] = -1;
+    ce.tv[tt] = -INFINITY;
+    ce.ti[tt] = kNoIdx;
+    ce.bv[tt] = -INFINITY;
+    ce.bi[tt] = kNoIdx;
     if constexpr (CE)
       if (a.tgt)
         ce.y[tt] = a.tgt64 ? reinterpret_cast<const int64_t*>(a.tgt)[a.tok0 + tt]
@@ -553,7 +565,7 @@ void k_gemv(GemvArgs a) {
         }
         apply_expansion<TOK, RB, KD, LPR>(acc, e, st, Rq, sl);
         load_exp(more ? nstep : cstep, e);
-        gemv_epilogue<TOK, LPR, RB, CE, false>(acc, a, cstep * WR, uint32_t(WR - 1), seg, sl,
+        gemv_epilogue<TOK, LPR, RB, CE, false, TK>(acc, a, cstep * WR, uint32_t(WR - 1), seg, sl,
                                                lane, my_row, writer, st, ce);
       }
       cstep = nstep;
@@ -612,7 +624,7 @@ void k_gemv(GemvArgs a) {
         for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] *= f;
       }
     }
-    gemv_epilogue<TOK, LPR, RB, CE, true>(acc, a, row0, lim, seg, sl, lane, my_row, writer, st,
+    gemv_epilogue<TOK, LPR, RB, CE, true, TK>(acc, a, row0, lim, seg, sl, lane, my_row, writer, st,
                                           ce);
   }
 
@@ -648,6 +660,23 @@ void k_gemv(GemvArgs a) {
         for (int w = 0; w < kWaves; ++w)
           if (red[w][tt].x == m) ai = min(ai, redi[w][tt]);
         a.part_idx[o] = ai;
+      }
+    }
+  }
+  if constexpr (TK) {
+    // the waves' lists merged into wave 0's, which leaves them as this
+    // workgroup's partial
+    __shared__ float tks_v[kWaves * 64];
+    __shared__ int tks_i[kWaves * 64];
+#pragma unroll
+    for (int tt = 0; tt < TOK; ++tt) {
+      if (tt) __syncthreads();
+      tk_block_merge<kWaves>(ce.tv[tt], ce.ti[tt], ce.bv[tt], ce.bi[tt], lane, wid, a.tk_k, tks_v,
+                             tks_i);
+      if (wid == 0 && lane < a.tk_k) {
+        const int64_t o = ((a.tok0 + tt) * a.n_part + (blockIdx.x - a.n_prod_blocks)) * a.tk_k + lane;
+        a.tk_val[o] = ce.tv[tt];
+        a.tk_idx[o] = ce.ti[tt];
       }
     }
   }

@@ -21,7 +21,7 @@ struct archead_handle {
   int t_spin_limit;       // polls of the in-launch stage-1 exchange before the fallback
   // persistent-grid sizes found with the occupancy API, keyed by kernel
   // variant; 0 = not computed yet
-  std::atomic<int> grid_cache[64];
+  std::atomic<int> grid_cache[128];
   // caller-owned hipEvent_t pair recorded around the head-streaming kernel
   std::atomic<void*> ev_start;
   std::atomic<void*> ev_stop;
@@ -43,6 +43,8 @@ constexpr int64_t kLdsBytes = 160 * 1024; // LDS per workgroup on gfx950
 constexpr int kMidTokMax = 32;            // tokens per tile of the several-token kernel
 constexpr int kMidWindow = 256;           // elements of d per x window of that kernel
 constexpr int kMidWaveCount = 8;          // its waves per workgroup
+constexpr int kTopKMaxK = 64;             // largest k of archead_logits_topk (lanes of a wave)
+constexpr int64_t kTopKChunk = 256;       // tokens per chunk of the unfused top-k
 
 archead_status fail(archead_status s, const char* fmt, ...);
 void clear_error();
@@ -62,6 +64,9 @@ int gen_codes(const archead_desc& d);
 int lanes_per_row(const archead_desc& d);
 
 // Workspace carve-up (byte offsets, each 256-aligned).
+// kernel family serving a call
+enum class Path { kDec, kMid, kGemv, kTiled };
+
 struct WsLayout {
   size_t tst_off = 0;    // u64 [M, r_c + r_r] stamped t (decode and several-token kernels)
   // many-token (MFMA) path only:
@@ -75,10 +80,21 @@ struct WsLayout {
   size_t part_off = 0;   // float2 [M, n_part] (CE)
   size_t tgt_off = 0;    // fp32 [M] (CE)
   size_t pidx_off = 0;   // int32 [M, n_part] (argmax)
+  // top-k: fused (single token on the decode GEMV) or over chunks of up to
+  // kTopKChunk tokens whose fp32 logits go to lg_off, computed with the
+  // workspace at in_off
+  bool tk_fused = false;
+  int64_t tk_chunk = 0;   // tokens per chunk (unfused)
+  size_t tk_lg_off = 0;   // fp32 [chunk][V]
+  size_t tk_in_off = 0;   // workspace of the chunk's logits call
+  size_t tk_pv_off = 0;   // fp32 [chunk or 1][n_part][kTopKMax] partial lists
+  size_t tk_pi_off = 0;   // int32, the same shape
+  Path tk_path = Path::kGemv;   // kernel of the chunks' logits (that of the whole M)
   size_t total = 0;
   int64_t n_part = 0;
 };
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op);
+WsLayout ws_layout_path(const archead_handle* h, int64_t M, archead_op op, Path path);
 
 // The many-token kernel's tables that depend on the head only (scale
 // ratios, final scales, bf16 V_c / B_w codes, paired U_c / A_w codes):
@@ -121,11 +137,10 @@ void default_ranges(const archead_desc& d, int64_t (&r)[4]);
 // The kernel a call with M tokens runs on: the MFMA decode kernel, the
 // several-token kernel, the decode GEMV or the tiled MFMA kernel, in that
 // order of preference where the M ranges and the head shape allow.
-enum class Path { kDec, kMid, kGemv, kTiled };
 Path choose_path(const archead_handle* h, int64_t M);
 
 // grid of the GEMV kernel: persistent workgroups, at most one per 8 rows
-int64_t gemv_grid(const archead_handle* h, int tok, bool ce);
+int64_t gemv_grid(const archead_handle* h, int tok, bool ce, bool topk = false);
 
 struct DecGrid {
   int prod_blocks = 0;          // stage-1 producer workgroups (first in the grid)

@@ -11,6 +11,12 @@ namespace kern {
 // scales, gen the factor-code reads (0 aligned int8; 1 int8 of any rank; 2
 // with ARCHEAD_I5 core-left codes; 1 and 2 only for lpr 8 and 16, else null)
 const void* gemv(int tok, int lpr, bool ce, bool sc8, int gen);
+// the single-token GEMV with the fused top-k epilogue (k_gemv<1, LPR, false,
+// SC8, GEN, true>; null where gemv has no such variant), the top-k of rows
+// of fp32 logits and the merge of per-partial top-k lists
+const void* gemv_topk(int lpr, bool sc8, int gen);
+const void* topk_rows();
+const void* topk_merge();
 // MFMA decode kernel k_dec<GW, CE, EK, SC8, GEN>: gw = g / 32 code words per
 // lane and group (1, 2, 4), ek expansion K-chunks held (2 or 4), gen as for
 // gemv (every variant exists)

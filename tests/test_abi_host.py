@@ -170,6 +170,9 @@ def test_null_handle_calls(L):
         ab.E_INVALID_ARG
     assert L.archead_logits_ce(None, None, 1, 8, None, ab.I32, None, None, None, 0,
                                None) == ab.E_INVALID_ARG
+    assert L.archead_logits_topk(None, None, 1, 8, 5, None, None, 5, None, 0, None) == \
+        ab.E_INVALID_ARG
+    assert L.archead_workspace_bytes(None, 4, ab.OP_TOPK) == 0
     assert L.archead_set_gemv_max_m(None, 3) == ab.E_INVALID_ARG
     assert L.archead_get_gemv_max_m(None) == -1
     assert L.archead_prepared_bytes(None) == 0
