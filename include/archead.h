@@ -213,7 +213,7 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *     which streams the head once per pass of up to 16 tokens (fewer when
  *     16 rows of x do not fit in LDS);
  *   - otherwise M in the range of archead_set_mid_range (default: from one
- *     past the decode kernel's range to 64) with g in {64, 128},
+ *     past the decode kernel's range to 32, one pass) with g in {64, 128},
  *     d % 512 == 0, d/g <= 64, r_c and r_r multiples of 4 and at most 128
  *     each: the several-token kernel, which streams the head once per tile
  *     of up to 32 tokens (x held in LDS in windows of 256 elements of d);
@@ -223,8 +223,10 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  * (a few leading workgroups publish t with a per-call stamp in the
  * workspace; the others wait for it a bounded time and otherwise compute it
  * themselves), so a decode step is a single kernel launch;
- *   - otherwise the tiled bf16 MFMA kernel (256 x 256 tiles of tokens x
- *     vocabulary rows).
+ *   - otherwise the tiled bf16 MFMA kernel (tiles of 128 tokens x 256
+ *     vocabulary rows, two workgroups per CU, up to M = 1024; 256 x 256
+ *     tiles above; its head-derived tables are built per call unless
+ *     archead_prepare keeps them).
  * All produce fp32 logits from fp32 accumulation.  The tiled kernel carries
  * its accumulator in units of the current scale group's scale and feeds the
  * rank-r expansion t as three bf16 parts (t to fp32 precision), so its
@@ -313,7 +315,7 @@ archead_status archead_logits_topk(const archead_handle* h, const void* x, int64
  *   Limit: M whose archead_workspace_bytes(h, M, ARCHEAD_OP_LOGITS) exceeds
  *   ARCHEAD_NOALLOC_SCRATCH_BYTES is rejected with ARCHEAD_E_WORKSPACE (the
  *   decode-shaped paths fit: at the Qwen3-8B shape, r_c + r_r = 96, every M
- *   up to 64; the many-token path's per-call tables do not).
+ *   up to 32; the many-token path's per-call tables do not).
  *   All calls on one GPU share that GPU's array, which keeps the last call's
  *   contents (no call needs it cleared): calls that overlap on one GPU, on
  *   different streams or from different threads, race and give undefined

@@ -729,10 +729,28 @@ archead_status launch_mid(const archead_handle* h, const void* x, int64_t M, int
   return ARCHEAD_OK;
 }
 
-// Token rows per tile of the tiled kernel: 128 for calls of at most 128
-// tokens (the 256-row tile would spend half or more of its MFMA work on
+// Token rows per tile of the 8-wave tiled kernel: 128 for calls of at most
+// 128 tokens (the 256-row tile would spend half or more of its MFMA work on
 // padding rows), else 256.
 int tiled_tm(int64_t M) { return M <= 128 ? 128 : kTM; }
+
+// Tile rows and waves per workgroup of the tiled kernel for a call of M
+// tokens: 128-row tiles of 4 waves, two workgroups per CU, up to
+// kTiledNw4MaxM tokens (measured 10-25% faster than one workgroup of 8
+// waves per CU at M = 16 .. 1024, where tile starts, LDS waits and the
+// epilogue would leave the matrix unit idle); above, 256-row tiles of 8
+// waves (equal at M = 4096, where the chip runs at its power limit).
+// ARCHEAD_MFMA_NW = 4 or 8 overrides the choice (tuning only).
+constexpr int64_t kTiledNw4MaxM = 1024;
+struct TiledShape { int tm, nw; };
+TiledShape tiled_shape(int64_t M) {
+  TiledShape t = M <= kTiledNw4MaxM ? TiledShape{128, 4} : TiledShape{kTM, 8};
+  if (const char* e = getenv("ARCHEAD_MFMA_NW")) {
+    if (atoi(e) == 4) t = TiledShape{128, 4};
+    else if (atoi(e) == 8) t = TiledShape{tiled_tm(M), 8};
+  }
+  return t;
+}
 
 MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ldx,
                    const WsLayout& w, char* ws) {
@@ -754,7 +772,7 @@ MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ld
   a.nslot = int(d.d / d.g) + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
   a.nch_u = exp_chunks(d.r_c);
   a.nch = a.nch_u + exp_chunks(d.r_r);
-  const int tm = tiled_tm(M);
+  const int tm = tiled_shape(M).tm;
   a.n_mt = (M + tm - 1) / tm;
   a.n_vt = (d.V + kTN - 1) / kTN;
   a.n_tiles = a.n_vt * a.n_mt;
@@ -766,9 +784,9 @@ archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStr
   // byte ranges of one tile's buffers must stay below 2 GiB
   if (int64_t(kTM) * a.ldx * 2 >= (int64_t(1) << 31))
     return fail(ARCHEAD_E_UNSUPPORTED, "ldx too large for the many-token kernel");
-  const int tm = tiled_tm(a.M);
-  const void* fn = kern::mfma(ce, tm);
-  const int lds = tm == 128 ? MGeomT<128>::LDS : MGeom::LDS;
+  const TiledShape ts = tiled_shape(a.M);
+  const void* fn = kern::mfma(ce, ts.tm, ts.nw);
+  const int lds = ts.nw == 4 ? MGeomT<128, 4>::LDS : ts.tm == 128 ? MGeomT<128>::LDS : MGeom::LDS;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return hip_fail(e, "MFMA LDS size attribute");
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));
@@ -776,7 +794,8 @@ archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStr
   void* args[] = {&a};
   const int64_t grid = 8 * a.tiles_per_xcd;
   if (grid > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "too many MFMA tiles");
-  e = hipExtLaunchKernel(fn, dim3(unsigned(grid)), dim3(kMBlock), args, size_t(lds), s, ev0, ev1, 0);
+  e = hipExtLaunchKernel(fn, dim3(unsigned(grid)), dim3(unsigned(ts.nw * 64)), args, size_t(lds), s,
+                         ev0, ev1, 0);
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "MFMA launch");
 }
 

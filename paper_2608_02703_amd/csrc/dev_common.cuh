@@ -351,21 +351,31 @@ constexpr int kRasterGM = 2;                 // token tiles per raster group
 constexpr float kZeroScale = 0x1p-60f;       // stand-in for a zero scale
 constexpr int kExpDims = 16;                 // rank dimensions per expansion stage
 
-// LDS geometry of a stage of the tiled kernel with TM token rows (256, or
-// 128 for calls with few tokens: half the padded MFMA work at M <= 128).
-template <int TM>
+// Geometry of the tiled kernel for TM token rows per tile and NW waves per
+// workgroup: NW = 8 (2 x 4 waves of TM/2 x 64; one workgroup per CU) or
+// NW = 4 (1 x 4 waves of TM x 64, TM = 128; two workgroups per CU, whose
+// stage barriers are independent, so one's LDS waits, tile start and
+// epilogue overlap the other's MFMAs).  A stage holds x [TM][kKS] bf16,
+// codes [kTN][kKS/2], the scale ratios of the kTN columns and the slot
+// biases of the TM rows.
+template <int TM, int NW = kMWaves>
 struct MGeomT {
+  static constexpr int WMW = NW / 4;                  // waves along the tokens
+  static constexpr int WM = TM / WMW;                 // token rows per wave
+  static constexpr int MI = WM / 16;                  // 16-row MFMA blocks per wave
   static constexpr int XBYTES = TM * kKS * 2;         // x [TM][kKS] bf16
   static constexpr int CBYTES = kTN * kKS / 2;        // codes [kTN][kKS/2]
   static constexpr int RAT = XBYTES + CBYTES;         // fp32 [kTN] scale ratios
   static constexpr int BIAS = RAT + kTN * 4;          // fp32 [TM] slot biases
   static constexpr int STAGE = BIAS + TM * 4;
-  static constexpr int NX = XBYTES / 1024 / kMWaves;  // x loads per wave and stage
-  static constexpr int NL = NX + 2;                   // loads per wave and stage
+  static constexpr int NX = XBYTES / 1024 / NW;       // x loads per wave and stage
+  static constexpr int NC = CBYTES / 1024 / NW;       // code loads per wave and stage
+  static constexpr int NA = NW == 8 ? 1 : 2;          // ratio / bias loads per wave
+  static constexpr int NL = NX + NC + NA;             // loads per wave and stage
   static constexpr int LDS = kRing * STAGE;
-  static constexpr int MI = TM / 32;                  // 16-row MFMA blocks per wave
-  static_assert(CBYTES / 1024 == kMWaves, "one code load per wave");
-  static_assert(LDS <= 160 * 1024, "LDS budget");
+  static_assert(NW == 8 || (NW == 4 && TM == 128), "layouts built");
+  static_assert(XBYTES % (1024 * NW) == 0 && CBYTES % (1024 * NW) == 0, "whole loads");
+  static_assert(LDS <= (NW == 8 ? 160 : 80) * 1024, "LDS budget");
   static_assert(NL <= MI, "one load per MFMA row block of the first K-chunk");
   static_assert(TM % 64 == 0 && TM <= kTM, "bias loads of 64 rows per wave");
 };
@@ -457,7 +467,7 @@ __device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint32_t w0, uint32_t w1) {
 constexpr int kTopKMax = 64;
 
 __device__ __forceinline__ bool tk_better(float av, int ai, float bv, int bi) {
-  return av > bv || (av == bv && ai < bi);
+  return (av > bv) | ((av == bv) & (ai < bi));   // non-short-circuit: no branches
 }
 
 __device__ __forceinline__ float rlane_f(float v, int l) {
@@ -470,10 +480,11 @@ __device__ __forceinline__ float rlane_f(float v, int l) {
 // is refreshed.
 __device__ __forceinline__ void tk_insert(float& lv, int& li, float& bv, int& bi, float cv,
                                           int ci, int lane, int k) {
-  const float pv = __shfl_up(lv, 1, 64);
-  const int pi = __shfl_up(li, 1, 64);
-  const bool here = lane < k && tk_better(cv, ci, lv, li);
-  const bool above = lane > 0 && tk_better(cv, ci, pv, pi);
+  // the previous lane's entry: DPP wave_shr:1 (a VALU move, no LDS trip)
+  const int pi = __builtin_amdgcn_update_dpp(0, li, 0x138, 0xF, 0xF, true);
+  const float pv = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(lv), 0x138, 0xF, 0xF, true));
+  const bool here = (lane < k) & tk_better(cv, ci, lv, li);
+  const bool above = (lane > 0) & tk_better(cv, ci, pv, pi);
   lv = here ? (above ? pv : cv) : lv;
   li = here ? (above ? pi : ci) : li;
   bv = rlane_f(lv, k - 1);
@@ -484,7 +495,7 @@ __device__ __forceinline__ void tk_insert(float& lv, int& li, float& bv, int& bi
 // enter one at a time, in lane order.
 __device__ __forceinline__ void tk_offer(float& lv, int& li, float& bv, int& bi, float v, int i,
                                          bool ok, int lane, int k) {
-  uint64_t m = __ballot(ok && tk_better(v, i, bv, bi));
+  uint64_t m = __ballot(ok & tk_better(v, i, bv, bi));
   while (m) {
     const int s = __builtin_ctzll(m);
     m &= m - 1;

@@ -56,11 +56,13 @@ struct MfmaArgs {
   float* tgt_logit;        // [M]
 };
 
-template <bool CE, int TM>
-__global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
-  using G = MGeomT<TM>;
+// (two waves per SIMD in both layouts: NW = 4 runs two workgroups per CU)
+template <bool CE, int TM, int NW>
+__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+void k_mfma(MfmaArgs a) {
+  using G = MGeomT<TM, NW>;
   constexpr int MI = G::MI;        // row blocks per wave
-  constexpr int WM = TM / 2;       // token rows per wave
+  constexpr int WM = G::WM;        // token rows per wave
   extern __shared__ __align__(16) uint8_t mfma_lds[];
   lds_u8* const L = (lds_u8*)mfma_lds;
 
@@ -83,7 +85,7 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wid >> 2, wn = wid & 3;
+  const int wm = NW == 8 ? wid >> 2 : 0, wn = wid & 3;
   const int lr = lane & 15, q = lane >> 4;
   const uint32_t kMask = opaque_vgpr(0x000F000Fu);
   const uint32_t kMagic = opaque_vgpr(0x43004300u);
@@ -106,20 +108,20 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
   const __amdgpu_buffer_rsrc_t ru = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<int8_t*>(a.ucodes + v0 * int64_t(urow)), 0, int(uint32_t(cols) * urow),
       kBufferWord3);
-  // auxiliary load of this wave: scale ratios (waves 0-3, 64 columns each)
-  // or slot biases (waves 4-7, 64 token rows each)
+  // auxiliary loads of this wave: the scale ratios of 64 columns and / or
+  // the slot biases of 64 token rows (NW = 8: waves 0-3 the ratios, 4-7 the
+  // biases; NW = 4: every wave both)
   // (the biases are laid out per 256 tokens, [slot][256]; a tile of TM < 256
   // rows starts inside such a block; waves past the tile's rows repeat the
   // loads of the waves before them into the same LDS words, so every wave
   // issues the same number of loads per stage)
-  const bool arat = wid < 4;
-  const int bw = (wid - 4) % (TM / 64);
+  const bool arat = NW == 4 || wid < 4;
+  const int bw = (NW == 8 ? wid - 4 : wid) % (TM / 64);
   const int64_t gb_off = (m0 / kTM) * a.nslot * kTM + m0 % kTM;
-  const __amdgpu_buffer_rsrc_t raux =
-      arat ? __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.ratio + vt * a.nslot * kTN),
-                                               0, a.nslot * kTN * 4, kBufferWord3)
-           : __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.gbias + gb_off), 0,
-                                               int(a.nslot * kTM - m0 % kTM) * 4, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rrat = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.ratio + vt * a.nslot * kTN), 0, a.nslot * kTN * 4, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rbias = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(a.gbias + gb_off), 0, int(a.nslot * kTM - m0 % kTM) * 4, kBufferWord3);
 
   // per-lane load offsets (row and swizzled 16-byte unit) of the residual
   // stages; the expansion stages use the same units with their own row
@@ -129,60 +131,56 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
     const int r = off / (2 * kKS), p = (off % (2 * kKS)) / 16;
     return uint32_t(r < rows ? r : rows - 1) * stride + 16u * uint32_t(p ^ swz_x(r));
   };
-  auto cunit = [&](uint32_t stride) {
-    const int off = wid * 1024 + 16 * lane;
+  auto cunit = [&](int ci, uint32_t stride) {
+    const int off = (wid * G::NC + ci) * 1024 + 16 * lane;
     const int c = off / (kKS / 2), p = (off % (kKS / 2)) / 16;
     return uint32_t(c < cols ? c : cols - 1) * stride + 16u * uint32_t(p ^ swz_c(c));
   };
   uint32_t xo[G::NX];
 #pragma unroll
   for (int i = 0; i < G::NX; ++i) xo[i] = xunit(i, ldx2);
-  const uint32_t co = cunit(rowbytes);
-  uint32_t ao;
-  int adst;
-  if (arat) {
-    ao = uint32_t(wid * 64 + lane) * 4;
-    adst = G::RAT + wid * 256;
-  } else {
-    const int r = bw * 64 + lane;
-    ao = uint32_t(r < rows ? r : rows - 1) * 4;
-    adst = G::BIAS + bw * 256;
-  }
+  uint32_t co[G::NC];
+#pragma unroll
+  for (int ci = 0; ci < G::NC; ++ci) co[ci] = cunit(ci, rowbytes);
+  const uint32_t ao_rat = uint32_t((wid & 3) * 64 + lane) * 4;
+  const uint32_t ao_bias = uint32_t(bw * 64 + lane < rows ? bw * 64 + lane : rows - 1) * 4;
 
   const int nst = a.d / kKS, spg = a.g / kKS, ntot = nst + a.nch;
   const int slot_u = ngrp, slot_a = ngrp + (a.nch_u > 0 ? 1 : 0);
   auto slot_of = [&](int s) {
     return s < nst ? s / spg : (s - nst < a.nch_u ? slot_u : slot_a);
   };
-  // load PART (0 .. NL-1) of this wave's share of stage s into ring slot buf
-  auto issue_part = [&](int s, int buf, int part) {
+  // load PART (0 .. NL-1) of this wave's share of stage s into ring slot
+  // buf: x (or t) units, code units, then the ratio / bias units.  KIND: 1
+  // a residual stage, 2 an expansion stage, 3 either (checked).
+  auto issue_part = [&](int s, int buf, int part, auto kind) {
+    constexpr int KIND = decltype(kind)::value;
     lds_u8* base = L + buf * G::STAGE;
+    const bool res = KIND == 1 || (KIND == 3 && s < nst);
     if (part < G::NX) {
-      if (s < nst) dma16(rx, base + (wid * G::NX + part) * 1024, xo[part] + uint32_t(s) * (kKS * 2));
-      else dma16(rt, base + (wid * G::NX + part) * 1024, xunit(part, trow) + uint32_t(s - nst) * 128);
-    } else if (part == G::NX) {
-      if (s < nst) dma16(rc, base + G::XBYTES + wid * 1024, co + uint32_t(s) * (kKS / 2));
-      else dma16(ru, base + G::XBYTES + wid * 1024, cunit(urow) + uint32_t(s - nst) * 32);
+      lds_u8* dst = base + (wid * G::NX + part) * 1024;
+      if (res) dma16(rx, dst, xo[part] + uint32_t(s) * (kKS * 2));
+      else dma16(rt, dst, xunit(part, trow) + uint32_t(s - nst) * 128);
+    } else if (part < G::NX + G::NC) {
+      const int ci = part - G::NX;
+      lds_u8* dst = base + G::XBYTES + (wid * G::NC + ci) * 1024;
+      if (res) dma16(rc, dst, co[ci] + uint32_t(s) * (kKS / 2));
+      else dma16(ru, dst, cunit(ci, urow) + uint32_t(s - nst) * 32);
     } else {
-      dma4(raux, base + adst, ao + uint32_t(slot_of(s)) * 1024u);
+      const uint32_t k = uint32_t(KIND == 1 ? s / spg : slot_of(s)) * 1024u;
+      if (NW == 4 ? part == G::NX + G::NC : arat)
+        dma4(rrat, base + G::RAT + (wid & 3) * 256, ao_rat + k);
+      else
+        dma4(rbias, base + G::BIAS + bw * 256, ao_bias + k);
     }
   };
+  using kMain = std::integral_constant<int, 1>;
+  using kExp = std::integral_constant<int, 2>;
+  using kAny = std::integral_constant<int, 3>;
+  using kNone = std::integral_constant<int, 0>;
   auto issue = [&](int s, int buf) {
 #pragma unroll
-    for (int part = 0; part < G::NL; ++part) issue_part(s, buf, part);
-  };
-  // the same for a stage known to be a residual / an expansion stage
-  auto issue_main = [&](int s, int buf, int part) {
-    lds_u8* base = L + buf * G::STAGE;
-    if (part < G::NX) dma16(rx, base + (wid * G::NX + part) * 1024, xo[part] + uint32_t(s) * (kKS * 2));
-    else if (part == G::NX) dma16(rc, base + G::XBYTES + wid * 1024, co + uint32_t(s) * (kKS / 2));
-    else dma4(raux, base + adst, ao + uint32_t(s / spg) * 1024u);
-  };
-  auto issue_exp = [&](int s, int buf, int part) {
-    lds_u8* base = L + buf * G::STAGE;
-    if (part < G::NX) dma16(rt, base + (wid * G::NX + part) * 1024, xunit(part, trow) + uint32_t(s - nst) * 128);
-    else if (part == G::NX) dma16(ru, base + G::XBYTES + wid * 1024, cunit(urow) + uint32_t(s - nst) * 32);
-    else dma4(raux, base + adst, ao + uint32_t(slot_of(s)) * 1024u);
+    for (int part = 0; part < G::NL; ++part) issue_part(s, buf, part, kAny{});
   };
 
   // fragment offsets within a stage: residual stages take x chunks 2q + kc,
@@ -264,8 +262,8 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Am, B[ni], acc[mi][ni], 0, 0, 0);
         if (kc == 0 && mi < G::NL) {
-          if constexpr (ISSUE == 1) issue_main(s + 2, nb, mi);
-          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi);
+          if constexpr (ISSUE == 1) issue_part(s + 2, nb, mi, kMain{});
+          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi, kAny{});
         }
       }
     }
@@ -292,16 +290,12 @@ __global__ __launch_bounds__(kMBlock) void k_mfma(MfmaArgs a) {
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
         if (kc == 0 && mi < G::NL) {
-          if constexpr (ISSUE == 2) issue_exp(s + 2, nb, mi);
-          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi);
+          if constexpr (ISSUE == 2) issue_part(s + 2, nb, mi, kExp{});
+          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi, kAny{});
         }
       }
     }
   };
-  using kNone = std::integral_constant<int, 0>;
-  using kMain = std::integral_constant<int, 1>;
-  using kExp = std::integral_constant<int, 2>;
-  using kAny = std::integral_constant<int, 3>;
   int s = 0;
 #pragma unroll 1
   for (; s + 2 < nst; ++s) main_stage(s, kMain{});

@@ -35,7 +35,7 @@ namespace archead {
 constexpr int64_t kDefaultGemvMaxM = 15;  // largest M on the decode kernel (measured crossover)
 constexpr int64_t kDefaultDecMinM = 3;    // M range of the MFMA decode kernel (one or
 constexpr int64_t kDefaultDecMaxM = 32;   // two tokens stream faster through the GEMV)
-constexpr int64_t kDefaultMidMaxM = 64;   // largest M of the several-token kernel
+constexpr int64_t kDefaultMidMaxM = 32;   // largest M of the several-token kernel (one pass)
 constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
 constexpr int kDecTok = 16;               // tokens per pass of the MFMA decode kernel
 constexpr int kDecWaves = 8;              // waves per workgroup of the MFMA decode kernel

@@ -232,12 +232,15 @@ __global__ __launch_bounds__(kBlock) void k_stage1m_fin(Stage1MArgs a) {
 namespace archead {
 namespace kern {
 
-const void* mfma(bool ce, int tm) {
+const void* mfma(bool ce, int tm, int nw) {
+  if (tm == 128 && nw == 4)
+    return ce ? reinterpret_cast<const void*>(k_mfma<true, 128, 4>)
+              : reinterpret_cast<const void*>(k_mfma<false, 128, 4>);
   if (tm == 128)
-    return ce ? reinterpret_cast<const void*>(k_mfma<true, 128>)
-              : reinterpret_cast<const void*>(k_mfma<false, 128>);
-  return ce ? reinterpret_cast<const void*>(k_mfma<true, kTM>)
-            : reinterpret_cast<const void*>(k_mfma<false, kTM>);
+    return ce ? reinterpret_cast<const void*>(k_mfma<true, 128, 8>)
+              : reinterpret_cast<const void*>(k_mfma<false, 128, 8>);
+  return ce ? reinterpret_cast<const void*>(k_mfma<true, kTM, 8>)
+            : reinterpret_cast<const void*>(k_mfma<false, kTM, 8>);
 }
 const void* prep() { return reinterpret_cast<const void*>(k_prep); }
 const void* stage1m() { return reinterpret_cast<const void*>(k_stage1m); }

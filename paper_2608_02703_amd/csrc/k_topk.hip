@@ -37,10 +37,36 @@ const void* gemv_topk_fn(int lpr, bool sc8) {
   return reinterpret_cast<const void*>(fn);
 }
 
+// Offer entries j in [lo, hi) of one wave's share of a flat array of
+// candidates (value val(j), index idx(j)) to the wave's list: 64 per step,
+// wave w of the workgroup taking steps lo + 64 w, lo + 64 (w + kWaves), ...;
+// kScanBatch steps' loads are issued together before any is offered, so a
+// scan costs one memory latency per batch, not per step.  Candidates ranked
+// below the floor (fv, fi) are not offered.
+constexpr int kScanBatch = 8;
+template <typename Val, typename Idx>
+__device__ __forceinline__ void tk_scan(int64_t lo, int64_t hi, Val val, Idx idx, int lane, int wid,
+                                        int k, float& lv, int& li, float& bv, int& bi,
+                                        float fv = -INFINITY, int fi = kNoIdx) {
+  for (int64_t b = lo + int64_t(wid) * 64; b < hi; b += int64_t(kScanBatch) * kBlock) {
+    float cv[kScanBatch];
+    int ci[kScanBatch];
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u) {
+      const int64_t j = b + int64_t(u) * kBlock + lane;
+      cv[u] = j < hi ? val(j) : -INFINITY;
+      ci[u] = j < hi ? idx(j) : kNoIdx;
+    }
+#pragma unroll
+    for (int u = 0; u < kScanBatch; ++u)
+      tk_offer(lv, li, bv, bi, cv[u], ci[u],
+               (b + int64_t(u) * kBlock + lane < hi) & !tk_better(fv, fi, cv[u], ci[u]), lane, k);
+  }
+}
+
 // Per (partial p, token m) of grid (n_part, M): the k best pairs of
 // logits[m, v] over the slice v in [p * slice, min(V, (p + 1) * slice)),
-// into pv / pi [M][n_part][k].  Each wave reads 64 consecutive logits per
-// step (coalesced), offers them to its list, and the four lists are merged.
+// into pv / pi [M][n_part][k]; the workgroup's four lists are merged.
 __global__ __launch_bounds__(kBlock) void k_topk_rows(const float* logits, int64_t ldl, int64_t V,
                                                       int k, int64_t slice, float* pv, int* pi) {
   __shared__ float sv[kWaves * 64];
@@ -53,12 +79,8 @@ __global__ __launch_bounds__(kBlock) void k_topk_rows(const float* logits, int64
   const float* row = logits + m * ldl;
   float lv = -INFINITY, bv = -INFINITY;
   int li = kNoIdx, bi = kNoIdx;
-  for (int64_t b = lo + wid * 64; b < hi; b += kBlock) {
-    const int64_t v = b + lane;
-    const bool ok = v < hi;
-    const float x = ok ? row[v] : -INFINITY;
-    tk_offer(lv, li, bv, bi, x, int(v), ok, lane, k);
-  }
+  tk_scan(lo, hi, [&](int64_t j) { return row[j]; }, [&](int64_t j) { return int(j); }, lane, wid,
+          k, lv, li, bv, bi);
   tk_block_merge<kWaves>(lv, li, bv, bi, lane, wid, k, sv, si);
   if (wid == 0 && lane < k) {
     const int64_t o = (m * n_part + p) * k + lane;
@@ -67,9 +89,10 @@ __global__ __launch_bounds__(kBlock) void k_topk_rows(const float* logits, int64
   }
 }
 
-// Per token m (grid M): the k best of its n_part partial lists of k pairs,
-// out to vals[m * ldk + j] (may be null) and idx[m * ldk + j], j < k; a slot
-// no value reached (fewer than k non-NaN logits) gets (-inf, -1).
+// Per token m (grid M): the k best of its n_part partial lists of k pairs
+// (scanned as one flat array of n_part * k candidates), out to
+// vals[m * ldk + j] (may be null) and idx[m * ldk + j], j < k; a slot no
+// value reached (fewer than k non-NaN logits) gets (-inf, -1).
 __global__ __launch_bounds__(kBlock) void k_topk_merge(const float* pv, const int* pi,
                                                        int64_t n_part, int k, float* vals,
                                                        int64_t* idx, int64_t ldk) {
@@ -78,15 +101,34 @@ __global__ __launch_bounds__(kBlock) void k_topk_merge(const float* pv, const in
   const int lane = threadIdx.x & 63;
   const int wid = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int64_t m = blockIdx.x;
+  const float* v = pv + m * n_part * k;
+  const int* ix = pi + m * n_part * k;
+  // a floor for the result's k-th entry: each list holds k entries ranked at
+  // or above its own k-th, so the best of the lists' k-th entries is ranked
+  // at or below the final k-th; candidates ranked below it are skipped
+  float fv = -INFINITY;
+  int fi = kNoIdx;
+  for (int64_t p = threadIdx.x; p < n_part; p += kBlock) {
+    const float c = v[p * k + k - 1];
+    const int ci = ix[p * k + k - 1];
+    if (tk_better(c, ci, fv, fi)) { fv = c; fi = ci; }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) {
+    const float ov = __shfl_xor(fv, off, 64);
+    const int oi = __shfl_xor(fi, off, 64);
+    if (tk_better(ov, oi, fv, fi)) { fv = ov; fi = oi; }
+  }
+  if (lane == 0) { sv[wid] = fv; si[wid] = fi; }
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w)
+    if (tk_better(sv[w], si[w], fv, fi)) { fv = sv[w]; fi = si[w]; }
+  __syncthreads();
   float lv = -INFINITY, bv = -INFINITY;
   int li = kNoIdx, bi = kNoIdx;
-  for (int64_t p = wid; p < n_part; p += kWaves) {
-    const bool ok = lane < k;
-    const int64_t o = (m * n_part + p) * k + lane;
-    const float x = ok ? pv[o] : -INFINITY;
-    const int i = ok ? pi[o] : kNoIdx;
-    tk_offer(lv, li, bv, bi, x, i, ok, lane, k);
-  }
+  tk_scan(0, n_part * k, [&](int64_t j) { return v[j]; }, [&](int64_t j) { return ix[j]; }, lane,
+          wid, k, lv, li, bv, bi, fv, fi);
   tk_block_merge<kWaves>(lv, li, bv, bi, lane, wid, k, sv, si);
   if (wid == 0 && lane < k) {
     if (vals) vals[m * ldk + lane] = lv;

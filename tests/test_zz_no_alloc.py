@@ -31,7 +31,7 @@ def _same_bits(a, b):
 
 
 @pytest.mark.parametrize("cfg,Ms", [("tiny", (8, 3)), ("qwen_decode", (16, 1)),
-                                    ("qwen_decode", (40, 4))])
+                                    ("qwen_decode", (32, 4))])
 def test_noalloc_matches_workspace_call(cfg, Ms):
     from paper_2608_02703_amd import PackedHead
     h = make_head(cfg)
