@@ -20,7 +20,8 @@ to their sustained-load state (--clock-warmup; a cold GPU runs the first
 and times exactly --steps steps.
 
 Prints one JSON line (rank 0, N=1).  --gpus N > 1 is refused: the
-benchmark runs on one GPU.  --profile decode|prefill runs the same work without timing
+benchmark runs on one GPU.  --profile decode|prefill|topk (the M=1 top-10
+selection) runs the same work without timing
 or JSON, for rocprofv3 (the decode form first copies 256 MiB once, the
 calibration kernel for the HBM byte counters).
 """
@@ -407,7 +408,15 @@ def profile_run(kind, steps):
     h = make_head("qwen_decode")
     heads = upload_copies(h, N_COPIES)
     x1 = torch.from_numpy(make_x("qwen_decode", 1).view(np.int16)).view(torch.bfloat16).cuda()
-    if kind == "decode":
+    if kind == "topk":
+        clock_warmup(heads, x1, 0.5)
+        wss = [hd.workspace(1, 3, x1.device) for hd in heads]
+        vals = torch.empty((1, 10), dtype=torch.float32, device="cuda")
+        idx = torch.empty((1, 10), dtype=torch.int64, device="cuda")
+        for i in range(5 + steps):
+            k = i % len(heads)
+            heads[k].logits_topk(x1, 10, vals=vals, idx=idx, ws=wss[k])
+    elif kind == "decode":
         src = torch.empty(CALIBRATION_BYTES, dtype=torch.uint8, device="cuda").fill_(3)
         dst = torch.empty_like(src)
         dst.copy_(src)
@@ -512,7 +521,7 @@ def main():
                          "r_c=10, r_r=6, g=64, 8-bit scale codes)")
     ap.add_argument("--no-dense", action="store_true",
                     help="skip the dense bf16 head context line")
-    ap.add_argument("--profile", choices=["decode", "prefill"])
+    ap.add_argument("--profile", choices=["decode", "prefill", "topk"])
     ap.add_argument("--sweep", action="store_true",
                     help="M sweep of a head (default the 128k-vocabulary one) through each kernel")
     ap.add_argument("--sweep-cfg", default="sweep128k",
@@ -540,7 +549,7 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     if args.profile:
-        profile_run(args.profile, args.steps if args.profile == "decode" else args.prefill_steps)
+        profile_run(args.profile, args.prefill_steps if args.profile == "prefill" else args.steps)
         return
     if args.sweep:
         sweep(min(args.steps, 40), args.sweep_cfg,
@@ -676,7 +685,8 @@ def main():
         tflops = flops / (kern_p * 1e-3) / 1e12
         prefill = {"M": Mp, "ms_per_step": round(ms_p, 4), "tok_s": round(Mp / ms_p * 1e3, 1),
                    "mean_ce": mean_ce,
-                   "mfma_kernel": {"kernel": "k_mfma<true>", "kernel_ms_median": round(kern_p, 4),
+                   "mfma_kernel": {"kernel": "k_mfma<true, 256, 8>",
+                                   "kernel_ms_median": round(kern_p, 4),
                                    "algorithmic_flops": flops,
                                    "achieved_tflops": round(tflops, 1),
                                    "peak_tflops": PEAK_BF16_TFLOPS,
@@ -692,13 +702,30 @@ def main():
         log(f"prefill CE M={Mp}: {ms_p:.3f} ms/step, {Mp / ms_p * 1e3:.0f} tok/s; "
             f"many-token kernel {kern_p:.3f} ms = {tflops:.0f} TFLOP/s "
             f"({100 * tflops / PEAK_BF16_TFLOPS:.1f}% of bf16 peak)")
+        if not args.no_dense:
+            # context: the logits of the same tokens through a dense bf16 head
+            # of the same shape (hipBLASLt through torch, random weights; the
+            # [M, V] logits are written, no softmax)
+            import torch.nn.functional as F
+            w = torch.randn((h.V, h.d), device="cuda", dtype=torch.bfloat16)
+            for _ in range(2):
+                F.linear(xp, w)
+            dms = _timed_loop(lambda i: F.linear(xp, w), max(3, args.prefill_steps // 2))
+            dfl = 2 * Mp * h.V * h.d
+            prefill["dense_bf16_linear"] = {
+                "ms_per_step": round(dms, 4), "tflops": round(dfl / dms / 1e9, 1),
+                "frac": round(dfl / dms / 1e9 / PEAK_BF16_TFLOPS, 4),
+                "op": "torch.nn.functional.linear, bf16 [M, d] x [V, d]^T, M=4096"}
+            log(f"dense bf16 linear M={Mp}: {dms:.3f} ms/step = {dfl / dms / 1e9:.0f} TFLOP/s")
+            del w
+            torch.cuda.empty_cache()
 
     copy = copy_bandwidth()
     log(f"device copy: {copy['gbs_read_plus_write']} GB/s (read + write)")
     ms1, kern1_mean, kern1 = res[1]
     value = pbytes / ms1 / 1e6          # GB/s
     alg = decode_algorithmic_bytes(pbytes, h, 1)
-    kname = f"k_gemv<1,{lanes_per_row(h)},false,false>"
+    kname = f"k_gemv<1, {lanes_per_row(h)}, false, false, 0, false>"
     achieved = alg / kern1 / 1e6
     out = {
         "metric": METRIC,
