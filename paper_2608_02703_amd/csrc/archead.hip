@@ -735,20 +735,27 @@ archead_status launch_mid(const archead_handle* h, const void* x, int64_t M, int
 int tiled_tm(int64_t M) { return M <= 128 ? 128 : kTM; }
 
 // Tile rows and waves per workgroup of the tiled kernel for a call of M
-// tokens: 128-row tiles of 4 waves, two workgroups per CU, up to
-// kTiledNw4MaxM tokens (measured 10-25% faster than one workgroup of 8
+// tokens: 64-row tiles of 4 waves, three workgroups per CU, up to
+// kTiled64MaxM tokens; 128-row tiles of 4 waves, two workgroups per CU, up
+// to kTiledNw4MaxM tokens (measured 10-25% faster than one workgroup of 8
 // waves per CU at M = 16 .. 1024, where tile starts, LDS waits and the
 // epilogue would leave the matrix unit idle); above, 256-row tiles of 8
 // waves (equal at M = 4096, where the chip runs at its power limit).
-// ARCHEAD_MFMA_NW = 4 or 8 overrides the choice (tuning only).
+// ARCHEAD_MFMA_NW = 4 or 8 and ARCHEAD_MFMA_TM override the choice (tuning
+// only).
+constexpr int64_t kTiled64MaxM = 64;
 constexpr int64_t kTiledNw4MaxM = 1024;
 struct TiledShape { int tm, nw; };
 TiledShape tiled_shape(int64_t M) {
-  TiledShape t = M <= kTiledNw4MaxM ? TiledShape{128, 4} : TiledShape{kTM, 8};
+  TiledShape t = M <= kTiled64MaxM    ? TiledShape{64, 4}
+                 : M <= kTiledNw4MaxM ? TiledShape{128, 4}
+                                      : TiledShape{kTM, 8};
   if (const char* e = getenv("ARCHEAD_MFMA_NW")) {
     if (atoi(e) == 4) t = TiledShape{128, 4};
     else if (atoi(e) == 8) t = TiledShape{tiled_tm(M), 8};
   }
+  if (const char* e = getenv("ARCHEAD_MFMA_TM"))
+    if (t.nw == 4 && (atoi(e) == 64 || atoi(e) == 128)) t.tm = atoi(e);
   return t;
 }
 
@@ -786,7 +793,8 @@ archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStr
     return fail(ARCHEAD_E_UNSUPPORTED, "ldx too large for the many-token kernel");
   const TiledShape ts = tiled_shape(a.M);
   const void* fn = kern::mfma(ce, ts.tm, ts.nw);
-  const int lds = ts.nw == 4 ? MGeomT<128, 4>::LDS : ts.tm == 128 ? MGeomT<128>::LDS : MGeom::LDS;
+  const int lds = ts.nw == 4 ? (ts.tm == 64 ? MGeomT<64, 4>::LDS : MGeomT<128, 4>::LDS)
+                  : ts.tm == 128 ? MGeomT<128>::LDS : MGeom::LDS;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
   if (e != hipSuccess) return hip_fail(e, "MFMA LDS size attribute");
   hipEvent_t ev0 = static_cast<hipEvent_t>(h->ev_start.load(std::memory_order_relaxed));

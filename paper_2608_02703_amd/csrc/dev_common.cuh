@@ -353,9 +353,9 @@ constexpr int kExpDims = 16;                 // rank dimensions per expansion st
 
 // Geometry of the tiled kernel for TM token rows per tile and NW waves per
 // workgroup: NW = 8 (2 x 4 waves of TM/2 x 64; one workgroup per CU) or
-// NW = 4 (1 x 4 waves of TM x 64, TM = 128; two workgroups per CU, whose
-// stage barriers are independent, so one's LDS waits, tile start and
-// epilogue overlap the other's MFMAs).  A stage holds x [TM][kKS] bf16,
+// NW = 4 (1 x 4 waves of TM x 64; TM = 128: two workgroups per CU, TM = 64:
+// three), whose stage barriers are independent, so one's LDS waits, tile
+// start and epilogue overlap the others' MFMAs.  A stage holds x [TM][kKS] bf16,
 // codes [kTN][kKS/2], the scale ratios of the kTN columns and the slot
 // biases of the TM rows.
 template <int TM, int NW = kMWaves>
@@ -373,10 +373,11 @@ struct MGeomT {
   static constexpr int NA = NW == 8 ? 1 : 2;          // ratio / bias loads per wave
   static constexpr int NL = NX + NC + NA;             // loads per wave and stage
   static constexpr int LDS = kRing * STAGE;
-  static_assert(NW == 8 || (NW == 4 && TM == 128), "layouts built");
+  static constexpr int WGS = NW == 8 ? 1 : (TM == 128 ? 2 : 3);   // workgroups per CU
+  static_assert(NW == 8 || (NW == 4 && (TM == 128 || TM == 64)), "layouts built");
   static_assert(XBYTES % (1024 * NW) == 0 && CBYTES % (1024 * NW) == 0, "whole loads");
-  static_assert(LDS <= (NW == 8 ? 160 : 80) * 1024, "LDS budget");
-  static_assert(NL <= MI, "one load per MFMA row block of the first K-chunk");
+  static_assert(LDS * WGS <= 160 * 1024, "LDS budget");
+  static_assert(NL <= 2 * MI, "one load per MFMA row block of the stage");
   static_assert(TM % 64 == 0 && TM <= kTM, "bias loads of 64 rows per wave");
 };
 using MGeom = MGeomT<kTM>;

@@ -56,9 +56,11 @@ struct MfmaArgs {
   float* tgt_logit;        // [M]
 };
 
-// (two waves per SIMD in both layouts: NW = 4 runs two workgroups per CU)
+// (waves per SIMD: 2 with 8-wave workgroups and with 128-row tiles of 4
+// waves, two workgroups per CU; 3 with 64-row tiles, three per CU)
 template <bool CE, int TM, int NW>
-__global__ __launch_bounds__(NW * 64) __attribute__((amdgpu_waves_per_eu(2)))
+__global__ __launch_bounds__(NW * 64)
+__attribute__((amdgpu_waves_per_eu(MGeomT<TM, NW>::WGS * NW / 4 > 2 ? MGeomT<TM, NW>::WGS * NW / 4 : 2)))
 void k_mfma(MfmaArgs a) {
   using G = MGeomT<TM, NW>;
   constexpr int MI = G::MI;        // row blocks per wave
@@ -211,8 +213,9 @@ void k_mfma(MfmaArgs a) {
   issue(0, 0);
   if (ntot > 1) issue(1, 1);
   // The loads of stage s + 2 are issued one part at a time between the
-  // MFMAs of stage s's first K-chunk, so the waves' vector-memory traffic
-  // does not queue up in one burst after the barrier.
+  // MFMAs of stage s (one per row block of its first K-chunk, then of the
+  // second where a wave has more loads than row blocks), so the waves'
+  // vector-memory traffic does not queue up in one burst after the barrier.
   int buf = 0;   // ring slot of the next stage to compute
   auto next_stage = [&](int s) {
     if (s + 1 < ntot) wait_loads_barrier<G::NL>();
@@ -261,9 +264,9 @@ void k_mfma(MfmaArgs a) {
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Am, B[ni], acc[mi][ni], 0, 0, 0);
-        if (kc == 0 && mi < G::NL) {
-          if constexpr (ISSUE == 1) issue_part(s + 2, nb, mi, kMain{});
-          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi, kAny{});
+        if (kc * MI + mi < G::NL) {
+          if constexpr (ISSUE == 1) issue_part(s + 2, nb, kc * MI + mi, kMain{});
+          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, kc * MI + mi, kAny{});
         }
       }
     }
@@ -289,9 +292,9 @@ void k_mfma(MfmaArgs a) {
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
-        if (kc == 0 && mi < G::NL) {
-          if constexpr (ISSUE == 2) issue_part(s + 2, nb, mi, kExp{});
-          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, mi, kAny{});
+        if (kc * MI + mi < G::NL) {
+          if constexpr (ISSUE == 2) issue_part(s + 2, nb, kc * MI + mi, kExp{});
+          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, kc * MI + mi, kAny{});
         }
       }
     }

@@ -233,6 +233,9 @@ namespace archead {
 namespace kern {
 
 const void* mfma(bool ce, int tm, int nw) {
+  if (tm == 64 && nw == 4)
+    return ce ? reinterpret_cast<const void*>(k_mfma<true, 64, 4>)
+              : reinterpret_cast<const void*>(k_mfma<false, 64, 4>);
   if (tm == 128 && nw == 4)
     return ce ? reinterpret_cast<const void*>(k_mfma<true, 128, 4>)
               : reinterpret_cast<const void*>(k_mfma<false, 128, 4>);

@@ -24,8 +24,8 @@ const void* dec(int gw, bool ce, int ek, bool sc8, int gen);
 // several-token kernel k_mid: gw = g / 32 (2 or 4), gen as for dec
 const void* mid(int gw, bool ce, bool sc8, int gen);
 // tiled many-token kernel k_mfma<CE, TM, NW> (tm = 256 or 128 token rows
-// per tile, nw = 8 waves per workgroup, or 4 with tm = 128) and its
-// prologue kernels
+// per tile with nw = 8 waves per workgroup, or tm = 128 or 64 with nw = 4)
+// and its prologue kernels
 const void* mfma(bool ce, int tm, int nw);
 const void* prep();
 const void* stage1m();
