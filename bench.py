@@ -717,7 +717,23 @@ def main():
                 "frac": round(dfl / dms / 1e9 / PEAK_BF16_TFLOPS, 4),
                 "op": "torch.nn.functional.linear, bf16 [M, d] x [V, d]^T, M=4096"}
             log(f"dense bf16 linear M={Mp}: {dms:.3f} ms/step = {dfl / dms / 1e9:.0f} TFLOP/s")
-            del w
+            # the fidelity metrics against that dense head inside the packed
+            # head's tile pass (archead_logit_fidelity_head: fidelity pass,
+            # merge, rank pass; no [M, V] array)
+            hd0 = heads[0]
+            wsf = hd0.workspace(Mp, 4, xp.device)
+            for _ in range(2):
+                hd0.logit_fidelity_head(xp, w, ws=wsf)
+            fms = _timed_loop(lambda i: hd0.logit_fidelity_head(xp, w, ws=wsf),
+                              max(3, args.prefill_steps // 2))
+            kl, sqe, ridx, rk = hd0.logit_fidelity_head(xp, w, ws=wsf)
+            prefill["fidelity_head"] = {
+                "ms_per_step": round(fms, 4), "tok_s": round(Mp / fms * 1e3, 1),
+                "mean_kl_random_dense": float(kl.mean()),
+                "op": "archead_logit_fidelity_head vs the random dense bf16 head above, M=4096"}
+            log(f"fidelity vs a dense head in the tile pass M={Mp}: {fms:.3f} ms/step, "
+                f"{Mp / fms * 1e3:.0f} tok/s")
+            del w, wsf
             torch.cuda.empty_cache()
 
     copy = copy_bandwidth()

@@ -99,7 +99,8 @@ typedef enum archead_op {
   ARCHEAD_OP_LOGITS = 0,    /* archead_logits    */
   ARCHEAD_OP_LOGITS_CE = 1, /* archead_logits_ce */
   ARCHEAD_OP_ARGMAX = 2,    /* archead_logits_argmax */
-  ARCHEAD_OP_TOPK = 3       /* archead_logits_topk */
+  ARCHEAD_OP_TOPK = 3,      /* archead_logits_topk */
+  ARCHEAD_OP_FIDELITY = 4   /* archead_logit_fidelity_head */
 } archead_op;
 
 /* Shape and encoding of a packed head (the "integer shapes/groups" metadata
@@ -271,6 +272,36 @@ archead_status archead_logits_ce(const archead_handle* h, const void* x,
 archead_status archead_logits_argmax(const archead_handle* h, const void* x, int64_t M,
                                      int64_t ldx, int64_t* idx, float* max_logit, void* ws,
                                      size_t ws_bytes, void* stream);
+
+/* Logit fidelity of the packed head against a dense bf16 head on the same
+ * tokens, computed in the packed head's vocabulary-tile pass (Section 4,
+ * "Logit Fidelity", and Table 8: KL, top-k agreement and logit MSE of a
+ * compressed head against the dense one).  Per token m < M, with a = the
+ * dense head's logits x W_dense^T and b = the packed head's logits (those of
+ * archead_logits): kl[m] = KL(softmax(a) || softmax(b)), sq[m] = sum_v
+ * (a_v - b_v)^2 (the MSE of Table 8 is its mean over tokens), ref_idx[m] =
+ * the first v attaining max a, rank[m] = the number of v whose b is larger
+ * than b at ref_idx[m], or equal at a smaller index (so the dense top-1 is
+ * in the packed head's top k exactly when rank < k).  The tiled kernel
+ * streams the dense head's rows through the same stages as the packed
+ * codes and accumulates both products per tile (64 tokens x 256 rows); each
+ * tile leaves per-token statistics, a merge kernel combines them in tile
+ * order (fp64), and a second pass of the packed head counts the rank.  No
+ * [M, V] array is written.  The same quantities as archead_logit_fidelity,
+ * there from two logit arrays.
+ *   dense      bf16 [V, ldw] device, 16-byte aligned, ldw >= d, ldw % 8 == 0
+ *              (row v: the dense head's weights of vocabulary entry v)
+ *   kl, sq     device fp32 [M];  ref_idx, rank  device int64 [M]
+ *   ws         archead_workspace_bytes(h, M, ARCHEAD_OP_FIDELITY) bytes
+ * The dense head is read once per 64 tokens (4 bytes per weight per 128
+ * tokens); this is an evaluation pass.  ARCHEAD_E_UNSUPPORTED for heads
+ * without the tiled kernel (g % 64 != 0) or ldw * 512 >= 2^31; other errors
+ * as archead_logits. */
+archead_status archead_logit_fidelity_head(const archead_handle* h, const void* x, int64_t M,
+                                           int64_t ldx, const void* dense, int64_t ldw,
+                                           float* kl, float* sq, int64_t* ref_idx,
+                                           int64_t* rank, void* ws, size_t ws_bytes,
+                                           void* stream);
 
 /* Largest k of archead_logits_topk. */
 #define ARCHEAD_TOPK_MAX 64

@@ -159,6 +159,15 @@ def logits_factorized(h, x) -> np.ndarray:
     return out
 
 
+def dense_bf16_logits(w_bits: np.ndarray, x) -> np.ndarray:
+    """Logits of a dense bf16 head (the reference the paper's fidelity
+    metrics compare a compressed head against, Section 4 "Logit Fidelity"):
+    x [M, d] times W^T, W the bf16 bit patterns [V, d], every value converted
+    to fp64 exactly, one fp64 matrix product."""
+    w = bf16_to_f64(np.asarray(w_bits).view(np.uint16))
+    return _as_f64_x(x) @ w.T
+
+
 def cross_entropy(lg: np.ndarray, targets) -> np.ndarray:
     """Per-token CE [M] = logsumexp_v(lg[m, :]) - lg[m, y_m], natural log.
 

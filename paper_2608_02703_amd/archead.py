@@ -20,7 +20,7 @@ ABI_VERSION = 3
 OK, E_INVALID_ARG, E_MISALIGNED, E_UNSUPPORTED, E_WORKSPACE, E_HIP = range(6)
 F32, BF16, F16, I32, I64, I8, U8, I5 = range(8)
 INT4_V1 = 1
-OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX, OP_TOPK = 0, 1, 2, 3
+OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX, OP_TOPK, OP_FIDELITY = 0, 1, 2, 3, 4
 TOPK_MAX = 64
 NOALLOC_SCRATCH_BYTES = 4 << 20   # ARCHEAD_NOALLOC_SCRATCH_BYTES of include/archead.h
 
@@ -80,6 +80,13 @@ _SIGS = {
     "archead_logits_argmax": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]),
+    "archead_logit_fidelity_head": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p,
+                                                   ctypes.c_int64, ctypes.c_int64,
+                                                   ctypes.c_void_p, ctypes.c_int64,
+                                                   ctypes.c_void_p, ctypes.c_void_p,
+                                                   ctypes.c_void_p, ctypes.c_void_p,
+                                                   ctypes.c_void_p, ctypes.c_size_t,
+                                                   ctypes.c_void_p]),
     "archead_logits_topk": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64,
                                            ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
                                            ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
@@ -513,6 +520,27 @@ class PackedHead:
             self.handle, _ptr(x), M, x.stride(0), int(k), _ptr(vals), _ptr(idx), idx.stride(0),
             _ptr(ws), ws.numel(), self._stream(x.device)), self._lib)
         return vals, idx
+
+    def logit_fidelity_head(self, x, dense, ws=None):
+        """Fidelity of this head to a dense bf16 head [V, d] on the tokens x,
+        in the head's tile pass (archead_logit_fidelity_head): returns (kl
+        fp32 [M], sq fp32 [M], ref_idx int64 [M], rank int64 [M])."""
+        import torch
+        if x.dtype != torch.bfloat16 or x.dim() != 2 or x.stride(1) != 1:
+            raise ValueError("x must be a 2-D bf16 tensor with unit column stride")
+        if dense.dtype != torch.bfloat16 or dense.dim() != 2 or dense.stride(1) != 1:
+            raise ValueError("dense must be a 2-D bf16 tensor with unit column stride")
+        M = x.shape[0]
+        kl = torch.empty(M, dtype=torch.float32, device=x.device)
+        sq = torch.empty(M, dtype=torch.float32, device=x.device)
+        ref_idx = torch.empty(M, dtype=torch.int64, device=x.device)
+        rank = torch.empty(M, dtype=torch.int64, device=x.device)
+        ws = self.workspace(M, OP_FIDELITY, x.device) if ws is None else ws
+        _check(self._lib.archead_logit_fidelity_head(
+            self.handle, _ptr(x), M, x.stride(0), _ptr(dense), dense.stride(0), _ptr(kl),
+            _ptr(sq), _ptr(ref_idx), _ptr(rank), _ptr(ws), ws.numel(), self._stream(x.device)),
+            self._lib)
+        return kl, sq, ref_idx, rank
 
     def logits_ce(self, x, targets, ce=None, mean=None, ws=None):
         """Fused log-softmax + cross-entropy; returns (ce [M], mean [1])."""

@@ -348,6 +348,14 @@ static WsLayout topk_layout(const archead_handle* h, int64_t M) {
 
 WsLayout ws_layout(const archead_handle* h, int64_t M, archead_op op) {
   if (h && M > 0 && op == ARCHEAD_OP_TOPK) return topk_layout(h, M);
+  if (h && M > 0 && op == ARCHEAD_OP_FIDELITY) {
+    WsLayout w = ws_layout_path(h, M, ARCHEAD_OP_LOGITS, Path::kTiled);
+    const size_t n_vt = size_t((h->desc.V + kTN - 1) / kTN);
+    w.fid_off = w.total;
+    w.bref_off = align256(w.fid_off + 32 * size_t(M) * n_vt);
+    w.total = align256(w.bref_off + sizeof(float) * size_t(M));
+    return w;
+  }
   return ws_layout_path(h, M, op, h ? choose_path(h, M) : Path::kGemv);
 }
 
@@ -1076,6 +1084,63 @@ archead_status archead_logits_argmax(const archead_handle* h, const void* x, int
                      w.n_part, idx, max_logit);
   hipError_t e = hipGetLastError();
   return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "argmax merge launch");
+}
+
+archead_status archead_logit_fidelity_head(const archead_handle* h, const void* x, int64_t M,
+                                           int64_t ldx, const void* dense, int64_t ldw,
+                                           float* kl, float* sq, int64_t* ref_idx,
+                                           int64_t* rank, void* ws, size_t ws_bytes,
+                                           void* stream) {
+  clear_error();
+  archead_status st = check_call(h, x, M, ldx, ws, ws_bytes, ARCHEAD_OP_FIDELITY);
+  if (st != ARCHEAD_OK || M == 0) return st;
+  if (!mfma_ok(h)) return fail(ARCHEAD_E_UNSUPPORTED, "the head has no tiled kernel (g %% 64 != 0)");
+  if (!dense || !kl || !sq || !ref_idx || !rank)
+    return fail(ARCHEAD_E_INVALID_ARG, "dense, kl, sq, ref_idx and rank are required");
+  if (ldw < h->desc.d) return fail(ARCHEAD_E_INVALID_ARG, "ldw < d");
+  if (!aligned(dense, 16) || ldw % 8)
+    return fail(ARCHEAD_E_MISALIGNED, "dense must be 16-byte aligned with ldw %% 8 == 0");
+  if (!aligned(kl, 4) || !aligned(sq, 4) || !aligned(ref_idx, 8) || !aligned(rank, 8))
+    return fail(ARCHEAD_E_MISALIGNED, "kl / sq / ref_idx / rank misaligned");
+  if (ldw * 2 * kTN >= (int64_t(1) << 31))
+    return fail(ARCHEAD_E_UNSUPPORTED, "ldw too large for the tiled kernel");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const WsLayout w = ws_layout(h, M, ARCHEAD_OP_FIDELITY);
+  char* base = static_cast<char*>(ws);
+  st = launch_mfma_prologue(h, x, M, ldx, w, base, s);
+  if (st != ARCHEAD_OK) return st;
+  MfmaArgs a = mfma_args(h, x, M, ldx, w, base);
+  a.n_mt = (M + 63) / 64;   // 64-row tiles of 4 waves in both passes
+  a.n_tiles = a.n_vt * a.n_mt;
+  a.tiles_per_xcd = (a.n_tiles + 7) / 8;
+  a.dense = static_cast<const uint16_t*>(dense);
+  a.ldw = ldw;
+  a.fid_part = base + w.fid_off;
+  float* bref = reinterpret_cast<float*>(base + w.bref_off);
+  a.bref = bref;
+  a.ref_idx = ref_idx;
+  a.rank = rank;
+  const int64_t grid = 8 * a.tiles_per_xcd;
+  if (grid > 0x7fffffff) return fail(ARCHEAD_E_UNSUPPORTED, "too many MFMA tiles");
+  for (int xe = 1; xe <= 2; ++xe) {
+    const void* fn = kern::mfma_fid(xe);
+    const int lds = xe == 1 ? MGeomT<64, 4, true>::LDS : MGeomT<64, 4>::LDS;
+    hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, lds);
+    if (e != hipSuccess) return hip_fail(e, "fidelity pass LDS size attribute");
+    void* args[] = {&a};
+    e = hipExtLaunchKernel(fn, dim3(unsigned(grid)), dim3(256), args, size_t(lds), s, nullptr,
+                           nullptr, 0);
+    if (e != hipSuccess) return hip_fail(e, "fidelity pass launch");
+    if (xe == 1) {
+      const FidTilePart* part = static_cast<const FidTilePart*>(a.fid_part);
+      int64_t n_vt = a.n_vt;
+      void* margs[] = {&part, &n_vt, &M, &kl, &sq, &ref_idx, &bref, &rank};
+      e = hipLaunchKernel(kern::fid_head_merge(), dim3(unsigned((M + 63) / 64)), dim3(64), margs,
+                          0, s);
+      if (e != hipSuccess) return hip_fail(e, "fidelity merge launch");
+    }
+  }
+  return ARCHEAD_OK;
 }
 
 archead_status archead_logits_topk(const archead_handle* h, const void* x, int64_t M,

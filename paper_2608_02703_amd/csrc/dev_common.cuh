@@ -356,28 +356,33 @@ constexpr int kExpDims = 16;                 // rank dimensions per expansion st
 // NW = 4 (1 x 4 waves of TM x 64; TM = 128: two workgroups per CU, TM = 64:
 // three), whose stage barriers are independent, so one's LDS waits, tile
 // start and epilogue overlap the others' MFMAs.  A stage holds x [TM][kKS] bf16,
-// codes [kTN][kKS/2], the scale ratios of the kTN columns and the slot
-// biases of the TM rows.
-template <int TM, int NW = kMWaves>
+// codes [kTN][kKS/2], (FID: the dense head's rows [kTN][kKS] bf16,) the scale
+// ratios of the kTN columns and the slot biases of the TM rows.
+template <int TM, int NW = kMWaves, bool FID = false>
 struct MGeomT {
   static constexpr int WMW = NW / 4;                  // waves along the tokens
   static constexpr int WM = TM / WMW;                 // token rows per wave
   static constexpr int MI = WM / 16;                  // 16-row MFMA blocks per wave
   static constexpr int XBYTES = TM * kKS * 2;         // x [TM][kKS] bf16
   static constexpr int CBYTES = kTN * kKS / 2;        // codes [kTN][kKS/2]
-  static constexpr int RAT = XBYTES + CBYTES;         // fp32 [kTN] scale ratios
+  static constexpr int DOFF = XBYTES + CBYTES;        // dense rows (fidelity pass)
+  static constexpr int DBYTES = FID ? kTN * kKS * 2 : 0;
+  static constexpr int RAT = DOFF + DBYTES;           // fp32 [kTN] scale ratios
   static constexpr int BIAS = RAT + kTN * 4;          // fp32 [TM] slot biases
   static constexpr int STAGE = BIAS + TM * 4;
   static constexpr int NX = XBYTES / 1024 / NW;       // x loads per wave and stage
   static constexpr int NC = CBYTES / 1024 / NW;       // code loads per wave and stage
   static constexpr int NA = NW == 8 ? 1 : 2;          // ratio / bias loads per wave
-  static constexpr int NL = NX + NC + NA;             // loads per wave and stage
+  static constexpr int ND = DBYTES / 1024 / NW;       // dense-row loads per wave
+  static constexpr int NL = NX + NC + NA + ND;        // loads per wave and stage
+  static constexpr int PPS = (NL + 2 * MI - 1) / (2 * MI);   // loads per MFMA row block
   static constexpr int LDS = kRing * STAGE;
-  static constexpr int WGS = NW == 8 ? 1 : (TM == 128 ? 2 : 3);   // workgroups per CU
+  static constexpr int WGS = FID ? 1 : NW == 8 ? 1 : (TM == 128 ? 2 : 3);   // workgroups per CU
   static_assert(NW == 8 || (NW == 4 && (TM == 128 || TM == 64)), "layouts built");
-  static_assert(XBYTES % (1024 * NW) == 0 && CBYTES % (1024 * NW) == 0, "whole loads");
+  static_assert(!FID || (NW == 4 && TM == 64), "fidelity pass: 64-row tiles of 4 waves");
+  static_assert(XBYTES % (1024 * NW) == 0 && CBYTES % (1024 * NW) == 0 &&
+                DBYTES % (1024 * NW) == 0, "whole loads");
   static_assert(LDS * WGS <= 160 * 1024, "LDS budget");
-  static_assert(NL <= 2 * MI, "one load per MFMA row block of the stage");
   static_assert(TM % 64 == 0 && TM <= kTM, "bias loads of 64 rows per wave");
 };
 using MGeom = MGeomT<kTM>;

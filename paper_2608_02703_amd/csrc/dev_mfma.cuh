@@ -54,15 +54,37 @@ struct MfmaArgs {
   float2* part;            // [M, n_vt]
   int* part_idx;           // [M, n_vt] argmax partials, or null
   float* tgt_logit;        // [M]
+  // logit fidelity against a dense bf16 head (XE = 1) and the rank pass (XE = 2)
+  const uint16_t* dense;   // [V][ldw] bf16
+  int64_t ldw;
+  void* fid_part;          // [M][n_vt] FidTilePart
+  const float* bref;       // [M] packed logit at the reference's top-1
+  const int64_t* ref_idx;  // [M] the reference's top-1
+  int64_t* rank;           // [M]
 };
 
+// One vocabulary tile's statistics of one token for the fidelity pass: the
+// maxima of the dense (a) and packed (b) logits, the first index of the
+// maximum of a and b there, and relative to the maxima sum e^(a - ma),
+// sum e^(b - mb), sum e^(a - ma) (a - b) and sum (a - b)^2.
+struct FidTilePart {
+  float ma, mb, bat, sa, sb, t, sq;
+  int ia;                  // vocabulary index (kNoIdx: none)
+};
+static_assert(sizeof(FidTilePart) == 32, "the workspace holds 32 bytes per tile and token");
+
+// XE: 0 logits or CE (CE), 1 the fidelity pass (the dense head's rows are
+// streamed through the same stages and accumulated beside the packed
+// logits; per-tile FidTilePart out), 2 the rank pass (per token, packed
+// logits ranked ahead of bref / ref_idx counted into rank).
 // (waves per SIMD: 2 with 8-wave workgroups and with 128-row tiles of 4
 // waves, two workgroups per CU; 3 with 64-row tiles, three per CU)
-template <bool CE, int TM, int NW>
+template <bool CE, int TM, int NW, int XE = 0>
 __global__ __launch_bounds__(NW * 64)
-__attribute__((amdgpu_waves_per_eu(MGeomT<TM, NW>::WGS * NW / 4 > 2 ? MGeomT<TM, NW>::WGS * NW / 4 : 2)))
+__attribute__((amdgpu_waves_per_eu(MGeomT<TM, NW, XE == 1>::WGS * NW / 4 > 2
+                                       ? MGeomT<TM, NW, XE == 1>::WGS * NW / 4 : 2)))
 void k_mfma(MfmaArgs a) {
-  using G = MGeomT<TM, NW>;
+  using G = MGeomT<TM, NW, XE == 1>;
   constexpr int MI = G::MI;        // row blocks per wave
   constexpr int WM = G::WM;        // token rows per wave
   extern __shared__ __align__(16) uint8_t mfma_lds[];
@@ -110,6 +132,15 @@ void k_mfma(MfmaArgs a) {
   const __amdgpu_buffer_rsrc_t ru = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<int8_t*>(a.ucodes + v0 * int64_t(urow)), 0, int(uint32_t(cols) * urow),
       kBufferWord3);
+  // dense rows of the tile (fidelity pass); the expansion stages load from
+  // an empty resource (zeros, no memory traffic) so every stage issues the
+  // same number of loads
+  const uint32_t dstride = uint32_t(a.ldw) * 2;
+  const __amdgpu_buffer_rsrc_t rd = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(XE == 1 ? a.dense + v0 * a.ldw : a.x), 0,
+      XE == 1 ? int((cols - 1) * dstride + uint32_t(a.d) * 2) : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t rdz = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(a.x), 0, 0, kBufferWord3);
   // auxiliary loads of this wave: the scale ratios of 64 columns and / or
   // the slot biases of 64 token rows (NW = 8: waves 0-3 the ratios, 4-7 the
   // biases; NW = 4: every wave both)
@@ -144,6 +175,15 @@ void k_mfma(MfmaArgs a) {
   uint32_t co[G::NC];
 #pragma unroll
   for (int ci = 0; ci < G::NC; ++ci) co[ci] = cunit(ci, rowbytes);
+  // dense-row units, laid out like x (rows of kKS bf16, XOR-swizzled units)
+  auto dunit = [&](int i) {
+    const int off = (wid * G::ND + i) * 1024 + 16 * lane;
+    const int r = off / (2 * kKS), p = (off % (2 * kKS)) / 16;
+    return uint32_t(r < cols ? r : cols - 1) * dstride + 16u * uint32_t(p ^ swz_x(r));
+  };
+  uint32_t dof[G::ND > 0 ? G::ND : 1];
+#pragma unroll
+  for (int i = 0; i < G::ND; ++i) dof[i] = dunit(i);
   const uint32_t ao_rat = uint32_t((wid & 3) * 64 + lane) * 4;
   const uint32_t ao_bias = uint32_t(bw * 64 + lane < rows ? bw * 64 + lane : rows - 1) * 4;
 
@@ -168,12 +208,17 @@ void k_mfma(MfmaArgs a) {
       lds_u8* dst = base + G::XBYTES + (wid * G::NC + ci) * 1024;
       if (res) dma16(rc, dst, co[ci] + uint32_t(s) * (kKS / 2));
       else dma16(ru, dst, cunit(ci, urow) + uint32_t(s - nst) * 32);
-    } else {
+    } else if (part < G::NX + G::NC + G::NA) {
       const uint32_t k = uint32_t(KIND == 1 ? s / spg : slot_of(s)) * 1024u;
       if (NW == 4 ? part == G::NX + G::NC : arat)
         dma4(rrat, base + G::RAT + (wid & 3) * 256, ao_rat + k);
       else
         dma4(rbias, base + G::BIAS + bw * 256, ao_bias + k);
+    } else {
+      const int di = part - G::NX - G::NC - G::NA;
+      lds_u8* dst = base + G::DOFF + (wid * G::ND + di) * 1024;
+      if (res) dma16(rd, dst, dof[di] + uint32_t(s) * (kKS * 2));
+      else dma16(rdz, dst, 0u);
     }
   };
   using kMain = std::integral_constant<int, 1>;
@@ -200,6 +245,18 @@ void k_mfma(MfmaArgs a) {
   for (int i = 0; i < MI; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // the dense head's logits (fidelity pass): plain fp32 sums of bf16 products
+  constexpr int MD = XE == 1 ? MI : 1;
+  f32x4_t accd[MD][4];
+#pragma unroll
+  for (int i = 0; i < MD; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) accd[i][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // dense B fragments: row 64 wn + 16 ni + lr, the same 16-byte units as x
+  uint32_t bdoff[2];
+#pragma unroll
+  for (int kc = 0; kc < 2; ++kc)
+    bdoff[kc] = G::DOFF + uint32_t(64 * wn + lr) * (2 * kKS) + 16u * uint32_t((2 * q + kc) ^ swz_x(lr));
 
   // final scales and (CE) the targets of the tile's rows, loaded before the
   // stage loads so they have arrived by the epilogue
@@ -257,6 +314,12 @@ void k_mfma(MfmaArgs a) {
       bf16x8_t B[4];
 #pragma unroll
       for (int ni = 0; ni < 4; ++ni) B[ni] = unpack8(braw[ni][kc], kMask, kMagic);
+      bf16x8_t Bd[XE == 1 ? 4 : 1];
+      if constexpr (XE == 1) {
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni)
+          Bd[ni] = lds_load<bf16x8_t>(base + bdoff[kc] + ni * 16 * (2 * kKS));
+      }
 #pragma unroll
       for (int mi = 0; mi < MI; ++mi) {
         const bf16x8_t Am = A[mi];
@@ -264,9 +327,18 @@ void k_mfma(MfmaArgs a) {
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Am, B[ni], acc[mi][ni], 0, 0, 0);
-        if (kc * MI + mi < G::NL) {
-          if constexpr (ISSUE == 1) issue_part(s + 2, nb, kc * MI + mi, kMain{});
-          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, kc * MI + mi, kAny{});
+        if constexpr (XE == 1) {
+#pragma unroll
+          for (int ni = 0; ni < 4; ++ni)
+            accd[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(Am, Bd[ni], accd[mi][ni], 0, 0, 0);
+        }
+#pragma unroll
+        for (int pp = 0; pp < G::PPS; ++pp) {
+          const int part = (kc * MI + mi) * G::PPS + pp;
+          if (part < G::NL) {
+            if constexpr (ISSUE == 1) issue_part(s + 2, nb, part, kMain{});
+            if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, part, kAny{});
+          }
         }
       }
     }
@@ -292,9 +364,13 @@ void k_mfma(MfmaArgs a) {
 #pragma unroll
         for (int ni = 0; ni < 4; ++ni)
           acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B[ni], acc[mi][ni], 0, 0, 0);
-        if (kc * MI + mi < G::NL) {
-          if constexpr (ISSUE == 2) issue_part(s + 2, nb, kc * MI + mi, kExp{});
-          if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, kc * MI + mi, kAny{});
+#pragma unroll
+        for (int pp = 0; pp < G::PPS; ++pp) {
+          const int part = (kc * MI + mi) * G::PPS + pp;
+          if (part < G::NL) {
+            if constexpr (ISSUE == 2) issue_part(s + 2, nb, part, kExp{});
+            if constexpr (ISSUE == 3) if (s + 2 < ntot) issue_part(s + 2, nb, part, kAny{});
+          }
         }
       }
     }
@@ -314,7 +390,123 @@ void k_mfma(MfmaArgs a) {
     for (int mi = 0; mi < MI; ++mi) acc[mi][ni] *= fin[ni];
 
   // ---- epilogue
-  if constexpr (!CE) {
+  if constexpr (XE == 1) {
+    // per token row of the tile: the FidTilePart of its valid columns (a the
+    // dense logit, b the packed one); the 16 lanes of a quarter-wave share
+    // rows, the four waves along the vocabulary merge through LDS in order
+    FidTilePart* sp = reinterpret_cast<FidTilePart*>(mfma_lds);   // [4][TM]
+    __syncthreads();
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = WM * wm + 16 * mi + 4 * q + i;
+        float ma = -INFINITY, mb = -INFINITY;
+        int ia = kNoIdx;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int col = 64 * wn + 16 * ni + lr;
+          if (col < cols) {
+            const float av = accd[mi][ni][i];
+            if (av > ma) {   // strict: a lane's columns rise, so its first maximum stays
+              ma = av;
+              ia = col;
+            }
+            mb = fmaxf(mb, acc[mi][ni][i]);
+          }
+        }
+        const float mar = row16_max(ma);
+        const int iar = row16_min_i(ma == mar ? ia : kNoIdx);
+        const float mbr = row16_max(mb);
+        float bat = -INFINITY, sa = 0.f, sb = 0.f, t = 0.f, sq = 0.f;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int col = 64 * wn + 16 * ni + lr;
+          if (col < cols) {
+            const float av = accd[mi][ni][i], bv = acc[mi][ni][i];
+            if (col == iar) bat = bv;
+            const float ea = expf(av - mar), dd = av - bv;
+            sa += ea;
+            sb += expf(bv - mbr);
+            t += ea * dd;
+            sq += dd * dd;
+          }
+        }
+        bat = row16_max(bat);
+        sa = row16_sum(sa);
+        sb = row16_sum(sb);
+        t = row16_sum(t);
+        sq = row16_sum(sq);
+        if (lr == 0) sp[wn * TM + row] = FidTilePart{mar, mbr, bat, sa, sb, t, sq, iar};
+      }
+    __syncthreads();
+    if (tid < rows) {
+      FidTilePart r = sp[tid];   // wave 0 holds column 0, always valid
+#pragma unroll
+      for (int w = 1; w < 4; ++w) {
+        const FidTilePart o = sp[w * TM + tid];
+        if (o.ma > r.ma) {
+          const float f = expf(r.ma - o.ma);
+          r.sa = r.sa * f + o.sa;
+          r.t = r.t * f + o.t;
+          r.ma = o.ma;
+          r.ia = o.ia;
+          r.bat = o.bat;
+        } else if (o.ma > -INFINITY) {   // equal maxima keep the smaller index (this wave's)
+          const float f = expf(o.ma - r.ma);
+          r.sa += o.sa * f;
+          r.t += o.t * f;
+        }
+        if (o.mb > r.mb) {
+          r.sb = r.sb * expf(r.mb - o.mb) + o.sb;
+          r.mb = o.mb;
+        } else if (o.mb > -INFINITY) {
+          r.sb += o.sb * expf(o.mb - r.mb);
+        }
+        r.sq += o.sq;
+      }
+      r.ia = r.ia == kNoIdx ? kNoIdx : int(v0) + r.ia;
+      reinterpret_cast<FidTilePart*>(a.fid_part)[(m0 + tid) * a.n_vt + vt] = r;
+    }
+  } else if constexpr (XE == 2) {
+    // per token row: the packed logits of this tile ranked ahead of the
+    // reference's top-1 (larger, or equal at a smaller index), added to rank
+    float* sbr = reinterpret_cast<float*>(mfma_lds);   // [TM] bref
+    int* sri = reinterpret_cast<int*>(sbr + TM);       // [TM] ref_idx - v0, clamped
+    int* scnt = sri + TM;                              // [4][TM]
+    __syncthreads();
+    if (tid < TM) {
+      const bool ok = tid < rows;
+      const int64_t dr = ok ? a.ref_idx[m0 + tid] - v0 : -1;
+      sbr[tid] = ok ? a.bref[m0 + tid] : 0.f;
+      sri[tid] = dr < 0 ? -1 : (dr > kTN ? kTN : int(dr));
+    }
+    __syncthreads();
+#pragma unroll
+    for (int mi = 0; mi < MI; ++mi)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int row = WM * wm + 16 * mi + 4 * q + i;
+        const float br = sbr[row];
+        const int ri = sri[row];
+        int c = 0;
+#pragma unroll
+        for (int ni = 0; ni < 4; ++ni) {
+          const int col = 64 * wn + 16 * ni + lr;
+          const float bv = acc[mi][ni][i];
+          c += (col < cols) & ((bv > br) | ((bv == br) & (col < ri)));
+        }
+#pragma unroll
+        for (int off = 8; off > 0; off >>= 1) c += __shfl_xor(c, off, 16);
+        if (lr == 0) scnt[wn * TM + row] = c;
+      }
+    __syncthreads();
+    if (tid < rows) {
+      const int tot = scnt[tid] + scnt[TM + tid] + scnt[2 * TM + tid] + scnt[3 * TM + tid];
+      if (tot) atomicAdd(reinterpret_cast<unsigned long long*>(a.rank + m0 + tid),
+                         (unsigned long long)tot);
+    }
+  } else if constexpr (!CE) {
 #pragma unroll
     for (int mi = 0; mi < MI; ++mi)
 #pragma unroll

@@ -90,6 +90,9 @@ struct WsLayout {
   size_t tk_pv_off = 0;   // fp32 [chunk or 1][n_part][kTopKMax] partial lists
   size_t tk_pi_off = 0;   // int32, the same shape
   Path tk_path = Path::kGemv;   // kernel of the chunks' logits (that of the whole M)
+  // fidelity against a dense head: the tiled path's layout, then
+  size_t fid_off = 0;     // [M][n_vt] per-tile statistics (32 bytes each)
+  size_t bref_off = 0;    // fp32 [M] packed logit at the dense top-1
   size_t total = 0;
   int64_t n_part = 0;
 };

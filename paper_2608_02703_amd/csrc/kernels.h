@@ -27,6 +27,11 @@ const void* mid(int gw, bool ce, bool sc8, int gen);
 // per tile with nw = 8 waves per workgroup, or tm = 128 or 64 with nw = 4)
 // and its prologue kernels
 const void* mfma(bool ce, int tm, int nw);
+// the tiled kernel's fidelity pass (xe = 1: dense rows streamed beside the
+// packed codes) and rank pass (xe = 2), 64-row tiles of 4 waves, and the
+// per-token merge of the fidelity pass's tile statistics
+const void* mfma_fid(int xe);
+const void* fid_head_merge();
 const void* prep();
 const void* stage1m();
 const void* stage1m_fin();

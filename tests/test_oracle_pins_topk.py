@@ -1,6 +1,8 @@
 """Pins of the oracle's top-k selection (oracle.metrics.topk), the reference
 for archead_logits_topk: the candidate set of top-k decoding and of the
-top-k agreement metric (Section 4, "Logit Fidelity", Table 8).
+top-k agreement metric (Section 4, "Logit Fidelity", Table 8); and of the
+oracle's dense bf16 head logits (oracle.head.dense_bf16_logits), the
+reference side of the fidelity pass.
 
 * hand-worked rows (tests/golden/topk_v1.txt): ties, NaN, -inf, signed
   zero, k = V and k = 1;
@@ -94,3 +96,25 @@ def test_topk_matches_fidelity_rank():
         _, i = metrics.topk(test, k)
         member = np.array([ref_idx[m] in i[m] for m in range(ref.shape[0])])
         assert np.array_equal(member, rank < k)
+
+
+def test_dense_bf16_logits_exact_on_tiny():
+    """oracle.head.dense_bf16_logits against exact rational dot products:
+    bf16 values are dyadic rationals, so every logit has an exact value, which
+    the fp64 result must match to its rounding."""
+    from fractions import Fraction
+    from oracle import head as ohead
+    from oracle import layout
+    rng = np.random.default_rng(6)
+    V, d, M = 5, 9, 3
+    def bits(shape):   # finite bf16 patterns of both signs, magnitudes ~2^-8 .. 2
+        r = rng.integers(0, 2 ** 16, size=shape)
+        return ((r & 0x3FFF) | 0x3C00 | (r & 0x8000)).astype(np.uint16)
+    w_bits, x_bits = bits((V, d)), bits((M, d))
+    got = ohead.dense_bf16_logits(w_bits, x_bits)
+    w = layout.bf16_to_f64(w_bits)
+    x = layout.bf16_to_f64(x_bits)
+    for m in range(M):
+        for v in range(V):
+            exact = sum(Fraction(float(x[m, i])) * Fraction(float(w[v, i])) for i in range(d))
+            assert abs(got[m, v] - float(exact)) <= 1e-14 * max(1.0, abs(float(exact)))
