@@ -685,7 +685,7 @@ def main():
         tflops = flops / (kern_p * 1e-3) / 1e12
         prefill = {"M": Mp, "ms_per_step": round(ms_p, 4), "tok_s": round(Mp / ms_p * 1e3, 1),
                    "mean_ce": mean_ce,
-                   "mfma_kernel": {"kernel": "k_mfma<true, 256, 8>",
+                   "mfma_kernel": {"kernel": "k_mfma<true, 256, 8, 0>",
                                    "kernel_ms_median": round(kern_p, 4),
                                    "algorithmic_flops": flops,
                                    "achieved_tflops": round(tflops, 1),
