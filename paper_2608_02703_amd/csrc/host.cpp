@@ -40,6 +40,12 @@ int lanes_per_row(const archead_desc& d) {
   while (lpr > 1 && chunks % lpr) lpr >>= 1;
   const int64_t r4 = (d.r_c + d.r_r) / 4;
   while (lpr < 64 && r4 > 2 * lpr && chunks % (2 * lpr) == 0) lpr *= 2;
+  // and where a row's group scales would not fit one dword per segment lane
+  // (2 fp16 scales or 4 8-bit codes per lane: g = 64 with fp16 scales at
+  // d = 4096 takes 32 lanes); the general-code variants keep 8 or 16
+  const int64_t gpl = d.scale_dtype == ARCHEAD_U8 ? 4 : 2;
+  if (!gen_codes(d))
+    while (lpr < 64 && d.d / d.g > gpl * lpr && chunks % (2 * lpr) == 0) lpr *= 2;
   return lpr;
 }
 

@@ -163,3 +163,24 @@ def test_paper_qwen_storage_head():
     err = assert_ce_close(ce[rows], ref, what="paper storage CE M=4096")
     say(f"  CE at M=4096 on {rows.size} sampled tokens: max |dCE| {err:.2e}")
     ph.close()
+
+
+@pytest.mark.timeout(900)
+def test_qwen_g64_fp16_scales_gemv():
+    """A Qwen-shaped head with groups of 64 and fp16 scales (the reading of
+    the paper's Gemma storage figure): 64 group scales per row take 32-lane
+    segments on the decode GEMV.  Sampled columns at M = 1 and 2, and CE."""
+    from paper_2608_02703_amd import PackedHead
+    h = make_head("qwen_decode", g=64)
+    ph = PackedHead.from_arrays(h)
+    try:
+        rng = np.random.default_rng(15)
+        ids = np.unique(np.concatenate([[0, 1, 127, 128, h.V - 1], rng.integers(0, h.V, 600)]))
+        x = make_x("qwen_decode", 2)
+        ref = ohead.logits(h, x, vocab=ids)
+        for M in (1, 2):
+            say(f"qwen g=64 fp16 scales: GEMV M={M}")
+            lg = gpu_logits(ph, x[:M])
+            assert_logits_close(lg[:, ids], ref[:M], what=f"g64 fp16 M={M}")
+    finally:
+        ph.close()
