@@ -21,7 +21,9 @@ namespace {
 //    the x fragment read from LDS).  The first MFMA's accumulator input is
 //    the group's offset bias -136 * (sum of x over the group), so the chain
 //    yields the group partial sum c x; the fp16 group scale multiplies it
-//    into the running fp32 total.
+//    into the running fp32 total.  Groups of 64 are loaded in pairs (4 words
+//    per lane, as for g = 128) and each group of a pair gets its own chain,
+//    fed the pair's code fragments with the other group's lanes zeroed.
 //  * then the rank-r expansion in K-chunks of 32 rank dimensions (U_c part
 //    first, then A_w; each zero-padded to whole chunks): lane (j, q) loads
 //    the int8 codes of dims 8q .. 8q+7 of each chunk of its row, converts
@@ -162,12 +164,18 @@ void k_dec(DecArgs a) {
   const uint32_t kMask = opaque_vgpr(0x000F000Fu);
   const uint32_t kMagic = opaque_vgpr(0x43004300u);
   const int xr = lr < M ? lr : M - 1;                  // token row of this lane's A fragments
-  const lds_u8* const xrow = L + xr * a.xstr + 16 * q * GW;
+  // groups of 64 (GW = 2) are read in pairs, one 128-code block per 16-byte
+  // load as for groups of 128 (16 rows x 64 B per load instruction instead
+  // of 16 x 32): lane quarter q holds words 4q .. 4q+3 of the pair, so
+  // quarters 0-1 hold the first group and 2-3 the second; each group's MFMA
+  // chain takes the pair's MFMAs with the other group's lanes zeroed
+  constexpr int QW = GW == 2 ? 4 : GW;                 // code words per lane and load
+  const lds_u8* const xrow = L + xr * a.xstr + 16 * q * QW;
   const lds_u8* const brow = L + a.off_bias + 16 * q;
   const int tpart = M * a.tstr;                        // bf16 elements per part of t in LDS
   const lds_u8* const trow = L + a.off_t + 2 * (xr * a.tstr);
   // this lane's byte offsets within a unit's rows
-  const int voff_c = int(uint32_t(lr) * rowbytes) + q * (4 * GW);        // codes: row lr, quarter q
+  const int voff_c = int(uint32_t(lr) * rowbytes) + q * (4 * QW);        // codes: row lr, quarter q
   constexpr int ESZ = SC8 ? 1 : 2;                                      // bytes per group scale
   const int voff_sc = (lane >> 2) * (ESZ * ngrp) + 16 * (lane & 3);     // scales: row lane/4
   const int voff_u = lr * a.rc + q * (8 * kcu);
@@ -235,8 +243,7 @@ void k_dec(DecArgs a) {
       if constexpr (GW == 4) {
         cbuf[slot][k] = __builtin_amdgcn_raw_buffer_load_b128(lrc, voff_c, so, kDecCpol);
       } else if constexpr (GW == 2) {
-        const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(lrc, voff_c, so, kDecCpol);
-        cbuf[slot][k] = u32x4_t{v.x, v.y, 0u, 0u};
+        if (k % 2 == 0) cbuf[slot][k] = __builtin_amdgcn_raw_buffer_load_b128(lrc, voff_c, so, kDecCpol);
       } else {
         cbuf[slot][k] = u32x4_t{__builtin_amdgcn_raw_buffer_load_b32(lrc, voff_c, so, kDecCpol),
                                 0u, 0u, 0u};
@@ -409,13 +416,32 @@ void k_dec(DecArgs a) {
       f32x4_t acc[SG];
 #pragma unroll
       for (int k = 0; k < SG; ++k) acc[k] = lds_load<f32x4_t>(brow + 64 * (cS * SG + k));
+      if constexpr (GW == 2) {
+        // pair p = groups 2p, 2p+1: the first group's chain sees the codes
+        // of quarters 0-1 only (bf16 zeros elsewhere), the second's those of
+        // quarters 2-3
+        const uint32_t mlo = q < 2 ? 0xffffffffu : 0u;
 #pragma unroll
-      for (int kc = 0; kc < GW; ++kc) {
+        for (int kc = 0; kc < 4; ++kc) {
 #pragma unroll
-        for (int k = 0; k < SG; ++k) {
-          const bf16x8_t A = lds_load<bf16x8_t>(xrow + 2 * (cS * SG + k) * g + 16 * kc);
-          acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              A, unpack8(cbuf[j][k][kc], kMask, kMagic), acc[k], 0, 0, 0);
+          for (int p2 = 0; p2 < SG / 2; ++p2) {
+            const bf16x8_t A = lds_load<bf16x8_t>(xrow + 2 * (cS * SG + 2 * p2) * g + 16 * kc);
+            const u32x4_t B = __builtin_bit_cast(u32x4_t, unpack8(cbuf[j][2 * p2][kc], kMask, kMagic));
+            const bf16x8_t B0 = __builtin_bit_cast(bf16x8_t, B & mlo);
+            const bf16x8_t B1 = __builtin_bit_cast(bf16x8_t, B & ~mlo);
+            acc[2 * p2] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B0, acc[2 * p2], 0, 0, 0);
+            acc[2 * p2 + 1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A, B1, acc[2 * p2 + 1], 0, 0, 0);
+          }
+        }
+      } else {
+#pragma unroll
+        for (int kc = 0; kc < GW; ++kc) {
+#pragma unroll
+          for (int k = 0; k < SG; ++k) {
+            const bf16x8_t A = lds_load<bf16x8_t>(xrow + 2 * (cS * SG + k) * g + 16 * kc);
+            acc[k] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                A, unpack8(cbuf[j][k][kc], kMask, kMagic), acc[k], 0, 0, 0);
+          }
         }
       }
 #pragma unroll

@@ -16,11 +16,14 @@ namespace {
 // writes that share, with the per-group offset biases (-136 times the sum
 // of x over the group, summed across the lanes holding the group with DPP),
 // to the other LDS buffer before the window's closing barrier.  Codes arrive
-// as in k_dec (lane (j, q): row j of the unit, GW dwords from q GW of each
-// group) for all NU units at once, a 128-byte line of each row per request
-// round, one line ahead; a unit's group partial starts from the bias (MFMA
-// C input) and is scaled into the unit's total.  After the last window of a pass the window buffers hold t (three
-// bf16 parts) for the rank-r expansion, then the units' logits go out.
+// in steps of 128 codes of every row (lane (j, q): row j of the unit, the 16
+// bytes from 16 q of the step) for all NU units at once, a 128-byte line of
+// each row per request round, one line ahead; a group's partial starts from
+// its bias (MFMA C input) and is scaled into the unit's total (groups of 64:
+// the two groups of a step each take the step's MFMAs with the other
+// group's lanes zeroed).  After the last window of a pass the window
+// buffers hold t (three bf16 parts) for the rank-r expansion, then the
+// units' logits go out.
 // Stage 1 (t) runs in the same launch as in k_dec.
 constexpr int kMidBlock = 512, kMidWaves = kMidBlock / 64;
 constexpr int kMidKW = 256;   // elements of d per x window
@@ -81,12 +84,17 @@ void k_mid(MidArgs a) {
   constexpr int TM = 16 * NF;
   constexpr int G = 32 * GW;                  // group size
   constexpr int SPW = kMidKW / G;             // groups per window
-  // Code loads go out a 128-byte line of each row at a time (LG groups:
-  // both halves of a line are requested together, not a step apart), one
-  // line ahead, so the ring holds two lines of groups
-  constexpr int LG = 256 / G;
+  // The head is walked in steps of 128 codes of every row: one group of
+  // 128, or a pair of groups of 64 (PG groups per step, one MFMA chain and
+  // scale each), so both group sizes share one loop shape and register
+  // budget.  Code loads go out a 128-byte line of each row at a time (LG
+  // steps: both halves of a line are requested together, not a step
+  // apart), one line ahead, so the ring holds two lines of steps
+  constexpr int PG = 128 / G;                 // groups per step
+  constexpr int SPS = kMidKW / 128;           // steps per window
+  constexpr int LG = 2;
   constexpr int NB = 2 * LG;
-  static_assert((2 * SPW) % NB == 0, "ring slots are compile-time per step");
+  static_assert((2 * SPS) % NB == 0, "ring slots are compile-time per step");
   extern __shared__ __align__(16) uint8_t mid_lds[];
   lds_u8* const L = (lds_u8*)mid_lds;
   const int tid = threadIdx.x, lane = tid & 63;
@@ -127,7 +135,7 @@ void k_mid(MidArgs a) {
   const uint32_t kMagic = opaque_vgpr(0x43004300u);
   const int kcu = a.kcu, kca = a.kca;
   // this lane's byte offsets within a unit's rows
-  const int voff_c = int(uint32_t(lr) * rowbytes) + q * (4 * GW);   // codes: row lr, part q
+  const int voff_c = int(uint32_t(lr) * rowbytes) + 16 * q;   // codes: row lr, part q of a step
   const int voff_u = lr * a.rc + q * (8 * kcu);
   const int voff_a = lr * a.rr + q * (8 * kca);
   auto* const sbias = reinterpret_cast<__attribute__((address_space(3))) float*>(L + a.off_bias);
@@ -204,8 +212,11 @@ void k_mid(MidArgs a) {
       *reinterpret_cast<__attribute__((address_space(3))) u32x4_t*>(xb + row * kMidXstr + 16 * c16) = v;
       float sm = ((bf16_lo(v.x) + bf16_hi(v.x)) + (bf16_lo(v.y) + bf16_hi(v.y))) +
                  ((bf16_lo(v.z) + bf16_hi(v.z)) + (bf16_lo(v.w) + bf16_hi(v.w)));
+      // every lane of the group ends with the same sum (each swap adds a
+      // pair of lanes' values in either order), so all of them store it:
+      // no branch splits the main loop here
       sm = GW == 4 ? row16_sum(sm) : row8_sum(sm);
-      if ((c16 & (4 * GW - 1)) == 0) bb[(c16 / (4 * GW)) * TM + row] = -float(archead::kInt4Bias) * sm;
+      bb[(c16 / (4 * GW)) * TM + row] = -float(archead::kInt4Bias) * sm;
     }
   };
 
@@ -262,19 +273,16 @@ void k_mid(MidArgs a) {
     }
   };
 
+  // step s: codes 128 s .. 128 s + 127 of every row (bytes 64 s ..); lane
+  // (j, q) holds words 4 q .. 4 q + 3 of the step (for groups of 64:
+  // quarters 0-1 the first group of the pair, 2-3 the second)
   u32x4_t cbuf[NB][NU];
   __amdgpu_buffer_rsrc_t rcu[NU];
   auto load_step = [&](auto SLOT, int s) {
     constexpr int slot = decltype(SLOT)::value;
 #pragma unroll
-    for (int j = 0; j < NU; ++j) {
-      if constexpr (GW == 4) {
-        cbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rcu[j], voff_c, s * (G / 2), kDecCpol);
-      } else {
-        const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(rcu[j], voff_c, s * (G / 2), kDecCpol);
-        cbuf[slot][j] = u32x4_t{v.x, v.y, 0u, 0u};
-      }
-    }
+    for (int j = 0; j < NU; ++j)
+      cbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rcu[j], voff_c, s * 64, kDecCpol);
   };
   // absent factors: stride-0 resources over valid buffers (read as zero)
   const void* const cu_b = a.rc ? static_cast<const void*>(a.cu) : static_cast<const void*>(a.rs);
@@ -312,10 +320,6 @@ void k_mid(MidArgs a) {
       load_win(std::integral_constant<int, 1>{}, 1);
       load_step(std::integral_constant<int, 0>{}, 0);
       load_step(std::integral_constant<int, 1>{}, 1);
-      if constexpr (LG == 4) {
-        load_step(std::integral_constant<int, 2>{}, 2);
-        load_step(std::integral_constant<int, 3>{}, 3);
-      }
       const int pr = ngrp / 4;   // pieces per row
 #pragma unroll
       for (int j = 0; j < NU; ++j)
@@ -345,52 +349,63 @@ void k_mid(MidArgs a) {
 #pragma unroll
       for (int f = 0; f < NF; ++f) tot[j][f] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
-    // iterations of two windows (2 SPW groups): window parity and ring slot
+    // iterations of two windows (2 SPS steps): window parity and ring slot
     // of every step are compile-time constants
-    constexpr int IT = 2 * SPW;
+    constexpr int IT = 2 * SPS;
+    const int nstep = ngrp / PG;
 #pragma unroll 1
-    for (int it = 0; it < ngrp / IT; ++it) {
+    for (int it = 0; it < nstep / IT; ++it) {
       auto body = [&](auto J) {
         constexpr int j = decltype(J)::value;
-        constexpr int par = j / SPW;             // window parity (set of its fetch)
-        const int s = IT * it + j;               // group of this step
+        constexpr int par = j / SPS;             // window parity (set of its fetch)
+        const int s = IT * it + j;               // this step
         const int w = 2 * it + par;              // its window
-        if constexpr (j % SPW == 0) load_win(std::integral_constant<int, par>{}, w + 2);
+        if constexpr (j % SPS == 0) load_win(std::integral_constant<int, par>{}, w + 2);
         if constexpr (j % LG == 0) {
-          // the next line of every row: groups s + LG .. s + 2 LG - 1
+          // the next line of every row: steps s + LG .. s + 2 LG - 1
           auto next = [&](auto E) {
             constexpr int e = decltype(E)::value;
             const int sn = s + LG + e;
-            load_step(std::integral_constant<int, (j + LG + e) % NB>{}, sn < ngrp ? sn : ngrp - 1);
+            load_step(std::integral_constant<int, (j + LG + e) % NB>{}, sn < nstep ? sn : nstep - 1);
           };
           next(std::integral_constant<int, 0>{});
           next(std::integral_constant<int, 1>{});
-          if constexpr (LG == 4) {
-            next(std::integral_constant<int, 2>{});
-            next(std::integral_constant<int, 3>{});
-          }
         }
         asm volatile("" ::: "memory");
-        const lds_u8* const xb = L + par * (TM * kMidXstr) + (j % SPW) * (2 * G);
-        const auto* bb = sbias + par * (SPW * TM) + (j % SPW) * TM;
-        f32x4_t acc[NU][NF];
+        // four K-chunks of 32 codes per step, MFMA kc taking word kc of every
+        // lane (elements 32 q + 8 kc .. of the step).  Groups of 64: each
+        // group of the pair has its own chain over all four chunks, fed the
+        // B fragment with the other group's quarters zeroed
+        const lds_u8* const xb = L + par * (TM * kMidXstr) + (j % SPS) * 256;
+        const auto* bb = sbias + par * (SPW * TM) + PG * (j % SPS) * TM;
+        const uint32_t mlo = q < 2 ? 0xffffffffu : 0u;
+        f32x4_t acc[PG][NU][NF];
 #pragma unroll
-        for (int kc = 0; kc < GW; ++kc) {
+        for (int kc = 0; kc < 4; ++kc) {
           bf16x8_t A[NF];
 #pragma unroll
           for (int f = 0; f < NF; ++f)
-            A[f] = lds_load<bf16x8_t>(xb + (16 * f + lr) * kMidXstr + 16 * (q * GW + kc));
+            A[f] = lds_load<bf16x8_t>(xb + (16 * f + lr) * kMidXstr + 16 * (4 * q + kc));
 #pragma unroll
           for (int u = 0; u < NU; ++u) {
-            const bf16x8_t B = unpack8(cbuf[j % NB][u][kc], kMask, kMagic);
-#pragma unroll
-            for (int f = 0; f < NF; ++f) {
-              const f32x4_t c0 =
-                  kc == 0 ? *reinterpret_cast<const __attribute__((address_space(3))) f32x4_t*>(
-                                bb + 16 * f + 4 * q)
-                          : acc[u][f];
-              acc[u][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[f], B, c0, 0, 0, 0);
+            bf16x8_t B[PG];
+            if constexpr (PG == 1) {
+              B[0] = unpack8(cbuf[j % NB][u][kc], kMask, kMagic);
+            } else {
+              const u32x4_t b = __builtin_bit_cast(u32x4_t, unpack8(cbuf[j % NB][u][kc], kMask, kMagic));
+              B[0] = __builtin_bit_cast(bf16x8_t, b & mlo);
+              B[PG - 1] = __builtin_bit_cast(bf16x8_t, b & ~mlo);
             }
+#pragma unroll
+            for (int h = 0; h < PG; ++h)
+#pragma unroll
+              for (int f = 0; f < NF; ++f) {
+                const f32x4_t c0 =
+                    kc == 0 ? *reinterpret_cast<const __attribute__((address_space(3))) f32x4_t*>(
+                                  bb + h * TM + 16 * f + 4 * q)
+                            : acc[h][u][f];
+                acc[h][u][f] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(A[f], B[h], c0, 0, 0, 0);
+              }
           }
           // one K-chunk's fragments live at a time (the scheduler would
           // otherwise hoist every chunk's LDS reads and unpacks, past the
@@ -398,12 +413,15 @@ void k_mid(MidArgs a) {
           __builtin_amdgcn_sched_barrier(0);
         }
 #pragma unroll
-        for (int u = 0; u < NU; ++u) {
-          const float sc = f16_to_f32(lds_load<uint16_t>(ssc + (u * 16 + lr) * sstr + 2 * s));
+        for (int h = 0; h < PG; ++h)
 #pragma unroll
-          for (int f = 0; f < NF; ++f) tot[u][f] += sc * acc[u][f];
-        }
-        if constexpr (j % SPW == SPW - 1) {
+          for (int u = 0; u < NU; ++u) {
+            const float sc =
+                f16_to_f32(lds_load<uint16_t>(ssc + (u * 16 + lr) * sstr + 2 * (PG * s + h)));
+#pragma unroll
+            for (int f = 0; f < NF; ++f) tot[u][f] += sc * acc[h][u][f];
+          }
+        if constexpr (j % SPS == SPS - 1) {
           // window w + 1 (fetched during window w - 1, or before the loop)
           store_win(std::integral_constant<int, 1 - par>{}, w + 1);
           lds_barrier();
@@ -413,12 +431,6 @@ void k_mid(MidArgs a) {
       body(std::integral_constant<int, 1>{});
       body(std::integral_constant<int, 2>{});
       body(std::integral_constant<int, 3>{});
-      if constexpr (IT == 8) {
-        body(std::integral_constant<int, 4>{});
-        body(std::integral_constant<int, 5>{});
-        body(std::integral_constant<int, 6>{});
-        body(std::integral_constant<int, 7>{});
-      }
     }
 
     // ---- rank-r expansion and the units' logits.  Its operands are

@@ -100,7 +100,7 @@ MidLds mid_lds(const archead_desc& d) {
   l.off_y = l.off_red + kMidWaveCount * tm * 8;
   l.off_idx = l.off_y + tm * 8;                 // argmax partials [waves][tm]
   l.off_sc = l.off_idx + kMidWaveCount * tm * 4; // per wave: [units][16 rows][d/g + 2] fp16
-  const int nu = d.g == 128 ? 3 : 2;            // units per wave and pass
+  const int nu = 3;                             // units per wave and pass
   l.total = l.off_sc + kMidWaveCount * nu * 16 * int(2 * (d.d / d.g) + 4);
   return l;
 }

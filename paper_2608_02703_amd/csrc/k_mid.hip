@@ -10,14 +10,13 @@ namespace {
 
 using MidFn = void (*)(MidArgs);
 
-// Tiles of 32 tokens (two MFMA row blocks) and 3 units per wave (groups of
-// 128) or 2 (groups of 64): the largest that keep the main loop within the
-// register budget.  (Tiles of 64 tokens with 2 units per wave measured
-// slower than two tiles of 32.)
+// Tiles of 32 tokens (two MFMA row blocks) and 3 units per wave, for both
+// group sizes (the main loop walks 128 codes per step either way).  (Tiles
+// of 64 tokens with 2 units per wave measured slower than two tiles of 32.)
 template <bool CE, int GEN>
 MidFn mid_fn(int gw, bool sc8) {
-  if (sc8) return gw == 4 ? k_mid<4, 2, 3, CE, true, GEN> : k_mid<2, 2, 2, CE, true, GEN>;
-  return gw == 4 ? k_mid<4, 2, 3, CE, false, GEN> : k_mid<2, 2, 2, CE, false, GEN>;
+  if (sc8) return gw == 4 ? k_mid<4, 2, 3, CE, true, GEN> : k_mid<2, 2, 3, CE, true, GEN>;
+  return gw == 4 ? k_mid<4, 2, 3, CE, false, GEN> : k_mid<2, 2, 3, CE, false, GEN>;
 }
 
 template <int GEN>

@@ -169,17 +169,18 @@ def test_paper_qwen_storage_head():
 def test_qwen_g64_fp16_scales_gemv():
     """A Qwen-shaped head with groups of 64 and fp16 scales (the reading of
     the paper's Gemma storage figure): 64 group scales per row take 32-lane
-    segments on the decode GEMV.  Sampled columns at M = 1 and 2, and CE."""
+    segments on the decode GEMV, and the MFMA decode kernels read the groups
+    in pairs.  Sampled columns at M = 1, 2 (GEMV), 8, 16 (k_dec) and 32."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("qwen_decode", g=64)
     ph = PackedHead.from_arrays(h)
     try:
         rng = np.random.default_rng(15)
         ids = np.unique(np.concatenate([[0, 1, 127, 128, h.V - 1], rng.integers(0, h.V, 600)]))
-        x = make_x("qwen_decode", 2)
+        x = make_x("qwen_decode", 32)
         ref = ohead.logits(h, x, vocab=ids)
-        for M in (1, 2):
-            say(f"qwen g=64 fp16 scales: GEMV M={M}")
+        for M in (1, 2, 8, 16, 32):
+            say(f"qwen g=64 fp16 scales: M={M}")
             lg = gpu_logits(ph, x[:M])
             assert_logits_close(lg[:, ids], ref[:M], what=f"g64 fp16 M={M}")
     finally:
