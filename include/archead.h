@@ -436,6 +436,42 @@ archead_status archead_get_mid_range(const archead_handle* h, int64_t* min_m, in
 size_t archead_prepared_bytes(const archead_handle* h);
 archead_status archead_prepare(archead_handle* h, void* buf, size_t bytes, void* stream);
 
+/* Launch settings of a handle, for tuning runs and tests; the library
+ * reads no environment variables.  knob is one of:
+ *   ARCHEAD_LAUNCH_GEMV_BLOCKS_PER_CU  resident decode-GEMV workgroups per CU
+ *                                      (at most what the occupancy allows)
+ *   ARCHEAD_LAUNCH_GEMV_GRID           decode-GEMV head-streaming workgroups
+ *   ARCHEAD_LAUNCH_DEC_BLOCKS          consumer workgroups of the MFMA decode
+ *                                      kernel (cap)
+ *   ARCHEAD_LAUNCH_MID_BLOCKS          consumer workgroups of the
+ *                                      several-token kernel (cap)
+ *   ARCHEAD_LAUNCH_TILE_WAVES          waves per workgroup of the tiled
+ *                                      kernel: 4 or 8
+ *   ARCHEAD_LAUNCH_TILE_ROWS           token rows per tile of the 4-wave
+ *                                      layout: 64 or 128
+ *   ARCHEAD_LAUNCH_T_SPIN_LIMIT        polls of the in-launch stage-1
+ *                                      exchange before a wave computes t
+ *                                      itself (0: always computes it)
+ * value 0 (the spin limit: -1) restores the built-in choice, which the
+ * library otherwise makes per call from the head shape and M.  Every value
+ * accepted keeps every kernel correct: the grids are persistent with
+ * bounded indexes, and a consumer wave that outruns the producers computes
+ * t itself after the bounded wait.  ARCHEAD_E_INVALID_ARG for a NULL handle
+ * or pointer, an unknown knob, a negative size, a tile shape other than
+ * those above, or a spin limit below -1.  Same threading rule as
+ * archead_set_gemv_max_m; get returns the stored value (0 or -1 when
+ * built-in). */
+#define ARCHEAD_LAUNCH_GEMV_BLOCKS_PER_CU 0
+#define ARCHEAD_LAUNCH_GEMV_GRID 1
+#define ARCHEAD_LAUNCH_DEC_BLOCKS 2
+#define ARCHEAD_LAUNCH_MID_BLOCKS 3
+#define ARCHEAD_LAUNCH_TILE_WAVES 4
+#define ARCHEAD_LAUNCH_TILE_ROWS 5
+#define ARCHEAD_LAUNCH_T_SPIN_LIMIT 6
+#define ARCHEAD_LAUNCH_KNOBS 7
+archead_status archead_set_launch(archead_handle* h, int knob, int64_t value);
+archead_status archead_get_launch(const archead_handle* h, int knob, int64_t* value);
+
 /* Profiling hook: when start and stop are non-NULL hipEvent_t handles
  * (created by the caller on the handle's device), every later compute call
  * attaches `start` to the dispatch of the kernel that streams the packed head

@@ -22,6 +22,8 @@ F32, BF16, F16, I32, I64, I8, U8, I5 = range(8)
 INT4_V1 = 1
 OP_LOGITS, OP_LOGITS_CE, OP_ARGMAX, OP_TOPK, OP_FIDELITY = 0, 1, 2, 3, 4
 TOPK_MAX = 64
+(LAUNCH_GEMV_BLOCKS_PER_CU, LAUNCH_GEMV_GRID, LAUNCH_DEC_BLOCKS, LAUNCH_MID_BLOCKS,
+ LAUNCH_TILE_WAVES, LAUNCH_TILE_ROWS, LAUNCH_T_SPIN_LIMIT) = range(7)
 NOALLOC_SCRATCH_BYTES = 4 << 20   # ARCHEAD_NOALLOC_SCRATCH_BYTES of include/archead.h
 
 
@@ -116,6 +118,9 @@ _SIGS = {
                                              ctypes.POINTER(ctypes.c_int64)]),
     "archead_set_timing_events": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p,
                                                  ctypes.c_void_p]),
+    "archead_set_launch": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int, ctypes.c_int64]),
+    "archead_get_launch": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int,
+                                          ctypes.POINTER(ctypes.c_int64)]),
     "archead_prepared_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
     "archead_prepare": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
                                        ctypes.c_void_p]),
@@ -135,6 +140,7 @@ _SIGS = {
 HOST_SYMBOLS = ("archead_validate_desc", "archead_set_gemv_max_m", "archead_set_timing_events",
                 "archead_get_gemv_max_m", "archead_set_dec_range", "archead_get_dec_range",
                 "archead_set_mid_range", "archead_get_mid_range",
+                "archead_set_launch", "archead_get_launch",
                 "archead_packed_bytes", "archead_pack_int4", "archead_pack_int5",
                 "archead_unpack_int5",
                 "archead_unpack_int4", "archead_status_str", "archead_last_error")
@@ -391,6 +397,16 @@ class PackedHead:
 
     def set_mid_range(self, min_m: int, max_m: int):
         _check(self._lib.archead_set_mid_range(self.handle, min_m, max_m), self._lib)
+
+    def set_launch(self, knob: int, value: int):
+        """archead_set_launch: one of the LAUNCH_* settings (0, or -1 for
+        LAUNCH_T_SPIN_LIMIT, restores the built-in choice)."""
+        _check(self._lib.archead_set_launch(self.handle, knob, value), self._lib)
+
+    def get_launch(self, knob: int) -> int:
+        v = ctypes.c_int64()
+        _check(self._lib.archead_get_launch(self.handle, knob, ctypes.byref(v)), self._lib)
+        return v.value
 
     def force_path(self, path: str):
         """Route every M to one kernel: "dec" (MFMA decode), "mid" (several

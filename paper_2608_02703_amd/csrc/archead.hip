@@ -202,15 +202,16 @@ int64_t gemv_grid(const archead_handle* h, int tok, bool ce, bool topk) {
                                                      kBlock, lds) != hipSuccess ||
         nb <= 0)
       nb = 1;
-    // a few resident workgroups per CU stream best; ARCHEAD_GEMV_BLOCKS_PER_CU
-    // overrides the built-in choice (tuning only)
-    int want = kGemvBlocksPerCu;
-    if (const char* e = getenv("ARCHEAD_GEMV_BLOCKS_PER_CU")) want = atoi(e) > 0 ? atoi(e) : want;
+    // a few resident workgroups per CU stream best (a launch setting may
+    // choose another count)
+    const int64_t bpc = h->launch[ARCHEAD_LAUNCH_GEMV_BLOCKS_PER_CU].load(std::memory_order_relaxed);
+    const int want = bpc > 0 ? int(bpc) : kGemvBlocksPerCu;
     if (nb > want) nb = want;
     // every resident wave (measured faster than fewer waves with an even
     // split of the steps)
     cached = nb * h->n_cu;
-    if (const char* e = getenv("ARCHEAD_GEMV_GRID")) cached = atoi(e) > 0 ? atoi(e) : cached;
+    const int64_t grid = h->launch[ARCHEAD_LAUNCH_GEMV_GRID].load(std::memory_order_relaxed);
+    if (grid > 0) cached = int(grid);
     mh->grid_cache[slot].store(cached, std::memory_order_relaxed);
   }
   return cached < max_blocks ? cached : max_blocks;
@@ -228,7 +229,7 @@ DecGrid dec_grid(const archead_handle* h) {
   gr.n_units = (d.V + 15) / 16;
   int64_t cap = int64_t(h->n_cu) - gr.prod_blocks;
   if (cap < 1) cap = 1;
-  if (const char* e = getenv("ARCHEAD_DEC_BLOCKS")) cap = atoi(e) > 0 ? atoi(e) : cap;
+  if (const int64_t c = h->launch[ARCHEAD_LAUNCH_DEC_BLOCKS].load(std::memory_order_relaxed)) cap = c;
   const int64_t wmax = cap * kDecWaves;
   const int64_t rounds = (gr.n_units + wmax - 1) / wmax;
   gr.n_waves = (gr.n_units + rounds - 1) / rounds;
@@ -247,7 +248,7 @@ MidGrid mid_grid(const archead_handle* h) {
   gr.n_units = (d.V + 15) / 16;
   int64_t cap = int64_t(h->n_cu) - gr.prod_blocks;
   if (cap < 1) cap = 1;
-  if (const char* e = getenv("ARCHEAD_MID_BLOCKS")) cap = atoi(e) > 0 ? atoi(e) : cap;
+  if (const int64_t c = h->launch[ARCHEAD_LAUNCH_MID_BLOCKS].load(std::memory_order_relaxed)) cap = c;
   gr.cblocks = cap < gr.n_units ? cap : gr.n_units;
   return gr;
 }
@@ -560,7 +561,10 @@ Stage1Ops stage1_ops(const archead_handle* h, uint64_t* tst) {
   o.d = int(d.d);
   o.tst = reinterpret_cast<unsigned long long*>(tst);
   o.epoch = next_epoch();
-  o.spin_limit = h->t_spin_limit;
+  {
+    const int64_t sl = h->launch[ARCHEAD_LAUNCH_T_SPIN_LIMIT].load(std::memory_order_relaxed);
+    o.spin_limit = sl >= 0 ? int(sl) : kDefaultSpinLimit;
+  }
   return o;
 }
 
@@ -749,21 +753,20 @@ int tiled_tm(int64_t M) { return M <= 128 ? 128 : kTM; }
 // waves per CU at M = 16 .. 1024, where tile starts, LDS waits and the
 // epilogue would leave the matrix unit idle); above, 256-row tiles of 8
 // waves (equal at M = 4096, where the chip runs at its power limit).
-// ARCHEAD_MFMA_NW = 4 or 8 and ARCHEAD_MFMA_TM override the choice (tuning
-// only).
+// The launch settings ARCHEAD_LAUNCH_TILE_WAVES (4 or 8) and
+// ARCHEAD_LAUNCH_TILE_ROWS (64 or 128, with 4 waves) override the choice.
 constexpr int64_t kTiled64MaxM = 64;
 constexpr int64_t kTiledNw4MaxM = 1024;
 struct TiledShape { int tm, nw; };
-TiledShape tiled_shape(int64_t M) {
+TiledShape tiled_shape(const archead_handle* h, int64_t M) {
   TiledShape t = M <= kTiled64MaxM    ? TiledShape{64, 4}
                  : M <= kTiledNw4MaxM ? TiledShape{128, 4}
                                       : TiledShape{kTM, 8};
-  if (const char* e = getenv("ARCHEAD_MFMA_NW")) {
-    if (atoi(e) == 4) t = TiledShape{128, 4};
-    else if (atoi(e) == 8) t = TiledShape{tiled_tm(M), 8};
-  }
-  if (const char* e = getenv("ARCHEAD_MFMA_TM"))
-    if (t.nw == 4 && (atoi(e) == 64 || atoi(e) == 128)) t.tm = atoi(e);
+  const int64_t nw = h->launch[ARCHEAD_LAUNCH_TILE_WAVES].load(std::memory_order_relaxed);
+  const int64_t tm = h->launch[ARCHEAD_LAUNCH_TILE_ROWS].load(std::memory_order_relaxed);
+  if (nw == 4) t = TiledShape{128, 4};
+  else if (nw == 8) t = TiledShape{tiled_tm(M), 8};
+  if (t.nw == 4 && (tm == 64 || tm == 128)) t.tm = int(tm);
   return t;
 }
 
@@ -787,7 +790,7 @@ MfmaArgs mfma_args(const archead_handle* h, const void* x, int64_t M, int64_t ld
   a.nslot = int(d.d / d.g) + (d.r_c ? 1 : 0) + (d.r_r ? 1 : 0);
   a.nch_u = exp_chunks(d.r_c);
   a.nch = a.nch_u + exp_chunks(d.r_r);
-  const int tm = tiled_shape(M).tm;
+  const int tm = tiled_shape(h, M).tm;
   a.n_mt = (M + tm - 1) / tm;
   a.n_vt = (d.V + kTN - 1) / kTN;
   a.n_tiles = a.n_vt * a.n_mt;
@@ -799,7 +802,7 @@ archead_status launch_mfma(const archead_handle* h, MfmaArgs& a, bool ce, hipStr
   // byte ranges of one tile's buffers must stay below 2 GiB
   if (int64_t(kTM) * a.ldx * 2 >= (int64_t(1) << 31))
     return fail(ARCHEAD_E_UNSUPPORTED, "ldx too large for the many-token kernel");
-  const TiledShape ts = tiled_shape(a.M);
+  const TiledShape ts = tiled_shape(h, a.M);
   const void* fn = kern::mfma(ce, ts.tm, ts.nw);
   const int lds = ts.nw == 4 ? (ts.tm == 64 ? MGeomT<64, 4>::LDS : MGeomT<128, 4>::LDS)
                   : ts.tm == 128 ? MGeomT<128>::LDS : MGeom::LDS;
@@ -973,10 +976,8 @@ archead_status archead_create(const archead_desc* desc, const archead_ptrs* ptrs
     h->mid_min_m.store(r[2]);
     h->mid_max_m.store(r[3]);
   }
-  // polls of the stage-1 exchange before the fallback (ARCHEAD_T_SPIN_LIMIT
-  // overrides; 0 makes every value take the fallback, for its tests)
-  h->t_spin_limit = 1 << 16;
-  if (const char* e = getenv("ARCHEAD_T_SPIN_LIMIT")) h->t_spin_limit = atoi(e) >= 0 ? atoi(e) : h->t_spin_limit;
+  for (auto& k : h->launch) k.store(0);
+  h->launch[ARCHEAD_LAUNCH_T_SPIN_LIMIT].store(-1);
   for (auto& c : h->grid_cache) c.store(0);
   h->ev_start.store(nullptr);
   h->ev_stop.store(nullptr);

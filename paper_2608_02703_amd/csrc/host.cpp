@@ -295,6 +295,45 @@ archead_status archead_set_gemv_max_m(archead_handle* h, int64_t m) {
   return ARCHEAD_OK;
 }
 
+archead_status archead_set_launch(archead_handle* h, int knob, int64_t value) {
+  if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
+  switch (knob) {
+    case ARCHEAD_LAUNCH_GEMV_BLOCKS_PER_CU:
+    case ARCHEAD_LAUNCH_GEMV_GRID:
+    case ARCHEAD_LAUNCH_DEC_BLOCKS:
+    case ARCHEAD_LAUNCH_MID_BLOCKS:
+      if (value < 0 || value > (int64_t(1) << 30))
+        return fail(ARCHEAD_E_INVALID_ARG, "launch size must be in [0, 2^30]");
+      break;
+    case ARCHEAD_LAUNCH_TILE_WAVES:
+      if (value != 0 && value != 4 && value != 8)
+        return fail(ARCHEAD_E_INVALID_ARG, "tile waves must be 0, 4 or 8");
+      break;
+    case ARCHEAD_LAUNCH_TILE_ROWS:
+      if (value != 0 && value != 64 && value != 128)
+        return fail(ARCHEAD_E_INVALID_ARG, "tile rows must be 0, 64 or 128");
+      break;
+    case ARCHEAD_LAUNCH_T_SPIN_LIMIT:
+      if (value < -1 || value > (int64_t(1) << 30))
+        return fail(ARCHEAD_E_INVALID_ARG, "spin limit must be in [-1, 2^30]");
+      break;
+    default:
+      return fail(ARCHEAD_E_INVALID_ARG, "unknown launch knob");
+  }
+  h->launch[knob].store(value);
+  // GEMV grids are cached per kernel variant: recompute them
+  if (knob == ARCHEAD_LAUNCH_GEMV_BLOCKS_PER_CU || knob == ARCHEAD_LAUNCH_GEMV_GRID)
+    for (auto& c : h->grid_cache) c.store(0);
+  return ARCHEAD_OK;
+}
+
+archead_status archead_get_launch(const archead_handle* h, int knob, int64_t* value) {
+  if (!h || !value) return fail(ARCHEAD_E_INVALID_ARG, "NULL argument");
+  if (knob < 0 || knob >= ARCHEAD_LAUNCH_KNOBS) return fail(ARCHEAD_E_INVALID_ARG, "unknown launch knob");
+  *value = h->launch[knob].load();
+  return ARCHEAD_OK;
+}
+
 archead_status archead_set_timing_events(archead_handle* h, void* start, void* stop) {
   if (!h) return fail(ARCHEAD_E_INVALID_ARG, "handle is NULL");
   if ((start == nullptr) != (stop == nullptr))

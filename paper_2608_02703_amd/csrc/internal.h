@@ -18,7 +18,8 @@ struct archead_handle {
   std::atomic<int64_t> dec_max_m;   // (empty when max < min)
   std::atomic<int64_t> mid_min_m;   // M range of the several-token kernel
   std::atomic<int64_t> mid_max_m;
-  int t_spin_limit;       // polls of the in-launch stage-1 exchange before the fallback
+  // archead_set_launch values (0 = built-in; the spin limit -1 = built-in)
+  std::atomic<int64_t> launch[ARCHEAD_LAUNCH_KNOBS];
   // persistent-grid sizes found with the occupancy API, keyed by kernel
   // variant; 0 = not computed yet
   std::atomic<int> grid_cache[128];
@@ -36,6 +37,7 @@ constexpr int64_t kDefaultGemvMaxM = 15;  // largest M on the decode kernel (mea
 constexpr int64_t kDefaultDecMinM = 3;    // M range of the MFMA decode kernel (one or
 constexpr int64_t kDefaultDecMaxM = 32;   // two tokens stream faster through the GEMV)
 constexpr int64_t kDefaultMidMaxM = 32;   // largest M of the several-token kernel (one pass)
+constexpr int kDefaultSpinLimit = 1 << 16;   // polls of the stage-1 exchange before the fallback
 constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
 constexpr int kDecTok = 16;               // tokens per pass of the MFMA decode kernel
 constexpr int kDecWaves = 8;              // waves per workgroup of the MFMA decode kernel

@@ -183,7 +183,17 @@ def test_null_handle_calls(L):
     assert L.archead_set_dec_range(None, 2, 3) == ab.E_INVALID_ARG
     lo, hi = ctypes.c_int64(), ctypes.c_int64()
     assert L.archead_get_dec_range(None, ctypes.byref(lo), ctypes.byref(hi)) == ab.E_INVALID_ARG
+    assert L.archead_set_launch(None, ab.LAUNCH_GEMV_GRID, 4) == ab.E_INVALID_ARG
+    assert L.archead_get_launch(None, ab.LAUNCH_GEMV_GRID, ctypes.byref(lo)) == ab.E_INVALID_ARG
     L.archead_destroy(None)
+
+
+def test_launch_knob_numbers_match_header():
+    found = dict(re.findall(r"#define (ARCHEAD_LAUNCH_[A-Z0-9_]+) (\d+)", open(HEADER).read()))
+    assert int(found.pop("ARCHEAD_LAUNCH_KNOBS")) == 7
+    assert len(found) == 7
+    for name, v in found.items():
+        assert getattr(ab, name[len("ARCHEAD_"):]) == int(v), name
 
 
 def test_host_only_build_agrees(tmp_path):

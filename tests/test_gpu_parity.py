@@ -345,17 +345,14 @@ def test_stage1_fallback_matches(path):
     """With the in-launch stage-1 exchange's wait bound set to zero polls,
     every consumer wave computes its t values itself; the logits and CE
     still match the oracle within tolerance (both decode kernels)."""
-    import os
     from paper_2608_02703_amd import PackedHead
     h = cached_head("tiny")
     x = make_x("tiny", 8)
     y = make_targets("tiny", 8)
     ref = cached_oracle_logits("tiny", 8)
-    os.environ["ARCHEAD_T_SPIN_LIMIT"] = "0"
-    try:
-        ph = PackedHead.from_arrays(h)
-    finally:
-        del os.environ["ARCHEAD_T_SPIN_LIMIT"]
+    from paper_2608_02703_amd import archead as ab
+    ph = PackedHead.from_arrays(h)
+    ph.set_launch(ab.LAUNCH_T_SPIN_LIMIT, 0)
     ph.force_path(path)
     say(f"{path} stage-1 fallback: tiny M=8")
     lg = gpu_logits(ph, x)
@@ -363,6 +360,42 @@ def test_stage1_fallback_matches(path):
     ce, _ = gpu_ce(ph, x, y)
     assert_ce_close(ce, ohead.cross_entropy(ref, y), what="fallback CE")
     ph.close()
+
+
+def test_launch_settings():
+    """archead_set_launch: small persistent grids on each decode kernel still
+    match the oracle; values outside the documented sets are rejected and
+    leave the setting unchanged; 0 restores the built-in choice."""
+    from paper_2608_02703_amd import ArcheadError, PackedHead
+    from paper_2608_02703_amd import archead as ab
+    h = cached_head("tiny")
+    ph = PackedHead.from_arrays(h)
+    try:
+        for path, knob, value, M in (("gemv", ab.LAUNCH_GEMV_GRID, 3, 1),
+                                     ("gemv", ab.LAUNCH_GEMV_BLOCKS_PER_CU, 1, 2),
+                                     ("dec", ab.LAUNCH_DEC_BLOCKS, 2, 8),
+                                     ("mid", ab.LAUNCH_MID_BLOCKS, 3, 8)):
+            ph.set_launch(knob, value)
+            assert ph.get_launch(knob) == value
+            ph.force_path(path)
+            say(f"launch setting {knob}={value} on {path}: tiny M={M}")
+            x = make_x("tiny", 8)[:M]
+            assert_logits_close(gpu_logits(ph, x), cached_oracle_logits("tiny", 8)[:M],
+                                what=f"{path} with launch setting {knob}={value}")
+            ph.set_launch(knob, 0)
+            assert ph.get_launch(knob) == 0
+        assert ph.get_launch(ab.LAUNCH_T_SPIN_LIMIT) == -1
+        for knob, value in ((ab.LAUNCH_TILE_WAVES, 5), (ab.LAUNCH_TILE_ROWS, 256),
+                            (ab.LAUNCH_TILE_ROWS, 32), (ab.LAUNCH_GEMV_GRID, -1),
+                            (ab.LAUNCH_DEC_BLOCKS, 1 << 31), (ab.LAUNCH_T_SPIN_LIMIT, -2),
+                            (ab.LAUNCH_T_SPIN_LIMIT + 1, 0), (-1, 0)):
+            with pytest.raises(ArcheadError) as e:
+                ph.set_launch(knob, value)
+            assert e.value.status == ab.E_INVALID_ARG
+            if 0 <= knob <= ab.LAUNCH_T_SPIN_LIMIT:
+                assert ph.get_launch(knob) == (-1 if knob == ab.LAUNCH_T_SPIN_LIMIT else 0)
+    finally:
+        ph.close()
 
 
 @pytest.mark.parametrize("V,d,g,M,rc,rr", [(1000, 512, 64, 17, 16, 8), (777, 256, 32, 5, 20, 4),

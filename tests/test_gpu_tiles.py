@@ -1,7 +1,8 @@
 """GPU parity of every tile layout of the many-token kernel, through the C
 ABI: 64-row tiles of 4 waves (three workgroups per CU), 128-row tiles of 4
 waves (two per CU), 128- and 256-row tiles of 8 waves (one per CU).  The
-library picks one by M; ARCHEAD_MFMA_TM / ARCHEAD_MFMA_NW force each here.
+library picks one by M; the launch settings ARCHEAD_LAUNCH_TILE_WAVES /
+ARCHEAD_LAUNCH_TILE_ROWS force each here.
 
 Each layout runs the same cases against the oracle: logits (fp32, a row
 stride wider than the row, nothing written past V), CE, the fused argmax and
@@ -13,7 +14,6 @@ agree with each other to the fp32 rounding of their shared arithmetic
 """
 from __future__ import annotations
 
-import os
 
 import numpy as np
 import pytest
@@ -27,9 +27,7 @@ pytestmark = pytest.mark.gpu
 
 torch = pytest.importorskip("torch")
 
-LAYOUTS = [("64x4", {"ARCHEAD_MFMA_NW": "4", "ARCHEAD_MFMA_TM": "64"}),
-           ("128x4", {"ARCHEAD_MFMA_NW": "4", "ARCHEAD_MFMA_TM": "128"}),
-           ("8-wave", {"ARCHEAD_MFMA_NW": "8"})]
+LAYOUTS = [("64x4", (4, 64)), ("128x4", (4, 128)), ("8-wave", (8, 0))]
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -40,10 +38,12 @@ def _gpu():
     torch.cuda.synchronize()
 
 
-def _set(env):
-    for k in ("ARCHEAD_MFMA_NW", "ARCHEAD_MFMA_TM"):
-        os.environ.pop(k, None)
-    os.environ.update(env)
+def _set(ph, layout):
+    from paper_2608_02703_amd import archead as ab
+    waves, rows = layout
+    ph.set_launch(ab.LAUNCH_TILE_WAVES, waves)
+    ph.set_launch(ab.LAUNCH_TILE_ROWS, rows)
+    assert (ph.get_launch(ab.LAUNCH_TILE_WAVES), ph.get_launch(ab.LAUNCH_TILE_ROWS)) == layout
 
 
 @pytest.mark.parametrize("scales", ["f16", "u8"])
@@ -57,8 +57,8 @@ def test_tile_layouts_match_oracle(scales):
     ref_all = ohead.logits(h, x_all)
     got = {}
     try:
-        for name, env in LAYOUTS:
-            _set(env)
+        for name, layout in LAYOUTS:
+            _set(ph, layout)
             for M in (1, 17, 64, 65, 130, 300):
                 say(f"tile layout {name} {scales}: M={M}")
                 x, ref = x_all[:M], ref_all[:M]
@@ -83,7 +83,6 @@ def test_tile_layouts_match_oracle(scales):
                 bits = bits.view(torch.int16).cpu().numpy().view(np.uint16)
                 assert_bf16_output(bits, lg, ref, f"{name} M={M} bf16")
     finally:
-        _set({})
         ph.close()
     for M in (1, 17, 64, 65, 130, 300):
         base = got[("64x4", M)]
