@@ -738,11 +738,16 @@ def main():
 
     copy = copy_bandwidth()
     log(f"device copy: {copy['gbs_read_plus_write']} GB/s (read + write)")
-    ms1, kern1_mean, kern1 = res[1]
+    ms1, _, kern1 = res[1]
     value = pbytes / ms1 / 1e6          # GB/s
     alg = decode_algorithmic_bytes(pbytes, h, 1)
     kname = f"k_gemv<1, {lanes_per_row(h)}, false, false, 0, false>"
-    achieved = alg / kern1 / 1e6
+    # a decode step at M = 1 is one launch of the head kernel, so the HIP
+    # events around the unmarked timed loop (on the stream the kernel is
+    # launched on) give its average launch duration, launch gaps included;
+    # events attached to every dispatch (the separate marked pass) slow the
+    # kernel on some boxes and are reported beside it only
+    achieved = alg / ms1 / 1e6
     out = {
         "metric": METRIC,
         "value": round(value, 1),
@@ -765,10 +770,11 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
                      "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
                      "traffic": measured_traffic(), "kernel": kname,
-                     "kernel_us_median": round(kern1 * 1e3, 2),
-                     "kernel_us_mean": round(kern1_mean * 1e3, 2), "algorithmic_bytes": alg,
-                     "timing": "HIP events attached to the kernel's dispatch, median of 100 "
-                               "dispatches after the timed loop"},
+                     "kernel_us_mean": round(ms1 * 1e3, 2), "algorithmic_bytes": alg,
+                     "timing": f"HIP events on the launch stream around the timed loop of "
+                               f"{args.steps} steps, one launch of the kernel per step "
+                               f"(per-launch average, launch gaps included)",
+                     "marked_pass_kernel_us_median": round(kern1 * 1e3, 2)},
         "step_us_percentiles": {k: round(v * 1e3, 2) for k, v in pcts.items()},
         "gpu_clock": clk.summary(),
         "hbm_copy": copy,
