@@ -297,6 +297,16 @@ PrepLayout prep_layout(const archead_handle* h) {
 }
 
 // Whether a top-k call of M tokens runs fused in the single-token GEMV.
+// The merge of per-partial top-k lists: k rounds of a workgroup-wide best
+// when every thread holds at most kTopKMergeC candidates, else the scan
+// (floor, per-wave lists, wave-ordered merge).
+static hipError_t launch_topk_merge(int64_t n_part, int k, int64_t rows, void** args,
+                                    hipStream_t s) {
+  if (n_part * k <= int64_t(kTopKMergeBlock) * kTopKMergeC)
+    return hipLaunchKernel(kern::topk_merge(), dim3(unsigned(rows)), dim3(kTopKMergeBlock), args, 0, s);
+  return hipLaunchKernel(kern::topk_merge_scan(), dim3(unsigned(rows)), dim3(kBlock), args, 0, s);
+}
+
 bool topk_fused(const archead_handle* h, int64_t M) {
   return M == 1 && choose_path(h, 1) == Path::kGemv &&
          kern::gemv_topk(lanes_per_row(h->desc), h->desc.scale_dtype == ARCHEAD_U8,
@@ -1172,7 +1182,7 @@ archead_status archead_logits_topk(const archead_handle* h, const void* x, int64
     st = launch_gemv_passes(h, a, 1, false, np, s, true);
     if (st != ARCHEAD_OK) return st;
     void* margs[] = {&pv, &pi, &np, &k, &vals, &idx, &ldk};
-    e = hipLaunchKernel(kern::topk_merge(), dim3(1), dim3(kBlock), margs, 0, s);
+    e = launch_topk_merge(np, k, 1, margs, s);
     return e == hipSuccess ? ARCHEAD_OK : hip_fail(e, "top-k merge launch");
   }
   const int64_t V = h->desc.V;
@@ -1193,7 +1203,7 @@ archead_status archead_logits_topk(const archead_handle* h, const void* x, int64
     float* vo = vals ? vals + m0 * ldk : nullptr;
     int64_t* io = idx + m0 * ldk;
     void* margs[] = {&pv, &pi, &np, &k, &vo, &io, &ldk};
-    e = hipLaunchKernel(kern::topk_merge(), dim3(unsigned(mc)), dim3(kBlock), margs, 0, s);
+    e = launch_topk_merge(np, k, mc, margs, s);
     if (e != hipSuccess) return hip_fail(e, "top-k merge launch");
   }
   return ARCHEAD_OK;

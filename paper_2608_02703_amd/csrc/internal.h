@@ -47,6 +47,8 @@ constexpr int kMidWindow = 256;           // elements of d per x window of that 
 constexpr int kMidWaveCount = 8;          // its waves per workgroup
 constexpr int kTopKMaxK = 64;             // largest k of archead_logits_topk (lanes of a wave)
 constexpr int64_t kTopKChunk = 256;       // tokens per chunk of the unfused top-k
+constexpr int kTopKMergeBlock = 1024;     // threads of the round-based top-k merge workgroup
+constexpr int kTopKMergeC = 8;            // candidates per thread of that merge (else the scan merge)
 
 archead_status fail(archead_status s, const char* fmt, ...);
 void clear_error();

@@ -89,11 +89,11 @@ __global__ __launch_bounds__(kBlock) void k_topk_rows(const float* logits, int64
   }
 }
 
-// Per token m (grid M): the k best of its n_part partial lists of k pairs
-// (scanned as one flat array of n_part * k candidates), out to
+// Per token m (grid M, workgroups of kBlock): the k best of its n_part partial
+// lists of k pairs (scanned as one flat array of n_part * k candidates), out to
 // vals[m * ldk + j] (may be null) and idx[m * ldk + j], j < k; a slot no
 // value reached (fewer than k non-NaN logits) gets (-inf, -1).
-__global__ __launch_bounds__(kBlock) void k_topk_merge(const float* pv, const int* pi,
+__global__ __launch_bounds__(kBlock) void k_topk_merge_scan(const float* pv, const int* pi,
                                                        int64_t n_part, int k, float* vals,
                                                        int64_t* idx, int64_t ldk) {
   __shared__ float sv[kWaves * 64];
@@ -136,6 +136,97 @@ __global__ __launch_bounds__(kBlock) void k_topk_merge(const float* pv, const in
   }
 }
 
+// Per token m (grid M, workgroups of kMergeBlock), for at most kMergeBlock *
+// kMergeC candidates: the same result in k rounds.  Each thread holds up to
+// kMergeC candidates and its best one; a round finds the best of the
+// workgroup (DPP within rows of 16 lanes, then the four rows of the wave,
+// then the waves through LDS), writes it out, and its owner (indices are
+// distinct across the partial lists) drops it and takes its next best.  The
+// cost is k rounds, whatever the values.
+constexpr int kMergeBlock = 1024, kMergeWaves = kMergeBlock / 64, kMergeC = 8;
+static_assert(kMergeBlock == archead::kTopKMergeBlock && kMergeC == archead::kTopKMergeC,
+              "host and kernel agree on the merge workgroup");
+
+__device__ __forceinline__ void tk_pick(float& bv, int& bi, float ov, int oi) {
+  const bool t = tk_better(ov, oi, bv, bi);
+  bv = t ? ov : bv;
+  bi = t ? oi : bi;
+}
+template <int CTRL>
+__device__ __forceinline__ void tk_pick_dpp(float& v, int& i) {
+  const float ov = dpp_swap<CTRL>(v);
+  const int oi = __builtin_amdgcn_update_dpp(0, i, CTRL, 0xF, 0xF, false);
+  tk_pick(v, i, ov, oi);
+}
+// the best pair of each row of 16 lanes, in every lane of the row
+__device__ __forceinline__ void tk_row16_best(float& v, int& i) {
+  tk_pick_dpp<0xB1>(v, i);
+  tk_pick_dpp<0x4E>(v, i);
+  tk_pick_dpp<0x141>(v, i);
+  tk_pick_dpp<0x140>(v, i);
+}
+
+__global__ __launch_bounds__(kMergeBlock) void k_topk_merge(const float* pv, const int* pi,
+                                                            int64_t n_part, int k, float* vals,
+                                                            int64_t* idx, int64_t ldk) {
+  __shared__ float wv[2][kMergeWaves];
+  __shared__ int wi[2][kMergeWaves];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wid = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int64_t m = blockIdx.x;
+  const int64_t n = n_part * k;
+  const float* v = pv + m * n;
+  const int* ix = pi + m * n;
+  float cv[kMergeC];
+  int ci[kMergeC];
+#pragma unroll
+  for (int u = 0; u < kMergeC; ++u) {
+    const int64_t j = int64_t(u) * kMergeBlock + tid;
+    cv[u] = j < n ? v[j] : -INFINITY;
+    ci[u] = j < n ? ix[j] : kNoIdx;
+  }
+  float tv = -INFINITY;
+  int ti = kNoIdx;
+#pragma unroll
+  for (int u = 0; u < kMergeC; ++u) tk_pick(tv, ti, cv[u], ci[u]);
+  for (int r = 0; r < k; ++r) {
+    float bv = tv;
+    int bi = ti;
+    tk_row16_best(bv, bi);
+    float gv = rlane_f(bv, 0);
+    int gi = __builtin_amdgcn_readlane(bi, 0);
+#pragma unroll
+    for (int row = 1; row < 4; ++row)
+      tk_pick(gv, gi, rlane_f(bv, 16 * row), __builtin_amdgcn_readlane(bi, 16 * row));
+    if (lane == 0) {
+      wv[r & 1][wid] = gv;
+      wi[r & 1][wid] = gi;
+    }
+    __syncthreads();
+    gv = lane < kMergeWaves ? wv[r & 1][lane] : -INFINITY;
+    gi = lane < kMergeWaves ? wi[r & 1][lane] : kNoIdx;
+    tk_row16_best(gv, gi);
+    gv = rlane_f(gv, 0);
+    gi = __builtin_amdgcn_readlane(gi, 0);
+    if (tid == 0) {
+      if (vals) vals[m * ldk + r] = gv;
+      idx[m * ldk + r] = gi == kNoIdx ? int64_t(-1) : int64_t(gi);
+    }
+    if (gi != kNoIdx && ti == gi) {
+#pragma unroll
+      for (int u = 0; u < kMergeC; ++u) {
+        const bool hit = ci[u] == gi;
+        cv[u] = hit ? -INFINITY : cv[u];
+        ci[u] = hit ? kNoIdx : ci[u];
+      }
+      tv = -INFINITY;
+      ti = kNoIdx;
+#pragma unroll
+      for (int u = 0; u < kMergeC; ++u) tk_pick(tv, ti, cv[u], ci[u]);
+    }
+  }
+}
+
 }  // namespace
 
 namespace archead {
@@ -149,6 +240,7 @@ const void* gemv_topk(int lpr, bool sc8, int gen) {
 
 const void* topk_rows() { return reinterpret_cast<const void*>(k_topk_rows); }
 const void* topk_merge() { return reinterpret_cast<const void*>(k_topk_merge); }
+const void* topk_merge_scan() { return reinterpret_cast<const void*>(k_topk_merge_scan); }
 
 }  // namespace kern
 }  // namespace archead
