@@ -318,6 +318,44 @@ __device__ __forceinline__ uint32_t fcodes4(__amdgpu_buffer_rsrc_t r, int row, i
   }
 }
 
+// fcodes4 in two halves, so the loads stay in flight until the codes are
+// used: fcodes4_fetch requests the two aligned words, fcodes4_decode joins
+// them later (int8 codes: sh = the byte offset of the first code, (row + k0)
+// & 3, which the caller recomputes from the row).
+struct RawCodes4 {
+  uint32_t w0, w1;
+};
+template <bool U5>
+__device__ __forceinline__ RawCodes4 fcodes4_fetch(__amdgpu_buffer_rsrc_t r, int row, int k0) {
+  RawCodes4 c;
+  if constexpr (U5) {
+    const int w = k0 / 6;
+    c.w0 = __builtin_amdgcn_raw_buffer_load_b32(r, row + 4 * w, 0, 0);
+    c.w1 = __builtin_amdgcn_raw_buffer_load_b32(r, row + 4 * w + 4, 0, 0);
+  } else {
+    const int al = (row + k0) & ~3;
+    c.w0 = __builtin_amdgcn_raw_buffer_load_b32(r, al, 0, 0);
+    c.w1 = __builtin_amdgcn_raw_buffer_load_b32(r, al + 4, 0, 0);
+  }
+  return c;
+}
+template <bool U5>
+__device__ __forceinline__ uint32_t fcodes4_decode(const RawCodes4& c, int k0, uint32_t sh) {
+  if constexpr (U5) {
+    const int w = k0 / 6;
+    uint32_t o = 0u;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int j = k0 + i - 6 * w;
+      const int v = j < 6 ? i5_field(c.w0, j) : i5_field(c.w1, j - 6);
+      o |= (uint32_t(v) & 0xffu) << (8 * i);
+    }
+    return o;
+  } else {
+    return __builtin_amdgcn_alignbyte(c.w1, c.w0, sh);
+  }
+}
+
 // code k of a row (rowp: its first byte), int8 or ARCHEAD_I5
 __device__ __forceinline__ int fcode1(const uint8_t* rowp, int k, bool u5) {
   if (u5) return i5_field(reinterpret_cast<const uint32_t*>(rowp)[k / 6], k % 6);

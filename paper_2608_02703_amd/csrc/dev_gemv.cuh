@@ -128,7 +128,8 @@ __device__ __forceinline__ int row_of_lane(int lane) {
 // r_c and r_r are multiples of 4 and (r_c + r_r) / 4 <= KD * LPR.
 template <int RB, int KD>
 struct ExpOps {
-  uint32_t c[RB][KD];   // four int8 codes
+  uint32_t c[RB][KD];   // four int8 codes (general reads: the raw words, decoded when applied)
+  RawCodes4 raw[RB][KD];
   uint16_t rsc[RB];     // fp16 row scale of 8-bit residual scale codes (unused otherwise)
   uint16_t s[RB][KD];   // fp16 bit pattern of the row scale (kept 16-bit: no extension op right after the load)
 };
@@ -141,9 +142,14 @@ struct ExpLanes {
 // acc += scale * (codes . t) over the lane's dwords of each row.  t is held
 // per token as [U_c part | A_w part], each part padded with zeros to a
 // multiple of 4 dimensions: R4 dwords of codes per row, Rp = 4 R4 values.
-template <int TOK, int RB, int KD, int LPR>
+// General reads (GEN > 0): the codes come as raw words; row v0 + rb SEG's
+// int8 codes start at byte offset (v cu_st) & 3 (U_c) or (v ca_st) & 3 (A_w)
+// of their aligned word (k0 is a multiple of 4).
+template <int TOK, int RB, int KD, int LPR, int GEN = 0>
 __device__ __forceinline__ void apply_expansion(float (&acc)[RB][TOK], const ExpOps<RB, KD>& e,
-                                                const float* st, int R4, int sl) {
+                                                const float* st, int R4, int sl, int rc4 = 0,
+                                                int64_t v0 = 0, int seg_rows = 0,
+                                                int64_t cu_st = 0, int64_t ca_st = 0) {
   const int Rp = 4 * R4;
 #pragma unroll
   for (int kd = 0; kd < KD; ++kd) {
@@ -155,7 +161,16 @@ __device__ __forceinline__ void apply_expansion(float (&acc)[RB][TOK], const Exp
       const float4 t4 = *reinterpret_cast<const float4*>(st + tt * Rp + 4 * qq);
 #pragma unroll
       for (int rb = 0; rb < RB; ++rb) {
-        const uint32_t u = e.c[rb][kd];
+        uint32_t u;
+        if constexpr (GEN > 0) {
+          const uint32_t v = uint32_t(v0 + int64_t(rb) * seg_rows);
+          const bool isu = qq < rc4;
+          const uint32_t sh = (v * uint32_t(isu ? cu_st : ca_st)) & 3u;
+          u = isu ? fcodes4_decode<GEN == 2>(e.raw[rb][kd], 4 * qq, sh)
+                  : fcodes4_decode<false>(e.raw[rb][kd], 4 * (qq - rc4), sh);
+        } else {
+          u = e.c[rb][kd];
+        }
         float du = float(int8_t(u)) * t4.x;
         du = fmaf(float(int8_t(u >> 8)), t4.y, du);
         du = fmaf(float(int8_t(u >> 16)), t4.z, du);
@@ -488,8 +503,10 @@ void k_gemv(GemvArgs a) {
           const int64_t v = v0 + rb * SEG;
           const uint16_t* sp = isu ? a.su + v * su_st : a.sa + v * sa_st;
           if constexpr (GEN > 0) {
-            e.c[rb][kd] = isu ? fcodes4<GEN == 2>(rcu, int(v * cu_st), 4 * q)
-                              : fcodes4<false>(rca, int(v * ca_st), 4 * (q - rc4));
+            // the words only: they are joined when the expansion is applied,
+            // so the loads stay in flight through the next step
+            e.raw[rb][kd] = isu ? fcodes4_fetch<GEN == 2>(rcu, int(v * cu_st), 4 * q)
+                                : fcodes4_fetch<false>(rca, int(v * ca_st), 4 * (q - rc4));
           } else {
             const int8_t* cb = isu ? a.cu + 4 * q + v * cu_st : a.ca + 4 * (q - rc4) + v * ca_st;
             e.c[rb][kd] = *reinterpret_cast<const uint32_t*>(cb);
@@ -563,7 +580,8 @@ void k_gemv(GemvArgs a) {
             for (int tt = 0; tt < TOK; ++tt) acc[rb][tt] *= f;
           }
         }
-        apply_expansion<TOK, RB, KD, LPR>(acc, e, st, Rq, sl);
+        apply_expansion<TOK, RB, KD, LPR, GEN>(acc, e, st, Rq, sl, rc4, cstep * WR + seg, SEG,
+                                               cu_st, ca_st);
         load_exp(more ? nstep : cstep, e);
         gemv_epilogue<TOK, LPR, RB, CE, false, TK>(acc, a, cstep * WR, uint32_t(WR - 1), seg, sl,
                                                lane, my_row, writer, st, ce);
