@@ -39,6 +39,9 @@ __device__ __forceinline__ uint4 load_stream16(const __attribute__((address_spac
 
 constexpr int kBlock = 256;          // 4 waves of 64
 constexpr int kWaves = kBlock / 64;
+// A GEMV step is 8 rows per lane segment with 1 iteration of loads in flight
+// (steps of 2 or 4 rows with the same bytes in flight measured slower: the
+// shorter last round of the grid does not repay the per-step work).
 #ifndef ARCHEAD_ROWS_PER_STEP
 #define ARCHEAD_ROWS_PER_STEP 8
 #endif
@@ -501,6 +504,16 @@ __device__ __forceinline__ bf16x8_t int8x8_to_bf16(uint32_t w0, uint32_t w1) {
 }
 
 // ------------------------------------------------------------ top-k lists
+// Calls f(integral_constant<J>) for J = I .. N-1 until one returns true.
+template <int I, int N, typename F>
+__device__ __forceinline__ bool unroll_until(F& f) {
+  if constexpr (I < N) {
+    if (f(std::integral_constant<int, I>{})) return true;
+    return unroll_until<I + 1, N>(f);
+  }
+  return false;
+}
+
 // A wave keeps the k best (value, index) pairs it has seen as one sorted
 // list spread over its lanes: lane j < k holds the j-th best, in the order
 // "larger value first, equal values by smaller index" (the order of the

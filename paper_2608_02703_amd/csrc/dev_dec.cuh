@@ -89,16 +89,6 @@ struct DecArgs {
   float* tgt_logit;
 };
 
-// Calls f(integral_constant<J>) for J = I .. N-1 until one returns true.
-template <int I, int N, typename F>
-__device__ __forceinline__ bool unroll_until(F& f) {
-  if constexpr (I < N) {
-    if (f(std::integral_constant<int, I>{})) return true;
-    return unroll_until<I + 1, N>(f);
-  }
-  return false;
-}
-
 // GEN: 0 = the factor codes are read as aligned 8-byte pieces (int8 codes,
 // ranks that are multiples of 4); 1 = through fcodes8 (int8 codes, any
 // rank); 2 = the same with the core-left codes in ARCHEAD_I5 words.
@@ -118,11 +108,24 @@ void k_dec(DecArgs a) {
   // ---- prologue: x rows of the pass -> LDS, offset biases, zero t padding
   // (every wave of the workgroup calls this once)
   auto prologue = [&]() {
-    const int x16 = d / 8;
-    for (int e = tid; e < M * x16; e += kDBlock) {
-      const int tt = e / x16, u = e - tt * x16;
-      *reinterpret_cast<__attribute__((address_space(3))) u32x4_t*>(L + tt * a.xstr + 16 * u) =
-          *reinterpret_cast<const u32x4_t*>(a.x + (a.tok0 + tt) * a.ldx + 8 * u);
+    // x: each thread's 16-byte pieces are requested in batches of 8 before
+    // any is stored, so the copy costs one memory latency per batch
+    const int x16 = d / 8, nx = M * x16;
+    for (int e0 = 0; e0 < nx; e0 += 8 * kDBlock) {
+      u32x4_t v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e0j = e0 + j * kDBlock + tid;
+        const int e = e0j < nx ? e0j : nx - 1;   // past the end: a valid piece, not stored
+        const int tt = e / x16, u = e - tt * x16;
+        v[j] = *reinterpret_cast<const u32x4_t*>(a.x + (a.tok0 + tt) * a.ldx + 8 * u);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int e = e0 + j * kDBlock + tid;
+        const int tt = e / x16, u = e - tt * x16;
+        if (e < nx) *reinterpret_cast<__attribute__((address_space(3))) u32x4_t*>(L + tt * a.xstr + 16 * u) = v[j];
+      }
     }
     __syncthreads();
     auto* sb = reinterpret_cast<__attribute__((address_space(3))) float*>(L + a.off_bias);
@@ -131,10 +134,16 @@ void k_dec(DecArgs a) {
       float s = 0.f;
       if (tt < M) {
         const lds_u8* p = L + tt * a.xstr + 2 * G * g;
-        for (int i = 0; i < g / 8; ++i) {
-          const u32x4_t u = lds_load<u32x4_t>(p + 16 * i);
-          s += bf16_lo(u.x) + bf16_hi(u.x) + bf16_lo(u.y) + bf16_hi(u.y) + bf16_lo(u.z) +
-               bf16_hi(u.z) + bf16_lo(u.w) + bf16_hi(u.w);
+        // four pieces per round, requested together
+        for (int i = 0; i < g / 8; i += 4) {
+          u32x4_t u[4];
+#pragma unroll
+          for (int j = 0; j < 4; ++j) u[j] = lds_load<u32x4_t>(p + 16 * (i + j < g / 8 ? i + j : i));
+#pragma unroll
+          for (int j = 0; j < 4; ++j)
+            if (i + j < g / 8)
+              s += bf16_lo(u[j].x) + bf16_hi(u[j].x) + bf16_lo(u[j].y) + bf16_hi(u[j].y) +
+                   bf16_lo(u[j].z) + bf16_hi(u[j].z) + bf16_lo(u[j].w) + bf16_hi(u[j].w);
         }
       }
       sb[e] = -float(archead::kInt4Bias) * s;

@@ -9,8 +9,8 @@ namespace {
 // Lanes are split into segments of LPR lanes; a segment owns one vocabulary
 // row at a time and walks along d in 16-byte chunks (32 codes), LPR chunks
 // per iteration, so each segment load is LPR * 16 contiguous bytes.  A wave
-// step covers kRowsPerStep rows per segment (WR rows in all).  Waves get
-// contiguous, balanced ranges of steps (persistent grid).  x, the chunk
+// step covers kRowsPerStep rows per segment (WR rows in all); steps are dealt
+// out grid-stride over a persistent grid of every resident wave.  x, the chunk
 // biases and t sit in LDS.  Step bases are wave-uniform (scalar registers);
 // per-lane offsets are 32-bit and computed once per step.  Rows past V (the
 // last step only) are clamped to row V-1 for loading and never stored.
@@ -350,10 +350,24 @@ void k_gemv(GemvArgs a) {
   // the chunk); every wave of the workgroup calls this once
   auto prologue = [&]() {
     const int x8n = d / 8;  // 16-byte units per token: unit u = chunk u/4, part u%4
-    for (int i = threadIdx.x; i < TOK * x8n; i += kBlock) {
-      const int tt = i / x8n, u = i - tt * x8n;
-      reinterpret_cast<uint4*>(sx)[(tt * 4 + (u & 3)) * C + (u >> 2)] =
-          *reinterpret_cast<const uint4*>(a.x + (a.tok0 + tt) * a.ldx + u * 8);
+    // each thread's units are requested in batches of 8 before any is
+    // stored, so the copy costs one memory latency per batch
+    const int nx = TOK * x8n;
+    for (int i0 = 0; i0 < nx; i0 += 8 * kBlock) {
+      uint4 v[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i0j = i0 + j * kBlock + int(threadIdx.x);
+        const int i = i0j < nx ? i0j : nx - 1;   // past the end: a valid unit, not stored
+        const int tt = i / x8n, u = i - tt * x8n;
+        v[j] = *reinterpret_cast<const uint4*>(a.x + (a.tok0 + tt) * a.ldx + u * 8);
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int i = i0 + j * kBlock + int(threadIdx.x);
+        const int tt = i / x8n, u = i - tt * x8n;
+        if (i < nx) reinterpret_cast<uint4*>(sx)[(tt * 4 + (u & 3)) * C + (u >> 2)] = v[j];
+      }
     }
     __syncthreads();
     for (int i = threadIdx.x; i < TOK * C; i += kBlock) {
@@ -590,20 +604,14 @@ void k_gemv(GemvArgs a) {
       cit = nit;
       done = !more;
     };
-    while (gw < full_steps) {
-      body(std::integral_constant<int, 0>{});
-      if (done) break;
-      body(std::integral_constant<int, 1>{});
-      if (done) break;
-      if constexpr (NB > 2) {
-        body(std::integral_constant<int, 2 % NB>{});
-        if (done) break;
+    // one pass of the loop takes every ring slot once, in order
+    auto body_done = [&](auto J) {
+      body(J);
+      return done;
+    };
+    if (gw < full_steps)
+      while (!unroll_until<0, NB>(body_done)) {
       }
-      if constexpr (NB > 3) {
-        body(std::integral_constant<int, 3 % NB>{});
-        if (done) break;
-      }
-    }
   }
 
   // ---- steps not taken above: the partial last step (rows past V clamped
