@@ -115,15 +115,29 @@ bool mid_supported(const archead_desc& d) {
   return mid_lds(d).total <= kLdsBytes;
 }
 
+// Two tokens: the GEMV's cost grows about 1.3x from one token to two on
+// every measured head, the MFMA decode kernel's not at all, so two tokens
+// take the MFMA decode kernel where its one-token cost is within that
+// margin: rows of at least 4096 (its fixed work per 16-row unit spread over
+// more bytes) and ranks of at most 64 (the 2-chunk expansion variant).
+// Measured at M = 2: Qwen shape 68.6 against 76.7 us on the GEMV; Gemma
+// shape (d = 2560) 88.5 against 86.6; 128k head (ranks 128 / 64) 137.8
+// against 128.9.
+static int64_t dec_min_m(const archead_desc& d) {
+  return d.d >= 4096 && d.r_c <= 64 && d.r_r <= 64 ? 2 : kDefaultDecMinM;
+}
+
 void default_ranges(const archead_desc& d, int64_t (&r)[4]) {
   const int tpp = dec_tokens_per_pass(d);
   if (mid_supported(d) && tpp > 0) {
-    r[0] = kDefaultDecMinM;
+    r[0] = dec_min_m(d);
     r[1] = tpp;
     r[2] = tpp + 1;
-    r[3] = kDefaultMidMaxM;
+    // at d >= 8192 the tiled kernel overtakes it from 24 tokens on (128k
+    // head: 198 / 224 us at M = 24 / 32 against 201 / 202 tiled)
+    r[3] = d.d >= 8192 ? 24 : kDefaultMidMaxM;
   } else {
-    r[0] = kDefaultDecMinM;
+    r[0] = dec_min_m(d);
     r[1] = kDefaultDecMaxM;
     r[2] = 1;
     r[3] = 0;

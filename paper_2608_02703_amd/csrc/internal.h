@@ -138,7 +138,8 @@ bool use_mid(const archead_handle* h, int64_t M);
 // Where the several-token kernel applies, the MFMA decode kernel keeps the M
 // it serves in one pass and the several-token kernel takes over from there
 // up to kDefaultMidMaxM (measured crossovers); otherwise the decode kernel
-// keeps 3 .. kDefaultDecMaxM.
+// keeps its first M .. kDefaultDecMaxM.  Its first M is 2 on heads with
+// d >= 4096 and both ranks at most 64, else kDefaultDecMinM.
 void default_ranges(const archead_desc& d, int64_t (&r)[4]);
 
 // The kernel a call with M tokens runs on: the MFMA decode kernel, the

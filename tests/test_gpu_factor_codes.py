@@ -170,7 +170,7 @@ def test_qwen_g64_fp16_scales_gemv():
     """A Qwen-shaped head with groups of 64 and fp16 scales (the reading of
     the paper's Gemma storage figure): 64 group scales per row take 32-lane
     segments on the decode GEMV, and the MFMA decode kernels read the groups
-    in pairs.  Sampled columns at M = 1, 2 (GEMV), 8, 16 (k_dec) and 32."""
+    in pairs.  Sampled columns at M = 1 (GEMV), 2, 8, 16 (k_dec) and 32."""
     from paper_2608_02703_amd import PackedHead
     h = make_head("qwen_decode", g=64)
     ph = PackedHead.from_arrays(h)
