@@ -302,8 +302,13 @@ PrepLayout prep_layout(const archead_handle* h) {
 // (floor, per-wave lists, wave-ordered merge).
 static hipError_t launch_topk_merge(int64_t n_part, int k, int64_t rows, void** args,
                                     hipStream_t s) {
+  // four waves while they hold every candidate (a round's barrier and
+  // cross-wave step are cheaper), else sixteen
+  if (n_part * k <= int64_t(256) * kTopKMergeC)
+    return hipLaunchKernel(kern::topk_merge(256), dim3(unsigned(rows)), dim3(256), args, 0, s);
   if (n_part * k <= int64_t(kTopKMergeBlock) * kTopKMergeC)
-    return hipLaunchKernel(kern::topk_merge(), dim3(unsigned(rows)), dim3(kTopKMergeBlock), args, 0, s);
+    return hipLaunchKernel(kern::topk_merge(kTopKMergeBlock), dim3(unsigned(rows)),
+                           dim3(kTopKMergeBlock), args, 0, s);
   return hipLaunchKernel(kern::topk_merge_scan(), dim3(unsigned(rows)), dim3(kBlock), args, 0, s);
 }
 

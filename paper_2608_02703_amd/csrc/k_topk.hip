@@ -64,28 +64,117 @@ __device__ __forceinline__ void tk_scan(int64_t lo, int64_t hi, Val val, Idx idx
   }
 }
 
+__device__ __forceinline__ void tk_pick(float& bv, int& bi, float ov, int oi) {
+  const bool t = tk_better(ov, oi, bv, bi);
+  bv = t ? ov : bv;
+  bi = t ? oi : bi;
+}
+template <int CTRL>
+__device__ __forceinline__ void tk_pick_dpp(float& v, int& i) {
+  const float ov = dpp_swap<CTRL>(v);
+  const int oi = __builtin_amdgcn_update_dpp(0, i, CTRL, 0xF, 0xF, false);
+  tk_pick(v, i, ov, oi);
+}
+// the best pair of each row of 16 lanes, in every lane of the row
+__device__ __forceinline__ void tk_row16_best(float& v, int& i) {
+  tk_pick_dpp<0xB1>(v, i);
+  tk_pick_dpp<0x4E>(v, i);
+  tk_pick_dpp<0x141>(v, i);
+  tk_pick_dpp<0x140>(v, i);
+}
+
 // Per (partial p, token m) of grid (n_part, M): the k best pairs of
 // logits[m, v] over the slice v in [p * slice, min(V, (p + 1) * slice)),
-// into pv / pi [M][n_part][k]; the workgroup's four lists are merged.
+// into pv / pi [M][n_part][k].
+//  * For k <= 16, a floor first: each lane's best logit of the slice (its
+//    share: v = lo + tid, lo + tid + kBlock, ...), then k rounds of the
+//    wave's best among those (the owner drops it after each): the k-th is
+//    ranked at or below the wave's own k-th best (k lanes hold one at least
+//    as good), so the wave's list only sees candidates at or above it.
+//  * The four wave lists then merge by rank (distinct indices: every entry
+//    has a distinct rank), not by inserting one list into another.
 __global__ __launch_bounds__(kBlock) void k_topk_rows(const float* logits, int64_t ldl, int64_t V,
                                                       int k, int64_t slice, float* pv, int* pi) {
   __shared__ float sv[kWaves * 64];
   __shared__ int si[kWaves * 64];
-  const int lane = threadIdx.x & 63;
+  __shared__ float ov[kTopKMax];
+  __shared__ int oi[kTopKMax];
+  const int tid = threadIdx.x, lane = tid & 63;
   const int wid = __builtin_amdgcn_readfirstlane(int(threadIdx.x >> 6));
   const int64_t m = blockIdx.y, p = blockIdx.x, n_part = gridDim.x;
   const int64_t lo = p * slice;
   const int64_t hi = lo + slice < V ? lo + slice : V;
   const float* row = logits + m * ldl;
+  float fv = -INFINITY;
+  int fi = kNoIdx;
+  if (k <= 16) {
+    float cv = -INFINITY;
+    int ci = kNoIdx;
+    for (int64_t j0 = lo + tid; j0 < hi; j0 += int64_t(kScanBatch) * kBlock) {
+      float v[kScanBatch];
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        const int64_t j = j0 + int64_t(u) * kBlock;
+        v[u] = j < hi ? row[j] : -INFINITY;
+      }
+#pragma unroll
+      for (int u = 0; u < kScanBatch; ++u) {
+        const int64_t j = j0 + int64_t(u) * kBlock;
+        if (j < hi) tk_pick(cv, ci, v[u], int(j));
+      }
+    }
+    for (int r = 0; r < k; ++r) {
+      float gv = cv;
+      int gi = ci;
+      tk_row16_best(gv, gi);
+      float bv = rlane_f(gv, 0);
+      int bi = __builtin_amdgcn_readlane(gi, 0);
+#pragma unroll
+      for (int rr = 1; rr < 4; ++rr)
+        tk_pick(bv, bi, rlane_f(gv, 16 * rr), __builtin_amdgcn_readlane(gi, 16 * rr));
+      fv = bv;
+      fi = bi;
+      if (bi != kNoIdx && ci == bi) {
+        cv = -INFINITY;
+        ci = kNoIdx;
+      }
+    }
+  }
   float lv = -INFINITY, bv = -INFINITY;
   int li = kNoIdx, bi = kNoIdx;
   tk_scan(lo, hi, [&](int64_t j) { return row[j]; }, [&](int64_t j) { return int(j); }, lane, wid,
-          k, lv, li, bv, bi);
-  tk_block_merge<kWaves>(lv, li, bv, bi, lane, wid, k, sv, si);
-  if (wid == 0 && lane < k) {
-    const int64_t o = (m * n_part + p) * k + lane;
-    pv[o] = lv;
-    pi[o] = li;
+          k, lv, li, bv, bi, fv, fi);
+  sv[tid] = lv;
+  si[tid] = li;
+  if (tid < kTopKMax) {
+    ov[tid] = -INFINITY;
+    oi[tid] = kNoIdx;
+  }
+  __syncthreads();
+  if (lane < k && li != kNoIdx) {
+    int rank = lane;
+    int top = 1;
+    while (top * 2 <= k) top *= 2;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w == wid) continue;
+      const float* lw = sv + w * 64;
+      const int* iw = si + w * 64;
+      int pos = 0;
+      for (int step = top; step > 0; step >>= 1)
+        if (pos + step <= k && tk_better(lw[pos + step - 1], iw[pos + step - 1], lv, li)) pos += step;
+      rank += pos;
+    }
+    if (rank < k) {
+      ov[rank] = lv;
+      oi[rank] = li;
+    }
+  }
+  __syncthreads();
+  if (tid < k) {
+    const int64_t o = (m * n_part + p) * k + tid;
+    pv[o] = ov[tid];
+    pi[o] = oi[tid];
   }
 }
 
@@ -143,32 +232,15 @@ __global__ __launch_bounds__(kBlock) void k_topk_merge_scan(const float* pv, con
 // then the waves through LDS), writes it out, and its owner (indices are
 // distinct across the partial lists) drops it and takes its next best.  The
 // cost is k rounds, whatever the values.
-constexpr int kMergeBlock = 1024, kMergeWaves = kMergeBlock / 64, kMergeC = 8;
-static_assert(kMergeBlock == archead::kTopKMergeBlock && kMergeC == archead::kTopKMergeC,
+constexpr int kMergeC = 8;
+static_assert(archead::kTopKMergeBlock == 1024 && kMergeC == archead::kTopKMergeC,
               "host and kernel agree on the merge workgroup");
 
-__device__ __forceinline__ void tk_pick(float& bv, int& bi, float ov, int oi) {
-  const bool t = tk_better(ov, oi, bv, bi);
-  bv = t ? ov : bv;
-  bi = t ? oi : bi;
-}
-template <int CTRL>
-__device__ __forceinline__ void tk_pick_dpp(float& v, int& i) {
-  const float ov = dpp_swap<CTRL>(v);
-  const int oi = __builtin_amdgcn_update_dpp(0, i, CTRL, 0xF, 0xF, false);
-  tk_pick(v, i, ov, oi);
-}
-// the best pair of each row of 16 lanes, in every lane of the row
-__device__ __forceinline__ void tk_row16_best(float& v, int& i) {
-  tk_pick_dpp<0xB1>(v, i);
-  tk_pick_dpp<0x4E>(v, i);
-  tk_pick_dpp<0x141>(v, i);
-  tk_pick_dpp<0x140>(v, i);
-}
-
+template <int kMergeBlock>
 __global__ __launch_bounds__(kMergeBlock) void k_topk_merge(const float* pv, const int* pi,
                                                             int64_t n_part, int k, float* vals,
                                                             int64_t* idx, int64_t ldk) {
+  constexpr int kMergeWaves = kMergeBlock / 64;
   __shared__ float wv[2][kMergeWaves];
   __shared__ int wi[2][kMergeWaves];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -239,7 +311,10 @@ const void* gemv_topk(int lpr, bool sc8, int gen) {
 }
 
 const void* topk_rows() { return reinterpret_cast<const void*>(k_topk_rows); }
-const void* topk_merge() { return reinterpret_cast<const void*>(k_topk_merge); }
+const void* topk_merge(int block) {
+  return block == 256 ? reinterpret_cast<const void*>(k_topk_merge<256>)
+                      : reinterpret_cast<const void*>(k_topk_merge<1024>);
+}
 const void* topk_merge_scan() { return reinterpret_cast<const void*>(k_topk_merge_scan); }
 
 }  // namespace kern

@@ -16,7 +16,7 @@ const void* gemv(int tok, int lpr, bool ce, bool sc8, int gen);
 // of fp32 logits and the merge of per-partial top-k lists
 const void* gemv_topk(int lpr, bool sc8, int gen);
 const void* topk_rows();
-const void* topk_merge();        // k rounds, at most kTopKMergeBlock * kTopKMergeC candidates
+const void* topk_merge(int block);   // k rounds; workgroups of 256 or kTopKMergeBlock threads, kTopKMergeC candidates each
 const void* topk_merge_scan();   // any number of candidates
 // MFMA decode kernel k_dec<GW, CE, EK, SC8, GEN>: gw = g / 32 code words per
 // lane and group (1, 2, 4), ek expansion K-chunks held (2 or 4), gen as for
