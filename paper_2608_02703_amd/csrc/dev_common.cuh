@@ -562,6 +562,46 @@ __device__ __forceinline__ void tk_offer(float& lv, int& li, float& bv, int& bi,
   }
 }
 
+// Merge the sorted lists of a workgroup's NW waves by rank: the entry in
+// lane j of wave w has j better entries in its own list and, in each other
+// list, as many as a binary search finds; entries have distinct indices, so
+// every one has a distinct rank, and those ranked below k land in (ov, oi)
+// [k] (slots no entry reaches hold the empty entry).  sv / si: LDS of NW *
+// 64 entries; ov / oi: LDS of kTopKMax.  Contains two barriers: every
+// thread of the workgroup calls it.
+template <int NW>
+__device__ __forceinline__ void tk_rank_merge(float lv, int li, int tid, int k, float* sv, int* si,
+                                              float* ov, int* oi) {
+  const int lane = tid & 63, wid = tid >> 6;
+  sv[tid] = lv;
+  si[tid] = li;
+  if (tid < kTopKMax) {
+    ov[tid] = -INFINITY;
+    oi[tid] = kNoIdx;
+  }
+  __syncthreads();
+  if (lane < k && li != kNoIdx) {
+    int rank = lane;
+    int top = 1;
+    while (top * 2 <= k) top *= 2;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      if (w == wid) continue;
+      const float* lw = sv + w * 64;
+      const int* iw = si + w * 64;
+      int pos = 0;
+      for (int step = top; step > 0; step >>= 1)
+        if (pos + step <= k && tk_better(lw[pos + step - 1], iw[pos + step - 1], lv, li)) pos += step;
+      rank += pos;
+    }
+    if (rank < k) {
+      ov[rank] = lv;
+      oi[rank] = li;
+    }
+  }
+  __syncthreads();
+}
+
 // Merge the lists of a workgroup's NW waves into wave 0's (the other waves'
 // lists are inserted in wave order; each is sorted, so its first entry
 // that fails the bar ends it).  sv / si: LDS of NW * 64 entries.  Contains

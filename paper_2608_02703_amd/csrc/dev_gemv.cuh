@@ -690,20 +690,21 @@ void k_gemv(GemvArgs a) {
     }
   }
   if constexpr (TK) {
-    // the waves' lists merged into wave 0's, which leaves them as this
-    // workgroup's partial
+    // the waves' lists merged by rank into this workgroup's partial
     __shared__ float tks_v[kWaves * 64];
     __shared__ int tks_i[kWaves * 64];
+    __shared__ float tko_v[kTopKMax];
+    __shared__ int tko_i[kTopKMax];
+    const int tid = int(threadIdx.x);
 #pragma unroll
     for (int tt = 0; tt < TOK; ++tt) {
-      if (tt) __syncthreads();
-      tk_block_merge<kWaves>(ce.tv[tt], ce.ti[tt], ce.bv[tt], ce.bi[tt], lane, wid, a.tk_k, tks_v,
-                             tks_i);
-      if (wid == 0 && lane < a.tk_k) {
-        const int64_t o = ((a.tok0 + tt) * a.n_part + (blockIdx.x - a.n_prod_blocks)) * a.tk_k + lane;
-        a.tk_val[o] = ce.tv[tt];
-        a.tk_idx[o] = ce.ti[tt];
+      tk_rank_merge<kWaves>(ce.tv[tt], ce.ti[tt], tid, a.tk_k, tks_v, tks_i, tko_v, tko_i);
+      if (tid < a.tk_k) {
+        const int64_t o = ((a.tok0 + tt) * a.n_part + (blockIdx.x - a.n_prod_blocks)) * a.tk_k + tid;
+        a.tk_val[o] = tko_v[tid];
+        a.tk_idx[o] = tko_i[tid];
       }
+      __syncthreads();
     }
   }
 }

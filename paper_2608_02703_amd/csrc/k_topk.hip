@@ -144,33 +144,7 @@ __global__ __launch_bounds__(kBlock) void k_topk_rows(const float* logits, int64
   int li = kNoIdx, bi = kNoIdx;
   tk_scan(lo, hi, [&](int64_t j) { return row[j]; }, [&](int64_t j) { return int(j); }, lane, wid,
           k, lv, li, bv, bi, fv, fi);
-  sv[tid] = lv;
-  si[tid] = li;
-  if (tid < kTopKMax) {
-    ov[tid] = -INFINITY;
-    oi[tid] = kNoIdx;
-  }
-  __syncthreads();
-  if (lane < k && li != kNoIdx) {
-    int rank = lane;
-    int top = 1;
-    while (top * 2 <= k) top *= 2;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w) {
-      if (w == wid) continue;
-      const float* lw = sv + w * 64;
-      const int* iw = si + w * 64;
-      int pos = 0;
-      for (int step = top; step > 0; step >>= 1)
-        if (pos + step <= k && tk_better(lw[pos + step - 1], iw[pos + step - 1], lv, li)) pos += step;
-      rank += pos;
-    }
-    if (rank < k) {
-      ov[rank] = lv;
-      oi[rank] = li;
-    }
-  }
-  __syncthreads();
+  tk_rank_merge<kWaves>(lv, li, tid, k, sv, si, ov, oi);
   if (tid < k) {
     const int64_t o = (m * n_part + p) * k + tid;
     pv[o] = ov[tid];
