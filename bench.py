@@ -479,7 +479,7 @@ def sweep(steps, cfg="sweep128k", Ms=None, paths=("auto", "dec", "mid", "gemv", 
     heads = upload_copies(h, 3)
     pbytes = lib_packed_bytes(heads[0])
     if pbytes > 400e6:
-        heads.pop().close()                  # two copies already exceed the cache   # copies exceed the 256 MB Infinity Cache
+        heads.pop().close()    # two copies already exceed the 256 MB Infinity Cache
     for hd in heads:
         hd.prepare()
     Ms = Ms or CONFIGS[cfg]["Ms"]
