@@ -655,6 +655,38 @@ def test_argmax_ties_take_the_smallest_index(path):
     ph.close()
 
 
+@pytest.mark.parametrize("cfg", ["tiny", "qwen_decode"])
+def test_argmax_one_launch_gemv_any_workspace_contents(cfg):
+    """1 to 4 tokens on the GEMV (one head pass, then the partials' merge):
+    over a workspace holding the previous call's leftovers, all ones, or in
+    every 64-bit word a foreign call stamp with a partial count, each call
+    gives the first-index argmax of the same kernel's fp32 logits and their
+    maximum, bit for bit."""
+    from paper_2608_02703_amd.archead import OP_ARGMAX
+    ph = packed(cfg)
+    x = make_x(cfg, max(4, max(CONFIGS[cfg]["Ms"])))
+    foreign = (0x5A5A5A5A << 32) | 7
+    ph.force_path("gemv")
+    try:
+        for M in (1, 2, 3, 4, 1):
+            lg = gpu_logits(ph, x[:M])
+            xt = torch_x(x[:M])
+            for fill in ("leftover", "ones", "foreign"):
+                say(f"argmax on the GEMV {cfg} M={M} workspace {fill}")
+                ws = ph.workspace(M, OP_ARGMAX, xt.device)
+                if fill == "ones":
+                    ws.fill_(0xFF)
+                elif fill == "foreign":
+                    ws.view(torch.int64).fill_(foreign)
+                idx, mx = ph.logits_argmax(xt, ws=ws)
+                torch.cuda.synchronize()
+                idx, mx = idx.cpu().numpy(), mx.cpu().numpy()
+                assert np.array_equal(idx, np.argmax(lg, axis=1)), f"M={M} {fill}: argmax differs"
+                assert np.array_equal(mx, lg.max(axis=1)), f"M={M} {fill}: max differs"
+    finally:
+        ph.force_path("auto")
+
+
 def test_argmax_gemma_m64_against_oracle():
     """The Gemma-shaped workload with 64 tokens (logits + argmax), through the
     library's own kernel choice: the fused argmax equals the oracle's on
