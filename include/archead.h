@@ -204,7 +204,7 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *            ARCHEAD_OP_LOGITS), 256-byte aligned; its contents on entry do
  *            not matter
  *   stream   hipStream_t to launch on (NULL = the default stream)
- * M == 0 returns ARCHEAD_OK without launching.  Three kernels serve the
+ * M == 0 returns ARCHEAD_OK without launching.  Four kernels serve the
  * call, chosen by M and the head shape:
  *   - M in the range of archead_set_dec_range (default from 2 where
  *     d >= 4096 and r_c, r_r <= 64, else from 3; to 32, or to the tokens it
@@ -225,9 +225,9 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  * (a few leading workgroups publish t with a per-call stamp in the
  * workspace; the others wait for it a bounded time and otherwise compute it
  * themselves), so a decode step is a single kernel launch;
- *   - otherwise the tiled bf16 MFMA kernel (tiles of 128 tokens x 256
- *     vocabulary rows, two workgroups per CU, up to M = 1024; 256 x 256
- *     tiles above; its head-derived tables are built per call unless
+ *   - otherwise the tiled bf16 MFMA kernel (tiles of 64 tokens x 256
+ *     vocabulary rows, three workgroups per CU, up to M = 64; 128 x 256,
+ *     two workgroups per CU, up to M = 1024; 256 x 256 tiles above; its head-derived tables are built per call unless
  *     archead_prepare keeps them).
  * All produce fp32 logits from fp32 accumulation.  The tiled kernel carries
  * its accumulator in units of the current scale group's scale and feeds the
